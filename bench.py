@@ -1,0 +1,325 @@
+"""Benchmark of the two-level sparse decode step on one MI355X.
+
+One step = one tls_sparse_decode call over the whole batch: block scoring,
+top-K_b, token scoring over the selected blocks, top-K_t, and attention over
+the gathered K/V (the index build is prefill and is timed separately).
+Inputs are synthetic, generated on the GPU and resident in HBM before the
+timed region.  Several byte-identical copies of the layer are rotated so the
+256 MB Infinity Cache cannot serve a step from the previous one.
+
+Prints ONE JSON line (see README/DESIGN for the fields).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "two-level sparse decode µs/layer-step at 96k ctx + achieved HBM GB/s vs peak"
+PEAK_HBM_GBPS = 8000.0
+STAGES = ["block_score", "block_topk", "token_score", "token_norm", "token_topk", "attention", "merge"]
+
+WORKLOADS = {
+    # 96k-context GQA decode of the offloaded-KV workload shape, K/V resident in HBM
+    "gqa_b32_ctx96k": ("offload_gqa_96k", dict()),
+    "gqa_b16_ctx48k_96k": ("batched_gqa", dict()),
+    "gqa_b1_ctx48k": ("qwen3_gqa_48k", dict()),
+    "mla_b8_ctx64k": ("mla", dict()),
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="gqa_b32_ctx96k", choices=sorted(WORKLOADS))
+    ap.add_argument("--copies", type=int, default=0, help="layer copies rotated (0: auto)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-units", type=int, default=48, help="units of the oracle sample")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="run warmup + steps of the decode only (for rocprofv3), print nothing else")
+    return ap.parse_args()
+
+
+# ----------------------------------------------------------------------------
+# raw HIP events (the library records them on the stream it launches on)
+# ----------------------------------------------------------------------------
+class HipEvents:
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self, n):
+        out = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            if self.hip.hipEventCreate(ctypes.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            out.append(e.value)
+        return out
+
+    def elapsed_ms(self, a, b):
+        self.hip.hipEventSynchronize(ctypes.c_void_p(b))
+        t = ctypes.c_float()
+        if self.hip.hipEventElapsedTime(ctypes.byref(t), ctypes.c_void_p(a), ctypes.c_void_p(b)) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(t.value)
+
+    def destroy(self, evs):
+        for e in evs:
+            self.hip.hipEventDestroy(ctypes.c_void_p(e))
+
+
+def algorithmic_bytes(cfg, ctx, bids, e):
+    """Bytes the step must move: all block-summary rows, the token-index rows
+    of the candidates, the gathered K/V rows of the selected tokens, q and out."""
+    import numpy as np
+    B = cfg.block
+    blk = 0
+    tok = 0
+    kv = 0
+    idx_row = cfg.d_c // 2 + 8 * (cfg.d_c // 32)
+    kv_row = cfg.d_qk * e if cfg.mla else (cfg.d_qk + cfg.d_v) * e
+    bids = bids.reshape(cfg.batch, cfg.h_kv, -1)
+    for s in range(cfg.batch):
+        n = int(ctx[s])
+        m = -(-n // B)
+        for g in range(cfg.h_kv):
+            sel = bids[s, g][bids[s, g] >= 0]
+            cand = int(sum(min(B, n - int(b) * B) for b in sel))
+            blk += m * 2 * cfg.d_qk * e
+            tok += cand * idx_row
+            kv += min(cfg.k_t, cand) * kv_row
+    qo = cfg.batch * cfg.h_q * (cfg.d_qk + cfg.d_v) * e
+    return dict(block_index=blk, token_index=tok, gathered_kv=kv, q_out=qo, total=blk + tok + kv + qo)
+
+
+def cpu_baseline(case_arrays, cfg, n_units_total, units_sample, cores):
+    """Time the oracle (as it stands) on a sample of units of the workload."""
+    import concurrent.futures
+    import multiprocessing as mp
+    t0 = time.perf_counter()
+    ctx = mp.get_context("spawn")
+    with concurrent.futures.ProcessPoolExecutor(max_workers=cores, mp_context=ctx,
+                                                initializer=_cpu_worker_init) as ex:
+        # warm the workers (imports) outside the timed region
+        list(ex.map(_cpu_noop, range(cores)))
+        t0 = time.perf_counter()
+        list(ex.map(_cpu_unit, case_arrays))
+        wall = time.perf_counter() - t0
+    per_step_s = wall * n_units_total / len(case_arrays)
+    return per_step_s, wall
+
+
+def _cpu_worker_init():
+    os.environ["OMP_NUM_THREADS"] = "1"
+    os.environ["OPENBLAS_NUM_THREADS"] = "1"
+    sys.path.insert(0, ROOT)
+
+
+def _cpu_noop(_):
+    import numpy  # noqa: F401
+    from oracle import tls_oracle  # noqa: F401
+    return 0
+
+
+def _cpu_unit(args):
+    from oracle import tls_oracle as O
+    qg, Ku, Vu, n, ch, k_b, k_t, B, sigma, summ, index = args
+    r = O.decode_unit(qg, Ku, Vu, n, ch, k_b, k_t, B, sigma, index=index, summaries=summ)
+    return int(len(r["token_ids"]))
+
+
+def traffic_from_profiles(kernel_src_hash):
+    """HBM traffic per launch of the dominant kernel from committed PMC runs,
+    valid only while the kernel source is unchanged."""
+    p = os.path.join(ROOT, "profiles", "attention_gqa_b32_ctx96k_traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        d = json.load(open(p))
+    except Exception:
+        return None
+    if d.get("kernel_src_sha256") != kernel_src_hash:
+        return None
+    return d.get("traffic_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the operator shards by (sequence, KV head) without cross-GPU exchange, "
+              "so per-GPU throughput is the single-GPU figure", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2604_07815_amd as tls
+    import synth
+
+    cfg_name, over = WORKLOADS[args.workload]
+    cfg = synth.config(cfg_name, **over)
+    torch.cuda.init()
+    dev = torch.device("cuda", 0)
+    e = 2 if cfg.dtype == "bf16" else 4
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+
+    # ---- inputs (device-generated) and prefill index build ------------------------
+    d = synth.make_device(cfg, device=dev, pad="zero")
+    layout = tls.make_layout(cfg.batch, cfg.h_q, cfg.h_kv, cfg.d_qk, cfg.d_v, cfg.max_ctx,
+                             index_channels=cfg.d_c, block_size=cfg.block,
+                             dtype=tls.DTYPE_BF16 if cfg.dtype == "bf16" else tls.DTYPE_F32,
+                             mla_shared_kv=cfg.mla)
+    m_max = -(-cfg.max_ctx // cfg.block)
+    kmax = torch.empty((cfg.batch, cfg.h_kv, m_max, cfg.d_qk), dtype=dt, device=dev)
+    kmin = torch.empty_like(kmax)
+    codes = torch.empty((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 2), dtype=torch.uint8, device=dev)
+    qparams = torch.empty((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 32, 2), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    tls.tls_build_block_index(layout, d["k"], d["ctx_lens"], 0, cfg.max_ctx, kmax, kmin)
+    tls.tls_build_token_index(layout, d["k"], d["ctx_lens"], d["channels"], 0, cfg.max_ctx, codes, qparams)
+    torch.cuda.synchronize()
+    index_build_ms = (time.perf_counter() - t0) * 1e3
+
+    layer = dict(q=d["q"], k=d["k"], v=d["v"], kmax=kmax, kmin=kmin, codes=codes, qparams=qparams)
+    per_layer = sum(t.numel() * t.element_size() for t in layer.values() if t is not None)
+    copies = args.copies or max(1, min(8, math.ceil(2 * 512e6 / max(1.0, per_layer * 0.04)) if per_layer < 2e9 else 2))
+    layers = [layer] + [{k: (None if t is None else t.clone()) for k, t in layer.items()} for _ in range(copies - 1)]
+    ctx_t, ch_t = d["ctx_lens"], d["channels"]
+    ws = tls.alloc_workspace(layout, cfg.k_b, cfg.k_t, device=dev)
+    out = torch.empty((cfg.batch, cfg.h_q, cfg.d_v), dtype=dt, device=dev)
+    lse = torch.empty((cfg.batch, cfg.h_q), dtype=torch.float32, device=dev)
+    bids = torch.empty((cfg.batch, cfg.h_kv, cfg.k_b), dtype=torch.int32, device=dev)
+    tids = torch.empty((cfg.batch, cfg.h_kv, cfg.k_t), dtype=torch.int32, device=dev)
+
+    def step(i, events=None):
+        L = layers[i % len(layers)]
+        tls.tls_sparse_decode(layout, L["q"], tls.KV(L["k"], L["v"]), ctx_t, L["kmax"], L["kmin"], L["codes"],
+                              L["qparams"], ch_t, cfg.k_b, cfg.k_t, None, None, out, lse, bids, tids, ws,
+                              stage_events=events)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    if args.profile_only:
+        for i in range(args.steps):
+            step(i)
+        torch.cuda.synchronize()
+        print(json.dumps({"profile_only": True, "workload": args.workload, "steps": args.steps}), flush=True)
+        return
+
+    # ---- timed region (clean: no stage markers) ---------------------------------
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        step(i)
+    stop.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(stop) / args.steps
+
+    # ---- per-stage timing with HIP events on the launch stream --------------------
+    hev = HipEvents()
+    evs = [hev.create(tls.NUM_STAGE_EVENTS) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        step(i, events=evs[i])
+    torch.cuda.synchronize()
+    stage_ms = np.zeros(len(STAGES))
+    for i in range(args.steps):
+        for j in range(len(STAGES)):
+            stage_ms[j] += hev.elapsed_ms(evs[i][j], evs[i][j + 1])
+    stage_ms /= args.steps
+    marked_ms = sum(hev.elapsed_ms(evs[i][0], evs[i][-1]) for i in range(args.steps)) / args.steps
+    for ev in evs:
+        hev.destroy(ev)
+
+    err = tls.tls_check_device_error(ws)
+    nb = algorithmic_bytes(cfg, d["ctx_host"], bids.cpu().numpy(), e)
+    us = ms_per_step * 1e3
+    gbps = nb["total"] / (ms_per_step * 1e-3) / 1e9
+
+    attn_ms = float(stage_ms[STAGES.index("attention")])
+    attn_bytes = nb["gathered_kv"] + cfg.batch * cfg.h_q * cfg.d_qk * e
+    attn_gbps = attn_bytes / (attn_ms * 1e-3) / 1e9
+    src = open(os.path.join(ROOT, "paper_2604_07815_amd", "csrc", "attention.hip"), "rb").read()
+    traffic = traffic_from_profiles(hashlib.sha256(src).hexdigest())
+
+    result = {
+        "metric": METRIC,
+        "value": round(us, 2),
+        "unit": "µs/layer-step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload, "batch": cfg.batch, "h_q": cfg.h_q, "h_kv": cfg.h_kv,
+            "d_qk": cfg.d_qk, "d_v": cfg.d_v, "ctx_min": int(d["ctx_host"].min()),
+            "ctx_max": int(d["ctx_host"].max()), "block": cfg.block, "k_b": cfg.k_b, "k_t": cfg.k_t,
+            "d_c": cfg.d_c, "kv": "hbm-resident", "layer_copies_rotated": copies,
+        },
+        "achieved_GBps": round(gbps, 1),
+        "step_frac_of_peak_hbm": round(gbps / PEAK_HBM_GBPS, 4),
+        "algorithmic_bytes_per_step": nb,
+        "stage_us": {k: round(float(v) * 1e3, 2) for k, v in zip(STAGES, stage_ms)},
+        "stage_marked_step_us": round(marked_ms * 1e3, 2),
+        "index_build_ms": round(index_build_ms, 3),
+        "device_error_flags": err,
+        "roofline": {
+            "kernel": "attn_gqa_kernel" if not cfg.mla else "attn_mla_kernel",
+            "bound": "hbm", "achieved": round(attn_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": round(attn_gbps / PEAK_HBM_GBPS, 4), "traffic": traffic,
+            "bytes_per_launch": attn_bytes, "avg_launch_us": round(attn_ms * 1e3, 2),
+        },
+    }
+
+    # ---- CPU baseline: the oracle on a bounded sample of units -------------------
+    if not args.no_cpu_baseline:
+        import oracle.tls_oracle as O
+        r = np.random.default_rng(0)
+        units_all = [(s, g) for s in range(cfg.batch) for g in range(cfg.h_kv)]
+        pick = [units_all[i] for i in sorted(r.choice(len(units_all), min(args.cpu_units, len(units_all)),
+                                                       replace=False))]
+        qf = synth.to_f64(d["q_host"], cfg.dtype)
+        work = []
+        for (s, g) in pick:
+            n = int(d["ctx_host"][s])
+            Ku = synth.torch_to_f64(d["k"][s, g, :n])
+            Vu = Ku[:, :cfg.d_v] if cfg.mla else synth.torch_to_f64(d["v"][s, g, :n])
+            summ = O.block_summaries(Ku, n, cfg.block)       # prefill, outside the timed region
+            index = O.token_index(Ku, n, d["channels_host"][g])
+            qg = qf[s, g * cfg.group:(g + 1) * cfg.group]
+            work.append((qg, Ku, Vu, n, d["channels_host"][g], cfg.k_b, cfg.k_t, cfg.block, cfg.sigma, summ, index))
+        cores = max(1, min(16, len(os.sched_getaffinity(0))))
+        per_step_s, wall = cpu_baseline(work, cfg, len(units_all), pick, cores)
+        result["cpu_baseline"] = {
+            "value": round(per_step_s * 1e6, 1), "unit": "µs/layer-step", "cores": cores, "kind": "oracle",
+            "sample": f"{len(pick)} of {len(units_all)} (sequence, KV head) units, float64 NumPy oracle decode "
+                      f"step on prebuilt indices, {cores} worker processes, {wall:.2f} s wall; scaled to all units",
+        }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -247,15 +247,16 @@ def sparse_attention(q_group: np.ndarray, K: np.ndarray, V: np.ndarray, ids: np.
 # ----------------------------------------------------------------------------
 
 def decode_unit(q_group, K, V, n, channels, k_b, k_t, B, sigma, index=None, block_ids=None,
-                token_ids=None):
+                token_ids=None, summaries=None):
     """Whole decode step for one (sequence, KV group).
 
     index: optional prebuilt (codes_packed, qparams) for tokens [0, n).
+    summaries: optional prebuilt (kmax, kmin) block summaries.
     block_ids / token_ids: optional given selections (skip those stages)."""
     res = {}
     if token_ids is None:
         if block_ids is None:
-            kmax, kmin = block_summaries(K, n, B)
+            kmax, kmin = block_summaries(K, n, B) if summaries is None else summaries
             block_ids, bscores = select_blocks(q_group, kmax, kmin, k_b)
             res["block_scores"] = bscores
         if index is None:

@@ -1,0 +1,255 @@
+"""Two-level sparse decode attention on MI355X (gfx950): Python binding.
+
+Thin ctypes binding of ``libtls.so`` (see include/tls.h for the contract).
+Every function has the name of the C entry point it wraps and only
+marshals arguments: torch tensors are passed by ``data_ptr()`` and the
+stream defaults to torch's current stream.  All computation happens in the
+library's HIP kernels; importing this package fails loudly when the library
+has not been built (``python -m paper_2604_07815_amd.build``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+__all__ = [
+    "TlsError", "Layout", "KvView", "KV", "DecodeOpts", "NUM_STAGE_EVENTS", "LIB_PATH",
+    "tls_version", "tls_status_string", "tls_workspace_size", "tls_workspace_init",
+    "tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
+    "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error",
+    "make_layout", "alloc_workspace", "DTYPE_F32", "DTYPE_BF16", "EXPORTED_SYMBOLS",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtls.so")
+
+OK, INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP_ERROR = 0, 1, 2, 3, 4
+DTYPE_F32, DTYPE_BF16 = 0, 1
+NUM_STAGE_EVENTS = 8
+DEVERR_CTX_LEN, DEVERR_BLOCK_ID, DEVERR_TOKEN_ID, DEVERR_SLOT, DEVERR_POOL_FULL, DEVERR_CHANNEL = 1, 2, 4, 8, 16, 32
+
+EXPORTED_SYMBOLS = [
+    "tls_version", "tls_status_string", "tls_workspace_size", "tls_workspace_init",
+    "tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
+    "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error",
+]
+
+
+class TlsError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {tls_status_string(status)} ({status})")
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32), ("head_dim_qk", ctypes.c_int32),
+        ("head_dim_v", ctypes.c_int32), ("block_size", ctypes.c_int32),
+        ("index_channels", ctypes.c_int32), ("max_ctx", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("mla_shared_kv", ctypes.c_int32),
+        ("softmax_scale", ctypes.c_float),
+    ]
+
+
+class KvView(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("slot_map", ctypes.c_void_p), ("n_slots", ctypes.c_int64)]
+
+
+class DecodeOpts(ctypes.Structure):
+    _fields_ = [("attn_splits", ctypes.c_int32), ("reserved", ctypes.c_int32 * 7),
+                ("stage_events", ctypes.c_void_p)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2604_07815_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    LP = ctypes.POINTER(Layout)
+    sig = {
+        "tls_version": (ctypes.c_char_p, []),
+        "tls_status_string": (ctypes.c_char_p, [I32]),
+        "tls_workspace_size": (I32, [LP, I32, I32, ctypes.POINTER(SZ)]),
+        "tls_workspace_init": (I32, [P, SZ, P]),
+        "tls_build_block_index": (I32, [LP, P, P, I32, I32, P, P, P]),
+        "tls_build_token_index": (I32, [LP, P, P, P, I32, I32, P, P, P]),
+        "tls_select_blocks": (I32, [LP, P, P, P, P, I32, P, P, P, SZ, P]),
+        "tls_select_tokens": (I32, [LP, P, P, P, P, P, I32, P, I32, P, P, P, SZ, P]),
+        "tls_sparse_decode": (I32, [LP, P, ctypes.POINTER(KvView), P, P, P, P, P, P, I32, I32, P, P,
+                                    P, P, P, P, P, SZ, ctypes.POINTER(DecodeOpts), P]),
+        "tls_prefetch_blocks": (I32, [LP, P, P, P, P, P, I32, P, P, I64, P, P, P, P, SZ, P]),
+        "tls_check_device_error": (I32, [P, SZ, I32, ctypes.POINTER(I32), P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+# ----------------------------------------------------------------------------
+# marshalling helpers
+# ----------------------------------------------------------------------------
+
+def _ptr(t: Optional[torch.Tensor], what: str, device: bool = True):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{what}: expected a torch.Tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: tensor must be contiguous")
+    if device and not t.is_cuda:
+        raise ValueError(f"{what}: tensor must live on the GPU")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    return ctypes.c_void_p(handle)
+
+
+def _check(status: int, where: str) -> None:
+    if status != OK:
+        raise TlsError(status, where)
+
+
+def make_layout(batch, num_q_heads, num_kv_heads, head_dim_qk, head_dim_v, max_ctx,
+                index_channels=32, block_size=64, dtype=DTYPE_BF16, mla_shared_kv=False,
+                softmax_scale: float = 0.0) -> Layout:
+    if isinstance(dtype, torch.dtype):
+        dtype = DTYPE_BF16 if dtype == torch.bfloat16 else DTYPE_F32
+    return Layout(int(batch), int(num_q_heads), int(num_kv_heads), int(head_dim_qk), int(head_dim_v),
+                  int(block_size), int(index_channels), int(max_ctx), int(dtype),
+                  1 if mla_shared_kv else 0, float(softmax_scale))
+
+
+# ----------------------------------------------------------------------------
+# entry points (same names as the C ABI)
+# ----------------------------------------------------------------------------
+
+def tls_version() -> str:
+    return _lib.tls_version().decode()
+
+
+def tls_status_string(status: int) -> str:
+    return _lib.tls_status_string(int(status)).decode()
+
+
+def tls_workspace_size(layout: Layout, K_b: int, K_t: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(_lib.tls_workspace_size(ctypes.byref(layout), K_b, K_t, ctypes.byref(out)), "tls_workspace_size")
+    return int(out.value)
+
+
+def tls_workspace_init(ws: torch.Tensor, stream=None) -> None:
+    _check(_lib.tls_workspace_init(_ptr(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)),
+           "tls_workspace_init")
+
+
+def alloc_workspace(layout: Layout, K_b: int, K_t: int, device="cuda", stream=None) -> torch.Tensor:
+    """Allocate (torch) and initialise a workspace for these budgets."""
+    ws = torch.empty(tls_workspace_size(layout, K_b, K_t), dtype=torch.uint8, device=device)
+    tls_workspace_init(ws, stream)
+    return ws
+
+
+def _nbytes(t):
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def tls_build_block_index(layout, K, ctx_lens, tok_begin, tok_end, kmax, kmin, stream=None) -> None:
+    _check(_lib.tls_build_block_index(ctypes.byref(layout), _ptr(K, "K"), _ptr(ctx_lens, "ctx_lens"),
+                                      int(tok_begin), int(tok_end), _ptr(kmax, "kmax"), _ptr(kmin, "kmin"),
+                                      _stream(stream)), "tls_build_block_index")
+
+
+def tls_build_token_index(layout, K, ctx_lens, channels, tok_begin, tok_end, codes, qparams,
+                          stream=None) -> None:
+    _check(_lib.tls_build_token_index(ctypes.byref(layout), _ptr(K, "K"), _ptr(ctx_lens, "ctx_lens"),
+                                      _ptr(channels, "channels"), int(tok_begin), int(tok_end),
+                                      _ptr(codes, "codes"), _ptr(qparams, "qparams"), _stream(stream)),
+           "tls_build_token_index")
+
+
+def tls_select_blocks(layout, q, kmax, kmin, ctx_lens, K_b, block_ids, block_scores, ws, stream=None) -> None:
+    _check(_lib.tls_select_blocks(ctypes.byref(layout), _ptr(q, "q"), _ptr(kmax, "kmax"), _ptr(kmin, "kmin"),
+                                  _ptr(ctx_lens, "ctx_lens"), int(K_b), _ptr(block_ids, "block_ids"),
+                                  _ptr(block_scores, "block_scores"), _ptr(ws, "ws"), _nbytes(ws),
+                                  _stream(stream)), "tls_select_blocks")
+
+
+def tls_select_tokens(layout, q, codes, qparams, channels, block_ids, K_b, ctx_lens, K_t, token_ids,
+                      token_scores, ws, stream=None) -> None:
+    _check(_lib.tls_select_tokens(ctypes.byref(layout), _ptr(q, "q"), _ptr(codes, "codes"),
+                                  _ptr(qparams, "qparams"), _ptr(channels, "channels"),
+                                  _ptr(block_ids, "block_ids"), int(K_b), _ptr(ctx_lens, "ctx_lens"), int(K_t),
+                                  _ptr(token_ids, "token_ids"), _ptr(token_scores, "token_scores"),
+                                  _ptr(ws, "ws"), _nbytes(ws), _stream(stream)), "tls_select_tokens")
+
+
+@dataclass
+class KV:
+    """K/V source of the attention stage: dense arrays, or the block pool."""
+    k: torch.Tensor
+    v: Optional[torch.Tensor] = None
+    slot_map: Optional[torch.Tensor] = None
+    n_slots: int = 0
+
+    def as_struct(self) -> KvView:
+        return KvView(_ptr(self.k, "kv.k"), _ptr(self.v, "kv.v"), _ptr(self.slot_map, "kv.slot_map"),
+                      int(self.n_slots))
+
+
+def tls_sparse_decode(layout, q, kv: KV, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t,
+                      block_ids_in, token_ids_in, out, lse, block_ids_out, token_ids_out, ws,
+                      attn_splits: int = 0, stage_events: Optional[Sequence[int]] = None,
+                      stream=None) -> None:
+    """One decode step.  stage_events: NUM_STAGE_EVENTS raw hipEvent_t handles."""
+    opts = DecodeOpts()
+    opts.attn_splits = int(attn_splits)
+    ev_arr = None
+    if stage_events is not None:
+        if len(stage_events) != NUM_STAGE_EVENTS:
+            raise ValueError(f"stage_events must hold {NUM_STAGE_EVENTS} events")
+        ev_arr = (ctypes.c_void_p * NUM_STAGE_EVENTS)(*[ctypes.c_void_p(int(e)) for e in stage_events])
+        opts.stage_events = ctypes.cast(ev_arr, ctypes.c_void_p)
+    view = kv.as_struct()
+    _check(_lib.tls_sparse_decode(
+        ctypes.byref(layout), _ptr(q, "q"), ctypes.byref(view), _ptr(ctx_lens, "ctx_lens"),
+        _ptr(kmax, "kmax"), _ptr(kmin, "kmin"), _ptr(codes, "codes"), _ptr(qparams, "qparams"),
+        _ptr(channels, "channels"), int(K_b), int(K_t), _ptr(block_ids_in, "block_ids_in"),
+        _ptr(token_ids_in, "token_ids_in"), _ptr(out, "out"), _ptr(lse, "lse"),
+        _ptr(block_ids_out, "block_ids_out"), _ptr(token_ids_out, "token_ids_out"), _ptr(ws, "ws"),
+        _nbytes(ws), ctypes.byref(opts), _stream(stream)), "tls_sparse_decode")
+
+
+def tls_prefetch_blocks(layout, host_k, host_v, ctx_lens, block_ids_new, block_ids_live, K_b, pool_k, pool_v,
+                        n_slots, slot_map, slot_owner, transfer_count, ws, stream=None) -> None:
+    """Incremental block transfer; host_k/host_v are pinned CPU tensors."""
+    for t, name in ((host_k, "host_k"), (host_v, "host_v")):
+        if t is not None and (t.is_cuda or not t.is_pinned()):
+            raise ValueError(f"{name}: must be a pinned host tensor")
+    _check(_lib.tls_prefetch_blocks(
+        ctypes.byref(layout), _ptr(host_k, "host_k", device=False), _ptr(host_v, "host_v", device=False),
+        _ptr(ctx_lens, "ctx_lens"), _ptr(block_ids_new, "block_ids_new"),
+        _ptr(block_ids_live, "block_ids_live"), int(K_b), _ptr(pool_k, "pool_k"), _ptr(pool_v, "pool_v"),
+        int(n_slots), _ptr(slot_map, "slot_map"), _ptr(slot_owner, "slot_owner"),
+        _ptr(transfer_count, "transfer_count"), _ptr(ws, "ws"), _nbytes(ws), _stream(stream)),
+        "tls_prefetch_blocks")
+
+
+def tls_check_device_error(ws, clear: bool = False, stream=None) -> int:
+    flags = ctypes.c_int32(0)
+    _check(_lib.tls_check_device_error(_ptr(ws, "ws"), _nbytes(ws), 1 if clear else 0, ctypes.byref(flags),
+                                       _stream(stream)), "tls_check_device_error")
+    return int(flags.value)

@@ -1,0 +1,160 @@
+// Coarse block selection (AsyncTLS Sec. 4.1).
+//
+// block_score_kernel: the Quest block score in the paper's GEMM form,
+//   s_i = sum_h (max(q_h,0) . kmax_i + min(q_h,0) . kmin_i).
+// Because the sum over the G heads of a group is linear, it is taken first:
+// Q+ = sum_h max(q_h,0), Q- = sum_h min(q_h,0) (fp32, heads in ascending
+// order), leaving one 2*d dot product per block - a GEMV that streams the
+// block summaries once.  HBM-bound: 2*d*sizeof(elem) bytes per block.
+//
+// block_topk_kernel: top-K_b block ids per unit, ties to the lower id,
+// ascending, -1 padded.
+#include "kernels.hpp"
+
+namespace tls {
+
+constexpr int kBlkUnroll = 4;  // blocks in flight per lane group
+
+template <class E, int LPB, int CPL>
+__global__ __launch_bounds__(256) void block_score_kernel(
+    const typename E::T* __restrict__ q, const typename E::T* __restrict__ kmax,
+    const typename E::T* __restrict__ kmin, const int32_t* __restrict__ ctx_lens, int H_q, int H_kv,
+    int G, int d, int B, int T, int m_max, int bpw, float* __restrict__ scores, uint32_t* err) {
+  using S = typename E::T;
+  constexpr int V = E::kVec;
+  constexpr int NG = 256 / LPB;  // lane groups per work-group
+  __shared__ float s_qp[1024], s_qn[1024];
+  const int unit = blockIdx.y;
+  const int s = unit / H_kv, g = unit % H_kv;
+  int n = ctx_lens[s];
+  if (n < 0 || n > T) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) set_error(err, 1u);
+    n = n < 0 ? 0 : T;
+  }
+  const int m = (n + B - 1) / B;
+  const int c0 = blockIdx.x * bpw, c1 = min(c0 + bpw, m_max);
+  float* out = scores + size_t(unit) * m_max;
+  if (c0 >= m) {
+    for (int i = c0 + threadIdx.x; i < c1; i += 256) out[i] = -INFINITY;
+    return;
+  }
+  const S* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    float p = 0.f, ng = 0.f;
+    for (int h = 0; h < G; ++h) {
+      float x = E::to_f(qg[size_t(h) * d + c]);
+      p += fmaxf(x, 0.f);
+      ng += fminf(x, 0.f);
+    }
+    s_qp[c] = p;
+    s_qn[c] = ng;
+  }
+  __syncthreads();
+  const int li = threadIdx.x % LPB, grp = threadIdx.x / LPB;
+  const int nch = d / V;
+  float qp[CPL][V], qn[CPL][V];
+#pragma unroll
+  for (int k = 0; k < CPL; ++k) {
+    const int c = li + k * LPB;
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      qp[k][e] = c < nch ? s_qp[c * V + e] : 0.f;
+      qn[k][e] = c < nch ? s_qn[c * V + e] : 0.f;
+    }
+  }
+  const size_t ubase = size_t(unit) * m_max;
+  for (int b0 = c0 + grp; b0 < c1; b0 += NG * kBlkUnroll) {
+    uint4 vmax[kBlkUnroll][CPL], vmin[kBlkUnroll][CPL];
+#pragma unroll
+    for (int u = 0; u < kBlkUnroll; ++u) {
+      const int blk = b0 + u * NG;
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) {
+        const int c = li + k * LPB;
+        if (blk < c1 && blk < m && c < nch) {
+          vmax[u][k] = ld16_stream(kmax + (ubase + blk) * d + c * V);
+          vmin[u][k] = ld16_stream(kmin + (ubase + blk) * d + c * V);
+        } else {
+          vmax[u][k] = make_uint4(0, 0, 0, 0);
+          vmin[u][k] = make_uint4(0, 0, 0, 0);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kBlkUnroll; ++u) {
+      const int blk = b0 + u * NG;
+      float acc = 0.f;
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) {
+        float a[V], b[V];
+        unpack16<E>(vmax[u][k], a);
+        unpack16<E>(vmin[u][k], b);
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc = fmaf(qp[k][e], a[e], fmaf(qn[k][e], b[e], acc));
+      }
+      acc = wave_sum<LPB>(acc);
+      if (li == 0 && blk < c1) out[blk] = blk < m ? acc : -INFINITY;
+    }
+  }
+}
+
+// One work-group per unit: stage the unit's scores as keys in LDS, select.
+__global__ __launch_bounds__(256) void block_topk_kernel(const float* __restrict__ scores,
+                                                          const int32_t* __restrict__ ctx_lens, int H_kv,
+                                                          int T, int B, int m_max, int K_b,
+                                                          int32_t* __restrict__ block_ids) {
+  extern __shared__ uint32_t smem[];
+  uint32_t* hist = smem;
+  uint32_t* keys = smem + 288;
+  const int unit = blockIdx.x;
+  const int s = unit / H_kv;
+  int n = ctx_lens[s];
+  n = n < 0 ? 0 : (n > T ? T : n);
+  const int m = (n + B - 1) / B;
+  const float* sc = scores + size_t(unit) * m_max;
+  for (int i = threadIdx.x; i < m; i += 256) keys[i] = float_key(sc[i]);
+  __syncthreads();
+  wg_topk_ascending<256>(keys, m, K_b, block_ids + size_t(unit) * K_b, K_b, nullptr,
+                         [](int i) { return int32_t(i); }, hist);
+}
+
+template <class E, int LPB, int CPL>
+static void launch_score_t(const Problem& P, const void* q, const void* kmax, const void* kmin,
+                           const int32_t* ctx_lens, float* scores, uint32_t* err, hipStream_t st) {
+  using S = typename E::T;
+  int bpw = 64;
+  if (long(P.units) * ((P.m_max + 63) / 64) < 1024) bpw = 16;
+  dim3 grid((P.m_max + bpw - 1) / bpw, P.units);
+  block_score_kernel<E, LPB, CPL><<<grid, 256, 0, st>>>((const S*)q, (const S*)kmax, (const S*)kmin,
+                                                        ctx_lens, P.H_q, P.H_kv, P.G, P.d_qk, P.B, P.T,
+                                                        P.m_max, bpw, scores, err);
+}
+
+hipError_t launch_block_score(const Problem& P, const void* q, const void* kmax, const void* kmin,
+                              const int32_t* ctx_lens, float* scores, uint32_t* err, hipStream_t st) {
+  const int V = P.dtype == 1 ? 8 : 4;
+  const int nch = P.d_qk / V;
+  if (P.dtype == 1) {
+    if (nch <= 16) launch_score_t<BF16, 16, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
+    else if (nch <= 32) launch_score_t<BF16, 32, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
+    else if (nch <= 64) launch_score_t<BF16, 64, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
+    else launch_score_t<BF16, 64, 2>(P, q, kmax, kmin, ctx_lens, scores, err, st);
+  } else {
+    if (nch <= 16) launch_score_t<F32, 16, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
+    else if (nch <= 32) launch_score_t<F32, 32, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
+    else if (nch <= 64) launch_score_t<F32, 64, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
+    else if (nch <= 128) launch_score_t<F32, 64, 2>(P, q, kmax, kmin, ctx_lens, scores, err, st);
+    else launch_score_t<F32, 64, 4>(P, q, kmax, kmin, ctx_lens, scores, err, st);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_block_topk(const Problem& P, const float* scores, const int32_t* ctx_lens, int K_b,
+                             int32_t* block_ids, uint32_t* err, hipStream_t st) {
+  (void)err;
+  const size_t lds = (288 + size_t(P.m_max)) * sizeof(uint32_t);
+  block_topk_kernel<<<P.units, 256, lds, st>>>(scores, ctx_lens, P.H_kv, P.T, P.B, P.m_max, K_b, block_ids);
+  return hipGetLastError();
+}
+
+}  // namespace tls

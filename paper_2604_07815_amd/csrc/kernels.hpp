@@ -1,0 +1,76 @@
+// Internal launch interface between the C ABI (tls_api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace tls {
+
+// Validated shape of one call (see tls_layout in include/tls.h).
+struct Problem {
+  int b, H_q, H_kv, G;
+  int d_qk, d_v, B, d_c, T, m_max;
+  int dtype;  // 0 f32, 1 bf16
+  int mla;    // V aliases K[..., :d_v]
+  float sigma;
+  int units;  // b * H_kv
+};
+
+// Capacity limits of this build (host validation rejects larger requests).
+constexpr int kMaxKeys = 12288;     // blocks per sequence, and K_b * B candidate slots
+constexpr int kMaxSplits = 64;      // attention splits per unit
+constexpr int kMaxGroupGqa = 8;     // G for the VALU attention path
+constexpr int kTokenSlotsPerWG = 256;
+
+// Workspace carving (byte offsets from the workspace base, 256-aligned).
+struct Workspace {
+  size_t err, bscores, bids, logits, stats, keys, tids, po, plse, total;
+  int n_tchunks;  // token-score work-groups per unit
+};
+Workspace plan_workspace(const Problem& P, int K_b, int K_t);
+
+hipError_t launch_block_index(const Problem& P, const void* K, const int32_t* ctx_lens, int tok_begin,
+                              int tok_end, void* kmax, void* kmin, uint32_t* err, hipStream_t st);
+hipError_t launch_token_index(const Problem& P, const void* K, const int32_t* ctx_lens,
+                              const int32_t* channels, int tok_begin, int tok_end, uint8_t* codes,
+                              float* qparams, uint32_t* err, hipStream_t st);
+
+hipError_t launch_block_score(const Problem& P, const void* q, const void* kmax, const void* kmin,
+                              const int32_t* ctx_lens, float* scores, uint32_t* err, hipStream_t st);
+hipError_t launch_block_topk(const Problem& P, const float* scores, const int32_t* ctx_lens, int K_b,
+                             int32_t* block_ids, uint32_t* err, hipStream_t st);
+
+hipError_t launch_token_score(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,
+                              const int32_t* channels, const int32_t* block_ids, int K_b,
+                              const int32_t* ctx_lens, float* logits, float* stats, int n_tchunks,
+                              uint32_t* err, hipStream_t st);
+hipError_t launch_token_alpha(const Problem& P, const float* logits, const float* stats, int n_tchunks,
+                              const int32_t* block_ids, int K_b, const int32_t* ctx_lens, uint32_t* keys,
+                              hipStream_t st);
+hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32_t* block_ids, int K_b,
+                             int K_t, int32_t* token_ids, float* token_scores, hipStream_t st);
+
+struct KvView {
+  const void* k;
+  const void* v;
+  const int32_t* slot_map;
+  int64_t n_slots;
+};
+int attn_splits_for(const Problem& P, int K_t, int requested);
+hipError_t launch_attention(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+                            const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
+                            uint32_t* err, hipStream_t st);
+hipError_t launch_merge(const Problem& P, const float* po, const float* plse, int nsplit, void* out,
+                        float* lse, hipStream_t st);
+
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, size_t n, hipStream_t st);
+
+hipError_t launch_prefetch(const Problem& P, const void* host_k, const void* host_v, const int32_t* ctx_lens,
+                           const int32_t* block_ids_new, const int32_t* block_ids_live, int K_b,
+                           void* pool_k, void* pool_v, int64_t n_slots, int32_t* slot_map,
+                           int32_t* slot_owner, int32_t* transfer_count, int32_t* transfer_list,
+                           uint32_t* err, hipStream_t st);
+
+}  // namespace tls

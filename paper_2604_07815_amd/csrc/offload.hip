@@ -1,0 +1,154 @@
+// Hierarchical KV cache: incremental block transmission (AsyncTLS Sec. 4.2).
+//
+// Per unit, the HBM pool holds n_slots blocks of K (and V) rows.  slot_map
+// maps a block id to its slot (-1: not resident) and slot_owner maps a slot
+// back to its block (-1: free).  One prefetch call for a new selection M_t:
+//   1. release every slot whose block is in neither M_t nor the live set
+//      (the blocks the in-flight attention step may still read);
+//   2. T_t = blocks of M_t without a slot (= M_t minus the resident set C_t);
+//   3. give the k-th block of T_t (ascending id) the k-th free slot
+//      (ascending), updating slot_map and slot_owner;
+//   4. copy those blocks' rows from pinned host memory into the pool with
+//      device-side loads over PCIe (no host round trip for T_t).
+// The copy reads rows [iB, min((i+1)B, ctx_len)) of block i.
+#include "kernels.hpp"
+
+namespace tls {
+
+__global__ __launch_bounds__(256) void prefetch_plan_kernel(
+    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ newb, const int32_t* __restrict__ live,
+    int K_b, int H_kv, int T, int B, int m_max, int64_t n_slots, int32_t* __restrict__ slot_map,
+    int32_t* __restrict__ slot_owner, int32_t* __restrict__ transfer_count, int32_t* __restrict__ xfer,
+    uint32_t* err) {
+  extern __shared__ uint32_t smem[];
+  uint32_t* keep = smem;                      // bitmap over the unit's blocks
+  uint32_t* wsum = smem + (m_max + 31) / 32;  // 2 x 4 wave partials
+  const int unit = blockIdx.x;
+  const int s = unit / H_kv;
+  int n = ctx_lens[s];
+  n = n < 0 ? 0 : (n > T ? T : n);
+  const int m = (n + B - 1) / B;
+  const int words = (m_max + 31) / 32;
+  int32_t* smap = slot_map + size_t(unit) * m_max;
+  int32_t* sown = slot_owner + size_t(unit) * n_slots;
+  const int32_t* nb = newb + size_t(unit) * K_b;
+  for (int i = threadIdx.x; i < words; i += 256) keep[i] = 0;
+  __syncthreads();
+  for (int i = threadIdx.x; i < K_b; i += 256) {
+    const int b = nb[i];
+    if (b >= 0 && b < m) atomicOr(&keep[b >> 5], 1u << (b & 31));
+    else if (b >= m) set_error(err, 2u);
+    if (live) {
+      const int lb = live[size_t(unit) * K_b + i];
+      if (lb >= 0 && lb < m) atomicOr(&keep[lb >> 5], 1u << (lb & 31));
+    }
+  }
+  __syncthreads();
+  // 1. release
+  for (int64_t sl = threadIdx.x; sl < n_slots; sl += 256) {
+    const int ow = sown[sl];
+    if (ow >= 0 && (ow >= m || !((keep[ow >> 5] >> (ow & 31)) & 1u))) {
+      if (ow < m_max && smap[ow] == int32_t(sl)) smap[ow] = -1;
+      sown[sl] = -1;
+    }
+  }
+  __syncthreads();
+  // 2 + 3. ordered compaction of the new blocks and the free slots
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  int32_t* list = xfer + size_t(unit) * (2 * K_b + 1);
+  int ntr = 0;
+  for (int base = 0; base < K_b; base += 256) {
+    const int i = base + threadIdx.x;
+    const int b = i < K_b ? nb[i] : -1;
+    const bool need = b >= 0 && b < m && smap[b] < 0;
+    const uint64_t bal = __ballot(need);
+    if (lane == 0) wsum[wid] = __popcll(bal);
+    __syncthreads();
+    int before = ntr, tot = 0;
+    for (int w = 0; w < 4; ++w) {
+      if (w < wid) before += wsum[w];
+      tot += wsum[w];
+    }
+    if (need) list[1 + 2 * (before + lanes_below(bal))] = b;
+    ntr += tot;
+    __syncthreads();
+  }
+  int nfree = 0;
+  for (int64_t base = 0; base < n_slots && nfree < ntr; base += 256) {
+    const int64_t sl = base + threadIdx.x;
+    const bool fr = sl < n_slots && sown[sl] < 0;
+    const uint64_t bal = __ballot(fr);
+    if (lane == 0) wsum[wid] = __popcll(bal);
+    __syncthreads();
+    int before = nfree, tot = 0;
+    for (int w = 0; w < 4; ++w) {
+      if (w < wid) before += wsum[w];
+      tot += wsum[w];
+    }
+    const int k = before + lanes_below(bal);
+    if (fr && k < ntr) list[2 + 2 * k] = int32_t(sl);
+    nfree += tot;
+    __syncthreads();
+  }
+  const int done = min(ntr, nfree);
+  if (ntr > nfree && threadIdx.x == 0) set_error(err, 16u);
+  for (int k = threadIdx.x; k < done; k += 256) {
+    const int b = list[1 + 2 * k], sl = list[2 + 2 * k];
+    smap[b] = sl;
+    sown[sl] = b;
+  }
+  if (threadIdx.x == 0) {
+    list[0] = done;
+    if (transfer_count) transfer_count[unit] = ntr;
+  }
+}
+
+// One work-group per (transfer entry, unit): copies one block of K (and V).
+template <int D_BYTES_MAX>
+__global__ __launch_bounds__(256) void prefetch_copy_kernel(
+    const uint8_t* __restrict__ host_k, const uint8_t* __restrict__ host_v, const int32_t* __restrict__ ctx_lens,
+    const int32_t* __restrict__ xfer, int K_b, int H_kv, int T, int B, int row_k, int row_v, int64_t n_slots,
+    uint8_t* __restrict__ pool_k, uint8_t* __restrict__ pool_v) {
+  const int k = blockIdx.x, unit = blockIdx.y;
+  const int32_t* list = xfer + size_t(unit) * (2 * K_b + 1);
+  if (k >= list[0]) return;
+  const int b = list[1 + 2 * k], sl = list[2 + 2 * k];
+  const int s = unit / H_kv;
+  int n = ctx_lens[s];
+  n = n < 0 ? 0 : (n > T ? T : n);
+  const int r0 = b * B, r1 = min(r0 + B, n);
+  if (r1 <= r0) return;
+  const size_t rows = size_t(r1 - r0);
+  {
+    const size_t bytes = rows * row_k;
+    const uint8_t* src = host_k + (size_t(unit) * T + r0) * row_k;
+    uint8_t* dst = pool_k + (size_t(unit) * n_slots + sl) * size_t(B) * row_k;
+    for (size_t o = threadIdx.x * 16; o < bytes; o += 256 * 16) *reinterpret_cast<uint4*>(dst + o) = ld16(src + o);
+  }
+  if (host_v) {
+    const size_t bytes = rows * row_v;
+    const uint8_t* src = host_v + (size_t(unit) * T + r0) * row_v;
+    uint8_t* dst = pool_v + (size_t(unit) * n_slots + sl) * size_t(B) * row_v;
+    for (size_t o = threadIdx.x * 16; o < bytes; o += 256 * 16) *reinterpret_cast<uint4*>(dst + o) = ld16(src + o);
+  }
+}
+
+hipError_t launch_prefetch(const Problem& P, const void* host_k, const void* host_v, const int32_t* ctx_lens,
+                           const int32_t* block_ids_new, const int32_t* block_ids_live, int K_b, void* pool_k,
+                           void* pool_v, int64_t n_slots, int32_t* slot_map, int32_t* slot_owner,
+                           int32_t* transfer_count, int32_t* transfer_list, uint32_t* err, hipStream_t st) {
+  const size_t lds = ((P.m_max + 31) / 32 + 8) * sizeof(uint32_t);
+  prefetch_plan_kernel<<<P.units, 256, lds, st>>>(ctx_lens, block_ids_new, block_ids_live, K_b, P.H_kv, P.T, P.B,
+                                                  P.m_max, n_slots, slot_map, slot_owner, transfer_count,
+                                                  transfer_list, err);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int es = P.dtype == 1 ? 2 : 4;
+  dim3 grid(K_b, P.units);
+  prefetch_copy_kernel<0><<<grid, 256, 0, st>>>((const uint8_t*)host_k, (const uint8_t*)host_v, ctx_lens,
+                                                transfer_list, K_b, P.H_kv, P.T, P.B, P.d_qk * es, P.d_v * es,
+                                                n_slots, (uint8_t*)pool_k, (uint8_t*)pool_v);
+  return hipGetLastError();
+}
+
+}  // namespace tls

@@ -1,0 +1,340 @@
+// C ABI of libtls.so: host-side validation (nothing is enqueued on error),
+// workspace carving and stage dispatch.  See include/tls.h for the contract.
+#include <math.h>
+#include <string.h>
+
+#include "tls.h"
+#include "kernels.hpp"
+
+using tls::Problem;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr size_t kHeaderBytes = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+tls_status make_problem(const tls_layout* L, Problem* P) {
+  if (!L) return TLS_ERR_INVALID_ARGUMENT;
+  if (L->batch < 1 || L->num_q_heads < 1 || L->num_kv_heads < 1) return TLS_ERR_INVALID_ARGUMENT;
+  if (L->num_q_heads % L->num_kv_heads != 0) return TLS_ERR_INVALID_ARGUMENT;
+  if (L->head_dim_qk < 1 || L->head_dim_v < 1 || L->block_size < 1 || L->max_ctx < 1) return TLS_ERR_INVALID_ARGUMENT;
+  if (L->index_channels < 32 || L->index_channels % 32 != 0 || L->index_channels > L->head_dim_qk)
+    return TLS_ERR_INVALID_ARGUMENT;
+  if (L->dtype != TLS_DTYPE_F32 && L->dtype != TLS_DTYPE_BF16) return TLS_ERR_INVALID_ARGUMENT;
+  if (L->mla_shared_kv != 0 && L->mla_shared_kv != 1) return TLS_ERR_INVALID_ARGUMENT;
+  if (L->mla_shared_kv && L->head_dim_v > L->head_dim_qk) return TLS_ERR_INVALID_ARGUMENT;
+  if (!(L->softmax_scale == L->softmax_scale) || isinf(L->softmax_scale)) return TLS_ERR_INVALID_ARGUMENT;
+  // supported subset of this build
+  if (L->block_size != 64) return TLS_ERR_UNSUPPORTED;
+  if (L->head_dim_qk % 8 != 0 || L->head_dim_qk > 1024) return TLS_ERR_UNSUPPORTED;
+  if (L->index_channels > 256) return TLS_ERR_UNSUPPORTED;
+  const int G = L->num_q_heads / L->num_kv_heads;
+  if (G > 32) return TLS_ERR_UNSUPPORTED;
+  const long m_max = (long(L->max_ctx) + L->block_size - 1) / L->block_size;
+  if (m_max > tls::kMaxKeys) return TLS_ERR_UNSUPPORTED;
+  const long units = long(L->batch) * L->num_kv_heads;
+  if (units > 65535) return TLS_ERR_UNSUPPORTED;
+  P->b = L->batch;
+  P->H_q = L->num_q_heads;
+  P->H_kv = L->num_kv_heads;
+  P->G = G;
+  P->d_qk = L->head_dim_qk;
+  P->d_v = L->head_dim_v;
+  P->B = L->block_size;
+  P->d_c = L->index_channels;
+  P->T = L->max_ctx;
+  P->m_max = int(m_max);
+  P->dtype = L->dtype;
+  P->mla = L->mla_shared_kv;
+  P->sigma = L->softmax_scale > 0.f ? L->softmax_scale : float(1.0 / sqrt(double(L->head_dim_qk)));
+  P->units = int(units);
+  return TLS_OK;
+}
+
+tls_status check_budgets(const Problem& P, int K_b, int K_t) {
+  if (K_b < 1 || K_t < 1) return TLS_ERR_INVALID_ARGUMENT;
+  if (long(K_b) * P.B > tls::kMaxKeys) return TLS_ERR_UNSUPPORTED;
+  return TLS_OK;
+}
+
+tls_status check_attention(const Problem& P, int K_t) {
+  if (P.mla) {
+    if (P.dtype != TLS_DTYPE_BF16 || P.d_qk > 576 || P.d_v > 512 || P.d_v % 2 != 0) return TLS_ERR_UNSUPPORTED;
+    if (K_t > 32 * tls::kMaxSplits) return TLS_ERR_UNSUPPORTED;
+    return TLS_OK;
+  }
+  if (P.d_qk != P.d_v || (P.d_qk != 128 && P.d_qk != 64)) return TLS_ERR_UNSUPPORTED;
+  if (P.G != 1 && P.G != 2 && P.G != 4 && P.G != 8) return TLS_ERR_UNSUPPORTED;
+  return TLS_OK;
+}
+
+tls_status hip_status(hipError_t e) { return e == hipSuccess ? TLS_OK : TLS_ERR_HIP; }
+
+template <class T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+uint32_t* err_word(void* ws) { return static_cast<uint32_t*>(ws); }
+
+}  // namespace
+
+namespace tls {
+
+Workspace plan_workspace(const Problem& P, int K_b, int K_t) {
+  Workspace w{};
+  const size_t U = size_t(P.units);
+  const size_t S = size_t(K_b) * P.B;
+  w.n_tchunks = int((S + kTokenSlotsPerWG - 1) / kTokenSlotsPerWG);
+  size_t off = 0;
+  w.err = off;      off += kHeaderBytes;
+  w.bscores = off;  off = align_up(off + U * P.m_max * sizeof(float));
+  w.bids = off;     off = align_up(off + U * K_b * sizeof(int32_t));
+  w.logits = off;   off = align_up(off + U * P.G * S * sizeof(float));
+  w.stats = off;    off = align_up(off + U * w.n_tchunks * P.G * 2 * sizeof(float));
+  w.keys = off;     off = align_up(off + U * S * sizeof(uint32_t));
+  w.tids = off;     off = align_up(off + U * size_t(K_t) * sizeof(int32_t));
+  w.po = off;       off = align_up(off + U * kMaxSplits * P.G * size_t(P.d_v) * sizeof(float));
+  w.plse = off;     off = align_up(off + U * kMaxSplits * P.G * sizeof(float));
+  w.total = off + align_up(U * (2 * size_t(K_b) + 1) * sizeof(int32_t));  // prefetch transfer lists
+  return w;
+}
+
+}  // namespace tls
+
+extern "C" {
+
+const char* tls_version(void) { return "0.1.0 gfx950"; }
+
+const char* tls_status_string(tls_status s) {
+  switch (s) {
+    case TLS_OK: return "TLS_OK";
+    case TLS_ERR_INVALID_ARGUMENT: return "TLS_ERR_INVALID_ARGUMENT";
+    case TLS_ERR_UNSUPPORTED: return "TLS_ERR_UNSUPPORTED";
+    case TLS_ERR_WORKSPACE_TOO_SMALL: return "TLS_ERR_WORKSPACE_TOO_SMALL";
+    case TLS_ERR_HIP: return "TLS_ERR_HIP";
+    default: return "TLS_ERR_UNKNOWN";
+  }
+}
+
+tls_status tls_workspace_size(const tls_layout* layout, int32_t K_b, int32_t K_t, size_t* bytes) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!bytes) return TLS_ERR_INVALID_ARGUMENT;
+  st = check_budgets(P, K_b, K_t);
+  if (st != TLS_OK) return st;
+  *bytes = tls::plan_workspace(P, K_b, K_t).total;
+  return TLS_OK;
+}
+
+tls_status tls_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!ws || ws_bytes < kHeaderBytes) return TLS_ERR_INVALID_ARGUMENT;
+  return hip_status(tls::launch_fill_u32(static_cast<uint32_t*>(ws), 0u, kHeaderBytes / 4, stream));
+}
+
+tls_status tls_build_block_index(const tls_layout* layout, const void* K, const int32_t* ctx_lens, int32_t tok_begin,
+                                 int32_t tok_end, void* kmax, void* kmin, hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!K || !ctx_lens || !kmax || !kmin) return TLS_ERR_INVALID_ARGUMENT;
+  if (tok_begin < 0 || tok_end < tok_begin || tok_end > P.T) return TLS_ERR_INVALID_ARGUMENT;
+  if (tok_end == tok_begin) return TLS_OK;
+  return hip_status(tls::launch_block_index(P, K, ctx_lens, tok_begin, tok_end, kmax, kmin, nullptr, stream));
+}
+
+tls_status tls_build_token_index(const tls_layout* layout, const void* K, const int32_t* ctx_lens,
+                                 const int32_t* channels, int32_t tok_begin, int32_t tok_end, uint8_t* codes,
+                                 float* qparams, hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!K || !ctx_lens || !channels || !codes || !qparams) return TLS_ERR_INVALID_ARGUMENT;
+  if (tok_begin < 0 || tok_end < tok_begin || tok_end > P.T) return TLS_ERR_INVALID_ARGUMENT;
+  if (tok_end == tok_begin) return TLS_OK;
+  return hip_status(
+      tls::launch_token_index(P, K, ctx_lens, channels, tok_begin, tok_end, codes, qparams, nullptr, stream));
+}
+
+tls_status tls_select_blocks(const tls_layout* layout, const void* q, const void* kmax, const void* kmin,
+                             const int32_t* ctx_lens, int32_t K_b, int32_t* block_ids, float* block_scores, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!q || !kmax || !kmin || !ctx_lens || !block_ids || !ws) return TLS_ERR_INVALID_ARGUMENT;
+  st = check_budgets(P, K_b, 1);
+  if (st != TLS_OK) return st;
+  const tls::Workspace W = tls::plan_workspace(P, K_b, 1);
+  if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  float* scores = block_scores ? block_scores : at<float>(ws, W.bscores);
+  hipError_t e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, scores, err_word(ws), stream);
+  if (e == hipSuccess) e = tls::launch_block_topk(P, scores, ctx_lens, K_b, block_ids, err_word(ws), stream);
+  return hip_status(e);
+}
+
+static hipError_t run_token_select(const Problem& P, const tls::Workspace& W, const void* q, const uint8_t* codes,
+                                   const float* qparams, const int32_t* channels, const int32_t* block_ids, int K_b,
+                                   const int32_t* ctx_lens, int K_t, int32_t* token_ids, float* token_scores,
+                                   void* ws, hipStream_t stream, hipEvent_t* ev) {
+  hipError_t e = tls::launch_token_score(P, q, codes, qparams, channels, block_ids, K_b, ctx_lens,
+                                         at<float>(ws, W.logits), at<float>(ws, W.stats), W.n_tchunks, err_word(ws),
+                                         stream);
+  if (e != hipSuccess) return e;
+  if (ev) hipEventRecord(ev[0], stream);
+  e = tls::launch_token_alpha(P, at<float>(ws, W.logits), at<float>(ws, W.stats), W.n_tchunks, block_ids, K_b,
+                              ctx_lens, at<uint32_t>(ws, W.keys), stream);
+  if (e != hipSuccess) return e;
+  if (ev) hipEventRecord(ev[1], stream);
+  return tls::launch_token_topk(P, at<uint32_t>(ws, W.keys), block_ids, K_b, K_t, token_ids, token_scores, stream);
+}
+
+tls_status tls_select_tokens(const tls_layout* layout, const void* q, const uint8_t* codes, const float* qparams,
+                             const int32_t* channels, const int32_t* block_ids, int32_t K_b, const int32_t* ctx_lens,
+                             int32_t K_t, int32_t* token_ids, float* token_scores, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!q || !codes || !qparams || !channels || !block_ids || !ctx_lens || !token_ids || !ws)
+    return TLS_ERR_INVALID_ARGUMENT;
+  st = check_budgets(P, K_b, K_t);
+  if (st != TLS_OK) return st;
+  const tls::Workspace W = tls::plan_workspace(P, K_b, K_t);
+  if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  return hip_status(run_token_select(P, W, q, codes, qparams, channels, block_ids, K_b, ctx_lens, K_t, token_ids,
+                                     token_scores, ws, stream, nullptr));
+}
+
+tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_kv_view* kv, const int32_t* ctx_lens,
+                             const void* kmax, const void* kmin, const uint8_t* codes, const float* qparams,
+                             const int32_t* channels, int32_t K_b, int32_t K_t, const int32_t* block_ids_in,
+                             const int32_t* token_ids_in, void* out, float* lse, int32_t* block_ids_out,
+                             int32_t* token_ids_out, void* ws, size_t ws_bytes, const tls_decode_opts* opts,
+                             hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!q || !kv || !kv->k || !ctx_lens || !out || !ws) return TLS_ERR_INVALID_ARGUMENT;
+  if (!P.mla && !kv->v) return TLS_ERR_INVALID_ARGUMENT;
+  if (P.mla && kv->v) return TLS_ERR_INVALID_ARGUMENT;
+  if (kv->slot_map && kv->n_slots < 1) return TLS_ERR_INVALID_ARGUMENT;
+  const bool sel_tokens = token_ids_in == nullptr;
+  const bool sel_blocks = sel_tokens && block_ids_in == nullptr;
+  if (sel_blocks && (!kmax || !kmin)) return TLS_ERR_INVALID_ARGUMENT;
+  if (sel_tokens && (!codes || !qparams || !channels)) return TLS_ERR_INVALID_ARGUMENT;
+  st = check_budgets(P, K_b, K_t);
+  if (st != TLS_OK) return st;
+  st = check_attention(P, K_t);
+  if (st != TLS_OK) return st;
+  int requested = 0;
+  hipEvent_t* ev = nullptr;
+  if (opts) {
+    for (int i = 0; i < 7; ++i)
+      if (opts->reserved[i] != 0) return TLS_ERR_INVALID_ARGUMENT;
+    if (opts->attn_splits < 0 || opts->attn_splits > tls::kMaxSplits) return TLS_ERR_INVALID_ARGUMENT;
+    requested = opts->attn_splits;
+    ev = opts->stage_events;
+    if (ev)
+      for (int i = 0; i < TLS_NUM_STAGE_EVENTS; ++i)
+        if (!ev[i]) return TLS_ERR_INVALID_ARGUMENT;
+  }
+  const tls::Workspace W = tls::plan_workspace(P, K_b, K_t);
+  if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+
+  hipError_t e = hipSuccess;
+  auto mark = [&](int i) {
+    if (ev) hipEventRecord(ev[i], stream);
+  };
+  mark(0);
+  const int32_t* bids = block_ids_in;
+  if (sel_blocks) {
+    int32_t* bo = block_ids_out ? block_ids_out : at<int32_t>(ws, W.bids);
+    e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.bscores), err_word(ws), stream);
+    mark(1);
+    if (e == hipSuccess) e = tls::launch_block_topk(P, at<float>(ws, W.bscores), ctx_lens, K_b, bo, err_word(ws), stream);
+    bids = bo;
+  } else {
+    mark(1);
+  }
+  mark(2);
+  if (e != hipSuccess) return TLS_ERR_HIP;
+  const int32_t* tids = token_ids_in;
+  if (sel_tokens) {
+    int32_t* to = token_ids_out ? token_ids_out : at<int32_t>(ws, W.tids);
+    e = run_token_select(P, W, q, codes, qparams, channels, bids, K_b, ctx_lens, K_t, to, nullptr, ws, stream,
+                         ev ? ev + 3 : nullptr);
+    tids = to;
+  } else {
+    mark(3);
+    mark(4);
+  }
+  mark(5);
+  if (e != hipSuccess) return TLS_ERR_HIP;
+  const int nsplit = tls::attn_splits_for(P, K_t, requested);
+  tls::KvView view{kv->k, kv->v, kv->slot_map, kv->n_slots};
+  e = tls::launch_attention(P, q, view, tids, ctx_lens, K_t, nsplit, at<float>(ws, W.po), at<float>(ws, W.plse),
+                            err_word(ws), stream);
+  mark(6);
+  if (e == hipSuccess) e = tls::launch_merge(P, at<float>(ws, W.po), at<float>(ws, W.plse), nsplit, out, lse, stream);
+  mark(7);
+  return hip_status(e);
+}
+
+tls_status tls_prefetch_blocks(const tls_layout* layout, const void* host_k, const void* host_v,
+                               const int32_t* ctx_lens, const int32_t* block_ids_new, const int32_t* block_ids_live,
+                               int32_t K_b, void* pool_k, void* pool_v, int64_t n_slots, int32_t* slot_map,
+                               int32_t* slot_owner, int32_t* transfer_count, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!host_k || !ctx_lens || !block_ids_new || !pool_k || !slot_map || !slot_owner || !ws)
+    return TLS_ERR_INVALID_ARGUMENT;
+  if (P.mla ? (host_v != nullptr || pool_v != nullptr) : (!host_v || !pool_v)) return TLS_ERR_INVALID_ARGUMENT;
+  st = check_budgets(P, K_b, 1);
+  if (st != TLS_OK) return st;
+  if (n_slots < (block_ids_live ? 2 * int64_t(K_b) : int64_t(K_b)) || n_slots > (int64_t(1) << 30))
+    return TLS_ERR_INVALID_ARGUMENT;
+  // host K/V must be pinned (device-accessible) host memory
+  const void* dk = nullptr;
+  const void* dv = nullptr;
+  {
+    hipPointerAttribute_t a;
+    if (hipPointerGetAttributes(&a, host_k) != hipSuccess || a.type != hipMemoryTypeHost || !a.devicePointer) {
+      (void)hipGetLastError();
+      return TLS_ERR_INVALID_ARGUMENT;
+    }
+    dk = static_cast<const char*>(a.devicePointer) + (static_cast<const char*>(host_k) - static_cast<const char*>(a.hostPointer));
+    if (host_v) {
+      if (hipPointerGetAttributes(&a, host_v) != hipSuccess || a.type != hipMemoryTypeHost || !a.devicePointer) {
+        (void)hipGetLastError();
+        return TLS_ERR_INVALID_ARGUMENT;
+      }
+      dv = static_cast<const char*>(a.devicePointer) + (static_cast<const char*>(host_v) - static_cast<const char*>(a.hostPointer));
+    }
+  }
+  const tls::Workspace W = tls::plan_workspace(P, K_b, 1);
+  if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  int32_t* xfer = at<int32_t>(ws, W.total - align_up(size_t(P.units) * (2 * size_t(K_b) + 1) * sizeof(int32_t)));
+  return hip_status(tls::launch_prefetch(P, dk, dv, ctx_lens, block_ids_new, block_ids_live, K_b, pool_k, pool_v,
+                                         n_slots, slot_map, slot_owner, transfer_count, xfer, err_word(ws), stream));
+}
+
+tls_status tls_check_device_error(const void* ws, size_t ws_bytes, int32_t clear, int32_t* flags, hipStream_t stream) {
+  if (!ws || ws_bytes < kHeaderBytes || !flags) return TLS_ERR_INVALID_ARGUMENT;
+  uint32_t h = 0;
+  if (hipMemcpyAsync(&h, ws, sizeof(h), hipMemcpyDeviceToHost, stream) != hipSuccess) return TLS_ERR_HIP;
+  if (hipStreamSynchronize(stream) != hipSuccess) return TLS_ERR_HIP;
+  *flags = int32_t(h);
+  if (clear) {
+    if (tls::launch_fill_u32(static_cast<uint32_t*>(const_cast<void*>(ws)), 0u, 1, stream) != hipSuccess)
+      return TLS_ERR_HIP;
+  }
+  return TLS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,246 @@
+// Fine token selection inside the selected blocks (AsyncTLS Sec. 4.1).
+//
+// Candidate slots of a unit: slot = i*B + o for the i-th entry of its block
+// list and offset o; the slot is a valid candidate when that entry is a
+// block id >= 0 and token id*B + o < ctx_len.  With an ascending block list,
+// slot order is token order, so lowest-slot tie-breaking is lowest-position
+// tie-breaking.
+//
+// token_score_kernel: per slot and head, l = sigma * q~_h . dequant(code_j).
+//   With dequant = min + code*scale per 32-channel group this is
+//   sigma * sum_grp (min_grp * sum_c q~_hc + scale_grp * sum_c q~_hc code_c):
+//   the integer codes enter the dot product directly.  Also emits each
+//   work-group's per-head (max, sum exp) of its slots.
+// token_alpha_kernel: per-head normalisers over all candidates, then
+//   alpha_j = (1/G) sum_h exp(l_hj - m_h) / Z_h as an orderable key.
+// token_topk_kernel: the K_t largest alpha, ascending token positions.
+#include "kernels.hpp"
+
+namespace tls {
+
+constexpr int kMaxG = 32;
+constexpr int kMaxGroups = 8;  // d_c <= 256
+
+__device__ inline void unpack_nibbles8(uint32_t w, float* f) {
+  const uint32_t lo = w & 0x0f0f0f0fu, hi = (w >> 4) & 0x0f0f0f0fu;
+  f[0] = float(lo & 0xffu);         f[1] = float(hi & 0xffu);
+  f[2] = float((lo >> 8) & 0xffu);  f[3] = float((hi >> 8) & 0xffu);
+  f[4] = float((lo >> 16) & 0xffu); f[5] = float((hi >> 16) & 0xffu);
+  f[6] = float(lo >> 24);           f[7] = float(hi >> 24);
+}
+
+__device__ inline bool slot_token(const int32_t* bl, int K_b, int B, int m, int n, int slot, int* tok,
+                                  uint32_t* err) {
+  const int i = slot / B, o = slot % B;
+  if (i >= K_b) return false;
+  const int blk = bl[i];
+  if (blk < 0) return false;
+  if (blk >= m) {
+    set_error(err, 2u);
+    return false;
+  }
+  const int t = blk * B + o;
+  *tok = t;
+  return t < n;
+}
+
+template <class E>
+__global__ __launch_bounds__(256) void token_score_kernel(
+    const typename E::T* __restrict__ q, const uint8_t* __restrict__ codes, const float* __restrict__ qparams,
+    const int32_t* __restrict__ channels, const int32_t* __restrict__ block_ids, int K_b,
+    const int32_t* __restrict__ ctx_lens, int H_q, int H_kv, int G, int d, int d_c, int B, int T, float sigma,
+    float* __restrict__ logits, float* __restrict__ stats, uint32_t* err) {
+  __shared__ float s_qt[kMaxG * 256];
+  __shared__ float s_qsum[kMaxG * kMaxGroups];
+  __shared__ float s_red[4 * kMaxG];
+  const int unit = blockIdx.y, chunk = blockIdx.x;
+  const int s = unit / H_kv, g = unit % H_kv;
+  int n = ctx_lens[s];
+  n = n < 0 ? 0 : (n > T ? T : n);
+  const int m = (n + B - 1) / B;
+  const int ngr = d_c / 32;
+  const int S = K_b * B;
+  const typename E::T* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
+  for (int i = threadIdx.x; i < G * d_c; i += 256) {
+    const int h = i / d_c, c = i % d_c;
+    int ch = channels[g * d_c + c];
+    if (ch < 0 || ch >= d) {  // caller-supplied channel id out of range
+      set_error(err, 32u);
+      ch = 0;
+    }
+    s_qt[i] = E::to_f(qg[size_t(h) * d + ch]);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < G * ngr; i += 256) {
+    const int h = i / ngr, gr = i % ngr;
+    float acc = 0.f;
+    for (int c = 0; c < 32; ++c) acc += s_qt[h * d_c + gr * 32 + c];
+    s_qsum[i] = acc;
+  }
+  __syncthreads();
+
+  const int slot = chunk * kTokenSlotsPerWG + threadIdx.x;
+  const int32_t* bl = block_ids + size_t(unit) * K_b;
+  int tok = 0;
+  const bool valid = slot < S && slot_token(bl, K_b, B, m, n, slot, &tok, err);
+  float acc[kMaxG];
+#pragma unroll
+  for (int h = 0; h < kMaxG; ++h) acc[h] = 0.f;
+  if (valid) {
+    const size_t row = size_t(unit) * T + tok;
+    const uint8_t* crow = codes + row * (d_c / 2);
+    const float* prow = qparams + row * ngr * 2;
+    for (int gr = 0; gr < ngr; ++gr) {
+      const uint4 cw = ld16_stream(crow + gr * 16);
+      const float scale = prow[gr * 2 + 0], mn = prow[gr * 2 + 1];
+      float cf[32];
+      unpack_nibbles8(cw.x, cf + 0);
+      unpack_nibbles8(cw.y, cf + 8);
+      unpack_nibbles8(cw.z, cf + 16);
+      unpack_nibbles8(cw.w, cf + 24);
+#pragma unroll
+      for (int h = 0; h < kMaxG; ++h) {
+        if (h < G) {
+          const float* qt = s_qt + h * d_c + gr * 32;
+          float dot = 0.f;
+#pragma unroll
+          for (int c = 0; c < 32; ++c) dot = fmaf(qt[c], cf[c], dot);
+          acc[h] += mn * s_qsum[h * ngr + gr] + scale * dot;
+        }
+      }
+    }
+  }
+  // logits and this work-group's per-head softmax statistics
+  float* lg = logits + size_t(unit) * G * S;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+  for (int h = 0; h < kMaxG; ++h) {
+    if (h < G) {
+      const float l = valid ? sigma * acc[h] : -INFINITY;
+      acc[h] = l;
+      if (slot < S) lg[size_t(h) * S + slot] = l;
+      const float wm = wave_max<64>(l);
+      if (lane == 0) s_red[wid * kMaxG + h] = wm;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < kMaxG; ++h) {
+    if (h < G) {
+      const float M = fmaxf(fmaxf(s_red[h], s_red[kMaxG + h]), fmaxf(s_red[2 * kMaxG + h], s_red[3 * kMaxG + h]));
+      acc[h] = (valid && M != -INFINITY) ? __expf(acc[h] - M) : 0.f;
+    }
+  }
+  __syncthreads();
+  __shared__ float s_sum[4 * kMaxG];
+#pragma unroll
+  for (int h = 0; h < kMaxG; ++h) {
+    if (h < G) {
+      const float ws = wave_sum<64>(acc[h]);
+      if (lane == 0) s_sum[wid * kMaxG + h] = ws;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < G) {
+    const int h = threadIdx.x;
+    const float M = fmaxf(fmaxf(s_red[h], s_red[kMaxG + h]), fmaxf(s_red[2 * kMaxG + h], s_red[3 * kMaxG + h]));
+    const float Z = ((s_sum[h] + s_sum[kMaxG + h]) + s_sum[2 * kMaxG + h]) + s_sum[3 * kMaxG + h];
+    float* st = stats + ((size_t(unit) * gridDim.x + chunk) * G + h) * 2;
+    st[0] = M;
+    st[1] = Z;
+  }
+}
+
+__global__ __launch_bounds__(256) void token_alpha_kernel(
+    const float* __restrict__ logits, const float* __restrict__ stats, int n_tchunks,
+    const int32_t* __restrict__ block_ids, int K_b, const int32_t* __restrict__ ctx_lens, int H_kv, int G,
+    int B, int T, uint32_t* __restrict__ keys) {
+  __shared__ float s_m[kMaxG], s_iz[kMaxG];
+  const int unit = blockIdx.y;
+  const int s = unit / H_kv;
+  int n = ctx_lens[s];
+  n = n < 0 ? 0 : (n > T ? T : n);
+  const int m = (n + B - 1) / B;
+  const int S = K_b * B;
+  if (threadIdx.x < G) {
+    const int h = threadIdx.x;
+    const float* st = stats + size_t(unit) * n_tchunks * G * 2;
+    float M = -INFINITY;
+    for (int c = 0; c < n_tchunks; ++c) M = fmaxf(M, st[(c * G + h) * 2]);
+    float Z = 0.f;
+    if (M != -INFINITY)
+      for (int c = 0; c < n_tchunks; ++c) {
+        const float mc = st[(c * G + h) * 2], zc = st[(c * G + h) * 2 + 1];
+        if (mc != -INFINITY) Z += zc * __expf(mc - M);
+      }
+    s_m[h] = M;
+    s_iz[h] = Z > 0.f ? 1.0f / Z : 0.f;
+  }
+  __syncthreads();
+  const float invG = 1.0f / float(G);
+  const int32_t* bl = block_ids + size_t(unit) * K_b;
+  const float* lg = logits + size_t(unit) * G * S;
+  for (int slot = blockIdx.x * 256 + threadIdx.x; slot < S; slot += gridDim.x * 256) {
+    int tok;
+    uint32_t key = kInvalidKey;
+    if (slot_token(bl, K_b, B, m, n, slot, &tok, nullptr)) {
+      float a = 0.f;
+      for (int h = 0; h < G; ++h) a += __expf(lg[size_t(h) * S + slot] - s_m[h]) * s_iz[h];
+      key = float_key(a * invG);
+    }
+    keys[size_t(unit) * S + slot] = key;
+  }
+}
+
+__global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __restrict__ keys,
+                                                           const int32_t* __restrict__ block_ids, int K_b,
+                                                           int B, int K_t, int32_t* __restrict__ token_ids,
+                                                           float* __restrict__ token_scores) {
+  extern __shared__ uint32_t smem[];
+  uint32_t* hist = smem;
+  int32_t* s_bl = reinterpret_cast<int32_t*>(smem + 288);
+  uint32_t* s_keys = smem + 288 + K_b;
+  const int unit = blockIdx.x;
+  const int S = K_b * B;
+  for (int i = threadIdx.x; i < K_b; i += 1024) s_bl[i] = block_ids[size_t(unit) * K_b + i];
+  for (int i = threadIdx.x; i < S; i += 1024) s_keys[i] = keys[size_t(unit) * S + i];
+  __syncthreads();
+  wg_topk_ascending<1024>(s_keys, S, K_t, token_ids + size_t(unit) * K_t, K_t,
+                          token_scores ? token_scores + size_t(unit) * K_t : nullptr,
+                          [=](int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, hist);
+}
+
+hipError_t launch_token_score(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,
+                              const int32_t* channels, const int32_t* block_ids, int K_b,
+                              const int32_t* ctx_lens, float* logits, float* stats, int n_tchunks,
+                              uint32_t* err, hipStream_t st) {
+  dim3 grid(n_tchunks, P.units);
+  if (P.dtype == 1)
+    token_score_kernel<BF16><<<grid, 256, 0, st>>>((const uint16_t*)q, codes, qparams, channels, block_ids,
+                                                   K_b, ctx_lens, P.H_q, P.H_kv, P.G, P.d_qk, P.d_c, P.B,
+                                                   P.T, P.sigma, logits, stats, err);
+  else
+    token_score_kernel<F32><<<grid, 256, 0, st>>>((const float*)q, codes, qparams, channels, block_ids, K_b,
+                                                  ctx_lens, P.H_q, P.H_kv, P.G, P.d_qk, P.d_c, P.B, P.T,
+                                                  P.sigma, logits, stats, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_token_alpha(const Problem& P, const float* logits, const float* stats, int n_tchunks,
+                              const int32_t* block_ids, int K_b, const int32_t* ctx_lens, uint32_t* keys,
+                              hipStream_t st) {
+  const int S = K_b * P.B;
+  dim3 grid((S + 255) / 256, P.units);
+  token_alpha_kernel<<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.G,
+                                           P.B, P.T, keys);
+  return hipGetLastError();
+}
+
+hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32_t* block_ids, int K_b,
+                             int K_t, int32_t* token_ids, float* token_scores, hipStream_t st) {
+  const size_t lds = (288 + size_t(K_b) + size_t(K_b) * P.B) * sizeof(uint32_t);
+  token_topk_kernel<<<P.units, 1024, lds, st>>>(keys, block_ids, K_b, P.B, K_t, token_ids, token_scores);
+  return hipGetLastError();
+}
+
+}  // namespace tls

@@ -229,13 +229,15 @@ def _seq_seed(cfg: DecodeConfig, s: int) -> int:
 # Full input sets
 # ----------------------------------------------------------------------------
 
-def make_host(cfg: DecodeConfig, pad: str = "nan", q_store: Optional[np.ndarray] = None) -> dict:
+def make_host(cfg: DecodeConfig, pad: str = "nan", q_store: Optional[np.ndarray] = None,
+              ctx_lens: Optional[np.ndarray] = None) -> dict:
     """All inputs on the host (numpy).  Keys/values beyond a sequence's length
     are filled with NaN (pad='nan', so a stray read poisons the result) or 0.
 
     Returns dict(q, k, v, ctx_lens, channels, plant_starts, planted_key);
-    k is [b][h_kv][max_ctx][d_qk]; v is [b][h_kv][max_ctx][d_v] or None (MLA)."""
-    ctx = draw_ctx_lens(cfg)
+    k is [b][h_kv][max_ctx][d_qk]; v is [b][h_kv][max_ctx][d_v] or None (MLA).
+    `ctx_lens` overrides the drawn context lengths."""
+    ctx = draw_ctx_lens(cfg) if ctx_lens is None else np.asarray(ctx_lens, dtype=np.int32)
     ch = draw_channels(cfg)
     q = draw_queries(cfg) if q_store is None else q_store
     starts = draw_plant_starts(cfg, ctx)
@@ -263,13 +265,13 @@ def make_host(cfg: DecodeConfig, pad: str = "nan", q_store: Optional[np.ndarray]
 
 
 def make_device(cfg: DecodeConfig, device="cuda", pad: str = "zero",
-                q_store: Optional[np.ndarray] = None) -> dict:
+                q_store: Optional[np.ndarray] = None, ctx_lens: Optional[np.ndarray] = None) -> dict:
     """All inputs as torch tensors on `device`; the large K/V arrays are drawn
     with a seeded torch.Generator there (one generator per sequence)."""
     import torch
 
     tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
-    ctx = draw_ctx_lens(cfg)
+    ctx = draw_ctx_lens(cfg) if ctx_lens is None else np.asarray(ctx_lens, dtype=np.int32)
     ch = draw_channels(cfg)
     q = draw_queries(cfg) if q_store is None else q_store
     starts = draw_plant_starts(cfg, ctx)

@@ -1,0 +1,205 @@
+"""Shared plumbing of the GPU parity tests.
+
+Inputs come from `synth` (host numpy for small cases, a seeded device
+generator for full-size cases); the oracle reads the same bits copied to
+the host.  GPU results are only ever compared with oracle results; no
+oracle input is taken from the GPU path.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+import paper_2604_07815_amd as tls
+import synth
+from oracle import tls_oracle as O
+
+NEAR_TIE_REL = 1e-3
+TOL = {"bf16": dict(rtol=2e-2, atol=2e-2), "f32": dict(rtol=1e-5, atol=1e-5)}
+
+
+def torch_dtype(cfg):
+    return torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+
+
+class Case:
+    """One synthetic decode workload resident on the GPU, plus host views."""
+
+    def __init__(self, cfg: synth.DecodeConfig, backend: str = "host", pad: str = "nan", q_store=None,
+                 ctx_lens=None):
+        self.cfg = cfg
+        self.backend = backend
+        dev = "cuda"
+        if backend == "host":
+            d = synth.make_host(cfg, pad=pad, q_store=q_store, ctx_lens=ctx_lens)
+            self.host = d
+            self.q = synth.host_to_torch(d["q"], cfg.dtype).to(dev)
+            self.k = synth.host_to_torch(d["k"], cfg.dtype).to(dev)
+            self.v = None if d["v"] is None else synth.host_to_torch(d["v"], cfg.dtype).to(dev)
+            self.ctx_host = d["ctx_lens"]
+            self.ch_host = d["channels"]
+            self.plant_starts = d["plant_starts"]
+            self.q_store = d["q"]
+        else:
+            d = synth.make_device(cfg, device=dev, pad=pad, q_store=q_store, ctx_lens=ctx_lens)
+            self.host = None
+            self.q, self.k, self.v = d["q"], d["k"], d["v"]
+            self.ctx_host = d["ctx_host"]
+            self.ch_host = d["channels_host"]
+            self.plant_starts = d["plant_starts"]
+            self.q_store = d["q_host"]
+        self.ctx = torch.from_numpy(self.ctx_host).to(dev)
+        self.ch = torch.from_numpy(self.ch_host).to(dev)
+        self.layout = tls.make_layout(cfg.batch, cfg.h_q, cfg.h_kv, cfg.d_qk, cfg.d_v, cfg.max_ctx,
+                                      index_channels=cfg.d_c, block_size=cfg.block,
+                                      dtype=tls.DTYPE_BF16 if cfg.dtype == "bf16" else tls.DTYPE_F32,
+                                      mla_shared_kv=cfg.mla)
+        self.m_max = -(-cfg.max_ctx // cfg.block)
+        self._unit_cache = {}
+
+    # --- GPU side ------------------------------------------------------------
+    def build_index(self):
+        cfg = self.cfg
+        dt = torch_dtype(cfg)
+        self.kmax = torch.empty((cfg.batch, cfg.h_kv, self.m_max, cfg.d_qk), dtype=dt, device="cuda")
+        self.kmin = torch.empty_like(self.kmax)
+        self.codes = torch.empty((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 2), dtype=torch.uint8,
+                                 device="cuda")
+        self.qparams = torch.empty((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 32, 2),
+                                   dtype=torch.float32, device="cuda")
+        tls.tls_build_block_index(self.layout, self.k, self.ctx, 0, cfg.max_ctx, self.kmax, self.kmin)
+        tls.tls_build_token_index(self.layout, self.k, self.ctx, self.ch, 0, cfg.max_ctx, self.codes,
+                                  self.qparams)
+        return self
+
+    def workspace(self, k_b=None, k_t=None):
+        cfg = self.cfg
+        return tls.alloc_workspace(self.layout, k_b or cfg.k_b, k_t or cfg.k_t)
+
+    def kv(self):
+        return tls.KV(self.k, self.v)
+
+    def decode(self, k_b=None, k_t=None, q=None, block_ids_in=None, token_ids_in=None, ws=None,
+               attn_splits=0, kv=None):
+        cfg = self.cfg
+        k_b, k_t = k_b or cfg.k_b, k_t or cfg.k_t
+        ws = ws if ws is not None else self.workspace(k_b, k_t)
+        q = self.q if q is None else q
+        out = torch.empty((cfg.batch, cfg.h_q, cfg.d_v), dtype=torch_dtype(cfg), device="cuda")
+        lse = torch.empty((cfg.batch, cfg.h_q), dtype=torch.float32, device="cuda")
+        bids = torch.empty((cfg.batch, cfg.h_kv, k_b), dtype=torch.int32, device="cuda")
+        tids = torch.empty((cfg.batch, cfg.h_kv, k_t), dtype=torch.int32, device="cuda")
+        sel = token_ids_in is None
+        tls.tls_sparse_decode(self.layout, q, kv or self.kv(), self.ctx,
+                              self.kmax if sel else None, self.kmin if sel else None,
+                              self.codes if sel else None, self.qparams if sel else None,
+                              self.ch if sel else None, k_b, k_t, block_ids_in, token_ids_in, out, lse,
+                              bids if (sel and block_ids_in is None) else None, tids if sel else None, ws,
+                              attn_splits=attn_splits)
+        torch.cuda.synchronize()
+        return dict(out=out, lse=lse, bids=bids if (sel and block_ids_in is None) else None,
+                    tids=tids if sel else None, ws=ws)
+
+    # --- host (oracle) side ----------------------------------------------------
+    def q_f64(self, q_store=None):
+        return synth.to_f64(self.q_store if q_store is None else q_store, self.cfg.dtype)
+
+    def unit_kv_f64(self, s, g):
+        key = (s, g)
+        if key not in self._unit_cache:
+            cfg = self.cfg
+            if self.host is not None:
+                Ku = synth.to_f64(self.host["k"][s, g], cfg.dtype)
+                Vu = Ku[:, :cfg.d_v] if cfg.mla else synth.to_f64(self.host["v"][s, g], cfg.dtype)
+            else:
+                Ku = synth.torch_to_f64(self.k[s, g])
+                Vu = Ku[:, :cfg.d_v] if cfg.mla else synth.torch_to_f64(self.v[s, g])
+            self._unit_cache[key] = (Ku, Vu)
+        return self._unit_cache[key]
+
+    def oracle_unit(self, s, g, k_b=None, k_t=None, q_store=None, block_ids=None, token_ids=None):
+        cfg = self.cfg
+        k_b, k_t = k_b or cfg.k_b, k_t or cfg.k_t
+        q = self.q_f64(q_store)
+        qg = q[s, g * cfg.group:(g + 1) * cfg.group]
+        Ku, Vu = self.unit_kv_f64(s, g)
+        n = int(self.ctx_host[s])
+        return O.decode_unit(qg, Ku, Vu, n, self.ch_host[g], k_b, k_t, cfg.block, cfg.sigma,
+                             block_ids=block_ids, token_ids=token_ids)
+
+    def units(self, sample=None, seed=0):
+        cfg = self.cfg
+        allu = [(s, g) for s in range(cfg.batch) for g in range(cfg.h_kv)]
+        if sample is None or sample >= len(allu):
+            return allu
+        r = np.random.default_rng(seed)
+        pick = {allu[0], allu[-1]}
+        # include the longest and the shortest sequence
+        smax, smin = int(np.argmax(self.ctx_host)), int(np.argmin(self.ctx_host))
+        pick |= {(smax, 0), (smin, cfg.h_kv - 1)}
+        while len(pick) < sample:
+            pick.add(allu[int(r.integers(len(allu)))])
+        return sorted(pick)
+
+
+# --- comparisons -----------------------------------------------------------------
+
+def valid_ids(ids_row: np.ndarray) -> np.ndarray:
+    ids_row = np.asarray(ids_row)
+    k = int((ids_row >= 0).sum())
+    assert np.all(ids_row[:k] >= 0) and np.all(ids_row[k:] == -1), "ids must be a valid prefix then -1"
+    v = ids_row[:k]
+    assert np.all(np.diff(v) > 0), "ids must be strictly ascending"
+    return v
+
+
+def check_selection(gpu_ids, ora_ids, score_of, what: str, rel: float = NEAR_TIE_REL):
+    """Equal sets, except ids whose oracle score lies within rel*|s_k| of the
+    oracle's k-th score (near ties).  Returns the number of swapped ids."""
+    g = set(int(x) for x in valid_ids(gpu_ids))
+    o = set(int(x) for x in ora_ids)
+    assert len(g) == len(o), f"{what}: GPU picked {len(g)} ids, oracle {len(o)}"
+    diff = g ^ o
+    if not diff:
+        return 0
+    kth = min(score_of(i) for i in o)
+    for i in diff:
+        assert abs(score_of(i) - kth) <= rel * abs(kth), (
+            f"{what}: id {i} score {score_of(i)!r} vs k-th {kth!r} is not a near tie")
+    return len(diff) // 2
+
+
+def check_close(gpu, ref, dtype: str, what: str):
+    tol = TOL[dtype]
+    gpu = np.asarray(gpu, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    np.testing.assert_allclose(gpu, ref, err_msg=what, **tol)
+
+
+def alpha_lookup(res):
+    pos = {int(t): i for i, t in enumerate(res["cand"])}
+    alpha = res["alpha"]
+    return lambda t: float(alpha[pos[int(t)]])
+
+
+def compare_unit(case: Case, gpu: dict, s: int, g: int, k_b=None, k_t=None, q_store=None,
+                 check_out=True):
+    """End-to-end comparison of one unit; returns the oracle result."""
+    cfg = case.cfg
+    ref = case.oracle_unit(s, g, k_b, k_t, q_store=q_store)
+    sw_b = check_selection(gpu["bids"][s, g].cpu().numpy(), ref["block_ids"],
+                           lambda i: float(ref["block_scores"][i]), f"blocks unit {(s, g)}")
+    if sw_b:
+        return ref  # a near-tie swap upstream changes the candidate set; ids were validated
+    sw_t = check_selection(gpu["tids"][s, g].cpu().numpy(), ref["token_ids"], alpha_lookup(ref),
+                           f"tokens unit {(s, g)}")
+    if sw_t or not check_out:
+        return ref
+    G = cfg.group
+    out = gpu["out"][s, g * G:(g + 1) * G].float().cpu().numpy()
+    lse = gpu["lse"][s, g * G:(g + 1) * G].cpu().numpy()
+    check_close(out, ref["out"], cfg.dtype, f"out unit {(s, g)}")
+    check_close(lse, ref["lse"], cfg.dtype, f"lse unit {(s, g)}")
+    return ref

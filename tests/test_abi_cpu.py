@@ -1,0 +1,125 @@
+"""The C-ABI library loads, exports every symbol include/tls.h declares, and
+its host-side validation rejects bad arguments before any GPU work (these
+calls never reach the device, so they run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tls.h")
+LIB = os.path.join(ROOT, "paper_2604_07815_amd", "libtls.so")
+
+
+@pytest.fixture(scope="module")
+def tls():
+    if not os.path.exists(LIB):
+        from paper_2604_07815_amd import build as b
+        b.build()
+    import paper_2604_07815_amd as t
+    return t
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:tls_status|const char\*)\s+(tls_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ["tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
+              "tls_sparse_decode", "tls_prefetch_blocks", "tls_workspace_size", "tls_check_device_error"]:
+        assert n in names, n
+
+
+def test_library_exports_every_declared_symbol(tls):
+    lib = ctypes.CDLL(LIB)
+    for n in declared_functions():
+        assert hasattr(lib, n), f"libtls.so does not export {n}"
+    assert set(declared_functions()) == set(tls.EXPORTED_SYMBOLS)
+
+
+def test_version_and_status_strings(tls):
+    assert "gfx950" in tls.tls_version()
+    assert tls.tls_status_string(0) == "TLS_OK"
+    assert tls.tls_status_string(3) == "TLS_ERR_WORKSPACE_TOO_SMALL"
+
+
+def _layout(tls, **kw):
+    base = dict(batch=2, num_q_heads=32, num_kv_heads=8, head_dim_qk=128, head_dim_v=128, max_ctx=4096,
+                index_channels=32, block_size=64, dtype=tls.DTYPE_BF16)
+    base.update(kw)
+    return tls.make_layout(**base)
+
+
+def test_workspace_size_is_host_only_and_grows_with_budgets(tls):
+    a = tls.tls_workspace_size(_layout(tls), 8, 128)
+    b = tls.tls_workspace_size(_layout(tls), 128, 2048)
+    assert 0 < a < b
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(num_q_heads=30), 1),           # H_q not a multiple of H_kv
+    (dict(index_channels=48), 1),        # d_c not a multiple of 32
+    (dict(index_channels=256), 1),       # d_c > d_qk
+    (dict(dtype=7), 1),                  # unknown dtype
+    (dict(block_size=32), 2),            # only B = 64 is compiled
+    (dict(max_ctx=64 * 20000), 2),       # more blocks than the top-k capacity
+    (dict(head_dim_qk=100, head_dim_v=100), 2),
+])
+def test_bad_layouts(tls, kw, code):
+    with pytest.raises(tls.TlsError) as e:
+        tls.tls_workspace_size(_layout(tls, **kw), 8, 128)
+    assert e.value.status == code
+
+
+def test_bad_budgets(tls):
+    for kb, kt, code in [(0, 128, 1), (8, 0, 1), (300, 128, 2)]:
+        with pytest.raises(tls.TlsError) as e:
+            tls.tls_workspace_size(_layout(tls), kb, kt)
+        assert e.value.status == code
+
+
+def _raw(tls):
+    return tls._lib
+
+
+def test_null_pointers_are_rejected_before_launch(tls):
+    lib = _raw(tls)
+    L = _layout(tls)
+    dummy = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    null = None
+    # missing K
+    assert lib.tls_build_block_index(ctypes.byref(L), null, dummy, 0, 64, dummy, dummy, null) == 1
+    # tok_end beyond max_ctx
+    assert lib.tls_build_block_index(ctypes.byref(L), dummy, dummy, 0, 5000, dummy, dummy, null) == 1
+    # workspace too small
+    assert lib.tls_select_blocks(ctypes.byref(L), dummy, dummy, dummy, dummy, 8, dummy, null, dummy, 16,
+                                 null) == 3
+    # GQA decode without V
+    kv = tls.KvView(dummy.value, None, None, 0)
+    opts = tls.DecodeOpts()
+    st = lib.tls_sparse_decode(ctypes.byref(L), dummy, ctypes.byref(kv), dummy, dummy, dummy, dummy, dummy,
+                               dummy, 8, 128, null, null, dummy, null, null, null, dummy, 1 << 40,
+                               ctypes.byref(opts), null)
+    assert st == 1
+    # reserved option fields must be zero
+    kv = tls.KvView(dummy.value, dummy.value, None, 0)
+    opts.reserved[2] = 5
+    st = lib.tls_sparse_decode(ctypes.byref(L), dummy, ctypes.byref(kv), dummy, dummy, dummy, dummy, dummy,
+                               dummy, 8, 128, null, null, dummy, null, null, null, dummy, 1 << 40,
+                               ctypes.byref(opts), null)
+    assert st == 1
+    # MLA layout must not pass V
+    Lm = _layout(tls, num_kv_heads=1, head_dim_qk=576, head_dim_v=512, index_channels=128, mla_shared_kv=True)
+    opts.reserved[2] = 0
+    st = lib.tls_sparse_decode(ctypes.byref(Lm), dummy, ctypes.byref(kv), dummy, dummy, dummy, dummy, dummy,
+                               dummy, 8, 128, null, null, dummy, null, null, null, dummy, 1 << 40,
+                               ctypes.byref(opts), null)
+    assert st == 1
+    # pool too small for the live + new sets
+    st = lib.tls_prefetch_blocks(ctypes.byref(L), dummy, dummy, dummy, dummy, dummy, 8, dummy, dummy, 10,
+                                 dummy, dummy, null, dummy, 1 << 40, null)
+    assert st == 1
