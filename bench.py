@@ -198,7 +198,12 @@ def main():
 
     layer = dict(q=d["q"], k=d["k"], v=d["v"], kmax=kmax, kmin=kmin, codes=codes, qparams=qparams)
     per_layer = sum(t.numel() * t.element_size() for t in layer.values() if t is not None)
-    copies = args.copies or max(1, min(8, math.ceil(2 * 512e6 / max(1.0, per_layer * 0.04)) if per_layer < 2e9 else 2))
+    # touched bytes per step (upper estimate) -> enough copies that a rotation
+    # spans at least twice the 256 MiB Infinity Cache, within a memory budget
+    m_hi = -(-int(d["ctx_host"].max()) // cfg.block)
+    units = cfg.batch * cfg.h_kv
+    touched = units * (m_hi * 2 * cfg.d_qk * e + cfg.k_b * cfg.block * 24 + cfg.k_t * (cfg.d_qk + cfg.d_v) * e)
+    copies = args.copies or int(min(64, max(2, math.ceil(2 * 2 ** 28 / touched)), max(2, 60e9 // per_layer)))
     layers = [layer] + [{k: (None if t is None else t.clone()) for k, t in layer.items()} for _ in range(copies - 1)]
     ctx_t, ch_t = d["ctx_lens"], d["channels"]
     ws = tls.alloc_workspace(layout, cfg.k_b, cfg.k_t, device=dev)

@@ -6,178 +6,9 @@
 // ranges; each work-group gathers its rows, keeps an online softmax per head
 // and writes a normalised partial output plus its log-sum-exp; merge_kernel
 // combines the partials exactly: o = sum_s e^{lse_s - M} o_s / sum_s e^{lse_s - M}.
-#include "kernels.hpp"
+#include "attn_common.hpp"
 
 namespace tls {
-
-template <class S>
-__device__ inline const S* kv_row(const S* base, const int32_t* slot_map, int64_t n_slots, size_t unit, int T,
-                                  int B, int m_max, int d, int tok, bool* ok) {
-  if (!slot_map) return base + (unit * size_t(T) + size_t(tok)) * d;
-  const int slot = slot_map[unit * size_t(m_max) + tok / B];
-  if (slot < 0 || slot >= n_slots) {
-    *ok = false;
-    return base;
-  }
-  return base + ((unit * size_t(n_slots) + size_t(slot)) * B + tok % B) * d;
-}
-
-__device__ inline float exp_or_zero(float x) { return x == -INFINITY ? 0.f : expf(x); }
-
-// ---------------------------------------------------------------------------
-// GQA: one row group of LPR = D/VEC lanes per token row; each lane owns VEC
-// channels of q (all G heads, pre-scaled by sigma) and of the output.
-// ---------------------------------------------------------------------------
-template <class E, int D, int G>
-__global__ __launch_bounds__(256) void attn_gqa_kernel(
-    const typename E::T* __restrict__ q, const typename E::T* __restrict__ Kp,
-    const typename E::T* __restrict__ Vp, const int32_t* __restrict__ slot_map, int64_t n_slots,
-    const int32_t* __restrict__ token_ids, const int32_t* __restrict__ ctx_lens, int H_q, int H_kv, int T,
-    int B, int m_max, int K_t, int ct, float sigma, float* __restrict__ po, float* __restrict__ plse,
-    uint32_t* err) {
-  using S = typename E::T;
-  constexpr int V = E::kVec;
-  constexpr int LPR = D / V;
-  constexpr int RG = 256 / LPR;
-  constexpr int RPW = 64 / LPR;
-  constexpr int U = 4;
-  __shared__ float s_m[4][G], s_l[4][G];
-  __shared__ float s_acc[4][G][D];
-
-  const int unit = blockIdx.y, split = blockIdx.x, nsplit = gridDim.x;
-  const int s = unit / H_kv, g = unit % H_kv;
-  int n = ctx_lens[s];
-  n = n < 0 ? 0 : (n > T ? T : n);
-  const int li = threadIdx.x % LPR, rg = threadIdx.x / LPR;
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-
-  float qr[G][V];
-  {
-    const S* qg = q + (size_t(s) * H_q + size_t(g) * G) * D;
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      unpack16<E>(ld16(qg + size_t(h) * D + li * V), qr[h]);
-#pragma unroll
-      for (int e = 0; e < V; ++e) qr[h][e] *= sigma;
-    }
-  }
-  float m[G], l[G], acc[G][V];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    m[h] = -INFINITY;
-    l[h] = 0.f;
-#pragma unroll
-    for (int e = 0; e < V; ++e) acc[h][e] = 0.f;
-  }
-
-  const int p0 = split * ct, p1 = min(K_t, p0 + ct);
-  const int32_t* ids = token_ids + size_t(unit) * K_t;
-  for (int pb = p0 + rg; pb < p1; pb += RG * U) {
-    uint4 kv[U], vv[U];
-    bool ok[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int p = pb + u * RG;
-      ok[u] = false;
-      kv[u] = vv[u] = make_uint4(0, 0, 0, 0);
-      if (p < p1) {
-        const int tok = ids[p];
-        if (tok >= 0) {
-          if (tok >= n) {
-            if (li == 0) set_error(err, 4u);
-          } else {
-            bool good = true;
-            const S* kr = kv_row(Kp, slot_map, n_slots, unit, T, B, m_max, D, tok, &good);
-            const S* vr = kv_row(Vp, slot_map, n_slots, unit, T, B, m_max, D, tok, &good);
-            if (good) {
-              kv[u] = ld16_stream(kr + li * V);
-              vv[u] = ld16_stream(vr + li * V);
-              ok[u] = true;
-            } else if (li == 0) {
-              set_error(err, 8u);
-            }
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float kf[V];
-      unpack16<E>(kv[u], kf);
-      float z[G];
-#pragma unroll
-      for (int h = 0; h < G; ++h) {
-        float dot = 0.f;
-#pragma unroll
-        for (int e = 0; e < V; ++e) dot = fmaf(qr[h][e], kf[e], dot);
-        z[h] = wave_sum<LPR>(dot);
-      }
-      if (ok[u]) {
-        float vf[V];
-        unpack16<E>(vv[u], vf);
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          const float mn = fmaxf(m[h], z[h]);
-          const float a = exp_or_zero(m[h] - mn);
-          const float p = expf(z[h] - mn);
-          m[h] = mn;
-          l[h] = l[h] * a + p;
-#pragma unroll
-          for (int e = 0; e < V; ++e) acc[h][e] = fmaf(p, vf[e], acc[h][e] * a);
-        }
-      }
-    }
-  }
-  // combine the row groups of a wave
-#pragma unroll
-  for (int off = LPR; off < 64; off <<= 1) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mo = __shfl_xor(m[h], off, 64);
-      const float lo = __shfl_xor(l[h], off, 64);
-      const float M = fmaxf(m[h], mo);
-      const float a = M == -INFINITY ? 0.f : exp_or_zero(m[h] - M);
-      const float b = M == -INFINITY ? 0.f : exp_or_zero(mo - M);
-      m[h] = M;
-      l[h] = l[h] * a + lo * b;
-#pragma unroll
-      for (int e = 0; e < V; ++e) {
-        const float ao = __shfl_xor(acc[h][e], off, 64);
-        acc[h][e] = acc[h][e] * a + ao * b;
-      }
-    }
-  }
-  if (lane < LPR) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      if (li == 0) {
-        s_m[wid][h] = m[h];
-        s_l[wid][h] = l[h];
-      }
-#pragma unroll
-      for (int e = 0; e < V; ++e) s_acc[wid][h][li * V + e] = acc[h][e];
-    }
-  }
-  __syncthreads();
-  const size_t pbase = (size_t(unit) * nsplit + split) * G;
-  for (int i = threadIdx.x; i < G * D; i += 256) {
-    const int h = i / D, dd = i % D;
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_m[w][h]);
-    float L = 0.f, O = 0.f;
-    if (M != -INFINITY) {
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float a = exp_or_zero(s_m[w][h] - M);
-        L += s_l[w][h] * a;
-        O += s_acc[w][h][dd] * a;
-      }
-    }
-    po[(pbase + h) * D + dd] = L > 0.f ? O / L : 0.f;
-    if (dd == 0) plse[pbase + h] = L > 0.f ? M + logf(L) : -INFINITY;
-  }
-}
 
 // ---------------------------------------------------------------------------
 // Absorbed MLA (one shared latent row per token; V = K[:, :d_v]), bf16.
@@ -371,42 +202,24 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t v, size_t n, hipStream_t st) {
   return hipGetLastError();
 }
 
+int gqa_tokens_per_split(const Problem& P);
+hipError_t launch_attention_gqa(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+                                const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
+                                uint32_t* err, hipStream_t st);
+
+int attn_tokens_per_split(const Problem& P) { return P.mla ? kMlaCt : gqa_tokens_per_split(P); }
+
 int attn_splits_for(const Problem& P, int K_t, int requested) {
-  if (P.mla) return (K_t + kMlaCt - 1) / kMlaCt > kMaxSplits ? kMaxSplits : (K_t + kMlaCt - 1) / kMlaCt;
-  int ns = requested;
-  if (ns <= 0) {
-    // aim for >= 2048 work-groups with at least 32 tokens each
-    ns = 1;
-    while (ns < kMaxSplits && long(P.units) * ns < 2048 && K_t / (ns * 2) >= 32) ns *= 2;
+  const int cap = attn_tokens_per_split(P);
+  const int need = (K_t + cap - 1) / cap;  // fewest splits the work-group capacity allows
+  int ns = requested > 0 ? requested : need;
+  if (requested <= 0) {
+    // small batches: more, shorter splits so the launch fills the chip
+    while (ns * 2 <= kMaxSplits && long(P.units) * ns < 1024 && K_t / (ns * 2) >= 32) ns *= 2;
   }
-  if (ns > kMaxSplits) ns = kMaxSplits;
+  if (ns < need) ns = need;
   if (ns > K_t) ns = K_t;
   return ns < 1 ? 1 : ns;
-}
-
-template <class E, int D, int G>
-static void launch_gqa_t(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
-                         const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse, uint32_t* err,
-                         hipStream_t st) {
-  using S = typename E::T;
-  const int ct = (K_t + nsplit - 1) / nsplit;
-  dim3 grid(nsplit, P.units);
-  attn_gqa_kernel<E, D, G><<<grid, 256, 0, st>>>((const S*)q, (const S*)kv.k, (const S*)kv.v, kv.slot_map,
-                                                 kv.n_slots, token_ids, ctx_lens, P.H_q, P.H_kv, P.T, P.B,
-                                                 P.m_max, K_t, ct, P.sigma, po, plse, err);
-}
-
-template <class E, int D>
-static bool launch_gqa_d(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
-                         const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse, uint32_t* err,
-                         hipStream_t st) {
-  switch (P.G) {
-    case 1: launch_gqa_t<E, D, 1>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
-    case 2: launch_gqa_t<E, D, 2>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
-    case 4: launch_gqa_t<E, D, 4>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
-    case 8: launch_gqa_t<E, D, 8>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
-    default: return false;
-  }
 }
 
 hipError_t launch_attention(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
@@ -420,16 +233,7 @@ hipError_t launch_attention(const Problem& P, const void* q, const KvView& kv, c
                                           P.m_max, K_t, ct, P.sigma, po, plse, err);
     return hipGetLastError();
   }
-  bool ok = false;
-  if (P.dtype == 1) {
-    if (P.d_qk == 128) ok = launch_gqa_d<BF16, 128>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
-    else if (P.d_qk == 64) ok = launch_gqa_d<BF16, 64>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
-  } else {
-    if (P.d_qk == 128) ok = launch_gqa_d<F32, 128>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
-    else if (P.d_qk == 64) ok = launch_gqa_d<F32, 64>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
-  }
-  if (!ok) return hipErrorInvalidValue;
-  return hipGetLastError();
+  return launch_attention_gqa(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
 }
 
 hipError_t launch_merge(const Problem& P, const float* po, const float* plse, int nsplit, void* out, float* lse,

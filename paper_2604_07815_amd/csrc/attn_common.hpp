@@ -1,0 +1,66 @@
+// Helpers shared by the attention kernels.
+#pragma once
+
+#include "kernels.hpp"
+
+namespace tls {
+
+// Address of token `tok`'s row in the direct layout [units][T][d] or, with a
+// slot map, in the block pool [units][n_slots][B][d].  *ok turns false when
+// the token's block is not resident.
+template <class S>
+__device__ inline const S* kv_row(const S* base, const int32_t* slot_map, int64_t n_slots, size_t unit, int T,
+                                  int B, int m_max, int d, int tok, bool* ok) {
+  if (!slot_map) return base + (unit * size_t(T) + size_t(tok)) * d;
+  const int slot = slot_map[unit * size_t(m_max) + tok / B];
+  if (slot < 0 || slot >= n_slots) {
+    *ok = false;
+    return base;
+  }
+  return base + ((unit * size_t(n_slots) + size_t(slot)) * B + tok % B) * d;
+}
+
+__device__ inline float exp_or_zero(float x) { return x == -INFINITY ? 0.f : expf(x); }
+
+// Transposing butterfly all-reduce over the MASK*2 lanes of a lane group:
+// while more than one value is left, each xor step sends half of the values
+// to the partner lane and keeps the other half, so NV values are reduced with
+// NV - 1 shuffles instead of NV*log2(W).  On return v[j] holds the fully
+// reduced value of original index xreduce_index<NV, W>(lane, j), for
+// j < max(1, NV / W).
+template <int NV, int MASK>
+struct XReduce {
+  __device__ static inline void run(float* v, int lane) {
+    if constexpr (MASK == 0) {
+      return;
+    } else if constexpr (NV > 1) {
+      constexpr int H = NV / 2;
+      const bool upper = (lane & MASK) != 0;
+#pragma unroll
+      for (int j = 0; j < H; ++j) {
+        const float send = upper ? v[j] : v[j + H];
+        const float keep = upper ? v[j + H] : v[j];
+        v[j] = keep + __shfl_xor(send, MASK, 64);
+      }
+      XReduce<H, MASK / 2>::run(v, lane);
+    } else {
+      v[0] += __shfl_xor(v[0], MASK, 64);
+      XReduce<1, MASK / 2>::run(v, lane);
+    }
+  }
+};
+
+template <int NV, int W>
+__device__ inline int xreduce_index(int lane, int j) {
+  int idx = j, cur = NV;
+#pragma unroll
+  for (int mask = W / 2; mask > 0; mask >>= 1) {
+    if (cur > 1) {
+      cur >>= 1;
+      if (lane & mask) idx += cur;
+    }
+  }
+  return idx;
+}
+
+}  // namespace tls

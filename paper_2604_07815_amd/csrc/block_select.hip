@@ -99,23 +99,24 @@ __global__ __launch_bounds__(256) void block_score_kernel(
 }
 
 // One work-group per unit: stage the unit's scores as keys in LDS, select.
-__global__ __launch_bounds__(256) void block_topk_kernel(const float* __restrict__ scores,
+__global__ __launch_bounds__(1024) void block_topk_kernel(const float* __restrict__ scores,
                                                           const int32_t* __restrict__ ctx_lens, int H_kv,
                                                           int T, int B, int m_max, int K_b,
                                                           int32_t* __restrict__ block_ids) {
   extern __shared__ uint32_t smem[];
-  uint32_t* hist = smem;
-  uint32_t* keys = smem + 288;
+  uint32_t* scratch = smem;
+  int32_t* stage = reinterpret_cast<int32_t*>(smem + topk_scratch_words(1024));
+  uint32_t* keys = smem + topk_scratch_words(1024) + K_b;
   const int unit = blockIdx.x;
   const int s = unit / H_kv;
   int n = ctx_lens[s];
   n = n < 0 ? 0 : (n > T ? T : n);
   const int m = (n + B - 1) / B;
   const float* sc = scores + size_t(unit) * m_max;
-  for (int i = threadIdx.x; i < m; i += 256) keys[i] = float_key(sc[i]);
+  for (int i = threadIdx.x; i < m; i += 1024) keys[i] = float_key(sc[i]);
   __syncthreads();
-  wg_topk_ascending<256>(keys, m, K_b, block_ids + size_t(unit) * K_b, K_b, nullptr,
-                         [](int i) { return int32_t(i); }, hist);
+  wg_topk_ascending<1024>(keys, m, K_b, block_ids + size_t(unit) * K_b, K_b, nullptr,
+                         [](int i) { return int32_t(i); }, scratch, stage, nullptr);
 }
 
 template <class E, int LPB, int CPL>
@@ -152,8 +153,8 @@ hipError_t launch_block_score(const Problem& P, const void* q, const void* kmax,
 hipError_t launch_block_topk(const Problem& P, const float* scores, const int32_t* ctx_lens, int K_b,
                              int32_t* block_ids, uint32_t* err, hipStream_t st) {
   (void)err;
-  const size_t lds = (288 + size_t(P.m_max)) * sizeof(uint32_t);
-  block_topk_kernel<<<P.units, 256, lds, st>>>(scores, ctx_lens, P.H_kv, P.T, P.B, P.m_max, K_b, block_ids);
+  const size_t lds = (topk_scratch_words(1024) + size_t(K_b) + size_t(P.m_max)) * sizeof(uint32_t);
+  block_topk_kernel<<<P.units, 1024, lds, st>>>(scores, ctx_lens, P.H_kv, P.T, P.B, P.m_max, K_b, block_ids);
   return hipGetLastError();
 }
 

@@ -114,131 +114,12 @@ __device__ inline float key_float(uint32_t k) {
   return __uint_as_float(u);
 }
 
-// ---------------------------------------------------------------------------
-// Work-group top-k over keys held in LDS.
-//
-// Selects the k largest keys among keys[0, n) (kInvalidKey entries never
-// count), ties resolved toward the lower position, and writes
-// map(position) for the selected positions in ascending position order to
-// out[0, k'), k' = min(k, #valid), then -1 up to out_cap.  If out_scores is
-// non-null it receives key_float of each selected key.
-//
-// Method: MSB-first radix select (4 passes of 8 bits, histograms in LDS)
-// finds the k'-th largest key T and how many keys equal to T are taken
-// (the lowest positions first); an ordered compaction then emits, in
-// position order, every key > T plus the first r keys == T.  No sort is
-// needed because the output is ordered by position.
-//
-// Scratch: `hist` holds 256 + 32 uint32; `NT` is the work-group size.
-// ---------------------------------------------------------------------------
-template <int NT, class Map>
-__device__ void wg_topk_ascending(const uint32_t* keys, int n, int k, int32_t* out, int out_cap,
-                                  float* out_scores, Map map, uint32_t* hist) {
-  constexpr int NW = NT / kWave;
-  const int tid = threadIdx.x;
-  const int lane = tid & (kWave - 1);
-  const int wid = tid / kWave;
-  uint32_t* wsum = hist + 256;  // per-wave partials (NW <= 16) + broadcast slots
-
-  // count valid keys
-  int cnt = 0;
-  for (int i = tid; i < n; i += NT) cnt += keys[i] != kInvalidKey;
-  for (int o = kWave / 2; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, kWave);
-  if (lane == 0) wsum[wid] = cnt;
-  __syncthreads();
-  int n_valid = 0;
-  for (int w = 0; w < NW; ++w) n_valid += wsum[w];
-  const int kk = min(k, n_valid);
-  __syncthreads();
-
-  uint32_t prefix = 0, pmask = 0;
-  int remaining = kk;
-  if (kk > 0) {
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int i = tid; i < 256; i += NT) hist[i] = 0;
-      __syncthreads();
-      for (int i = tid; i < n; i += NT) {
-        uint32_t key = keys[i];
-        if (key != kInvalidKey && (key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
-      }
-      __syncthreads();
-      if (wid == 0) {
-        // lane L owns digits 255-4L .. 252-4L (descending); suffix-scan from the top
-        uint32_t c[4];
-        uint32_t local = 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) { c[j] = hist[255 - 4 * lane - j]; local += c[j]; }
-        uint32_t incl = local;
-#pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) {
-          uint32_t t = __shfl_up(incl, o, kWave);
-          if (lane >= o) incl += t;
-        }
-        uint32_t above = incl - local;  // keys with larger digits than this lane's range
-        // find the digit where the cumulative count first reaches `remaining`
-        uint32_t run = above;
-        int found = -1;
-        uint32_t found_above = 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          if (found < 0 && run + c[j] >= uint32_t(remaining)) { found = 255 - 4 * lane - j; found_above = run; }
-          run += c[j];
-        }
-        uint64_t hit = __ballot(found >= 0);
-        int src = __ffsll((unsigned long long)hit) - 1;  // the first (highest-digit) lane that hits
-        int dig = __shfl(found, src, kWave);
-        uint32_t ab = __shfl(found_above, src, kWave);
-        if (lane == 0) { wsum[16] = uint32_t(dig); wsum[17] = ab; }
-      }
-      __syncthreads();
-      uint32_t dig = wsum[16];
-      remaining -= int(wsum[17]);
-      prefix |= dig << shift;
-      pmask |= 255u << shift;
-      __syncthreads();
-    }
-  }
-  const uint32_t T = prefix;
-  const int r = remaining;  // number of keys equal to T to take (lowest positions)
-
-  // ordered compaction, one tile of NT positions at a time
-  int gt_base = 0, eq_base = 0;
-  if (kk > 0) {
-    for (int base = 0; base < n; base += NT) {
-      int i = base + tid;
-      uint32_t key = i < n ? keys[i] : kInvalidKey;
-      bool gt = key != kInvalidKey && key > T;
-      bool eq = key != kInvalidKey && key == T;
-      uint64_t bg = __ballot(gt), be = __ballot(eq);
-      if (lane == 0) { wsum[wid] = __popcll(bg); wsum[NW + wid] = __popcll(be); }
-      __syncthreads();
-      int gb = gt_base, eb = eq_base, gtot = 0, etot = 0;
-      for (int w = 0; w < NW; ++w) {
-        int g = wsum[w], e = wsum[NW + w];
-        if (w < wid) { gb += g; eb += e; }
-        gtot += g; etot += e;
-      }
-      gb += lanes_below(bg);
-      eb += lanes_below(be);
-      if (gt || (eq && eb < r)) {
-        int pos = gb + min(eb, r);
-        out[pos] = map(i);
-        if (out_scores) out_scores[pos] = key_float(key);
-      }
-      gt_base += gtot;
-      eq_base += etot;
-      __syncthreads();
-    }
-  }
-  for (int i = kk + tid; i < out_cap; i += NT) {
-    out[i] = -1;
-    if (out_scores) out_scores[i] = 0.0f;
-  }
-}
-
 // Device error word (first 4 bytes of the workspace).
 __device__ inline void set_error(uint32_t* err, uint32_t bit) {
   if (err) atomicOr(err, bit);
 }
 
 }  // namespace tls
+
+// Work-group top-k selection (keys in registers, LDS histograms).
+#include "topk.hpp"

@@ -52,12 +52,22 @@ hipError_t launch_token_alpha(const Problem& P, const float* logits, const float
 hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32_t* block_ids, int K_b,
                              int K_t, int32_t* token_ids, float* token_scores, hipStream_t st);
 
+// One work-group per unit: (optional) block top-k from block_scores, then the
+// whole token selection on chip.  Valid when fused_token_select_ok().
+bool fused_token_select_ok(const Problem& P, int K_b, int K_t);
+hipError_t launch_token_select_fused(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,
+                                     const int32_t* channels, const float* block_scores,
+                                     const int32_t* block_ids_in, int32_t* block_ids_out, const int32_t* ctx_lens,
+                                     int K_b, int K_t, int32_t* token_ids, float* token_scores, uint32_t* err,
+                                     hipStream_t st);
+
 struct KvView {
   const void* k;
   const void* v;
   const int32_t* slot_map;
   int64_t n_slots;
 };
+int attn_tokens_per_split(const Problem& P);  // token capacity of one attention work-group
 int attn_splits_for(const Problem& P, int K_t, int requested);
 hipError_t launch_attention(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
                             const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,

@@ -62,11 +62,11 @@ tls_status check_budgets(const Problem& P, int K_b, int K_t) {
 tls_status check_attention(const Problem& P, int K_t) {
   if (P.mla) {
     if (P.dtype != TLS_DTYPE_BF16 || P.d_qk > 576 || P.d_v > 512 || P.d_v % 2 != 0) return TLS_ERR_UNSUPPORTED;
-    if (K_t > 32 * tls::kMaxSplits) return TLS_ERR_UNSUPPORTED;
-    return TLS_OK;
+  } else {
+    if (P.d_qk != P.d_v || (P.d_qk != 128 && P.d_qk != 64)) return TLS_ERR_UNSUPPORTED;
+    if (P.G != 1 && P.G != 2 && P.G != 4 && P.G != 8) return TLS_ERR_UNSUPPORTED;
   }
-  if (P.d_qk != P.d_v || (P.d_qk != 128 && P.d_qk != 64)) return TLS_ERR_UNSUPPORTED;
-  if (P.G != 1 && P.G != 2 && P.G != 4 && P.G != 8) return TLS_ERR_UNSUPPORTED;
+  if (long(K_t) > long(tls::kMaxSplits) * tls::attn_tokens_per_split(P)) return TLS_ERR_UNSUPPORTED;
   return TLS_OK;
 }
 
@@ -205,8 +205,26 @@ tls_status tls_select_tokens(const tls_layout* layout, const void* q, const uint
   if (st != TLS_OK) return st;
   const tls::Workspace W = tls::plan_workspace(P, K_b, K_t);
   if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  if (tls::fused_token_select_ok(P, K_b, K_t))
+    return hip_status(tls::launch_token_select_fused(P, q, codes, qparams, channels, nullptr, block_ids, nullptr,
+                                                     ctx_lens, K_b, K_t, token_ids, token_scores, err_word(ws),
+                                                     stream));
   return hip_status(run_token_select(P, W, q, codes, qparams, channels, block_ids, K_b, ctx_lens, K_t, token_ids,
                                      token_scores, ws, stream, nullptr));
+}
+
+// Attention over the selected tokens and the split merge (stages 6 and 7).
+static tls_status finish_decode(const Problem& P, const tls::Workspace& W, const void* q, const tls_kv_view* kv,
+                                const int32_t* ctx_lens, int K_t, const int32_t* tids, void* out, float* lse,
+                                void* ws, int requested, hipEvent_t* ev, hipStream_t stream) {
+  const int nsplit = tls::attn_splits_for(P, K_t, requested);
+  tls::KvView view{kv->k, kv->v, kv->slot_map, kv->n_slots};
+  hipError_t e = tls::launch_attention(P, q, view, tids, ctx_lens, K_t, nsplit, at<float>(ws, W.po),
+                                       at<float>(ws, W.plse), err_word(ws), stream);
+  if (ev) hipEventRecord(ev[6], stream);
+  if (e == hipSuccess) e = tls::launch_merge(P, at<float>(ws, W.po), at<float>(ws, W.plse), nsplit, out, lse, stream);
+  if (ev) hipEventRecord(ev[7], stream);
+  return hip_status(e);
 }
 
 tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_kv_view* kv, const int32_t* ctx_lens,
@@ -251,6 +269,27 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
   };
   mark(0);
   const int32_t* bids = block_ids_in;
+  if (sel_tokens && tls::fused_token_select_ok(P, K_b, K_t)) {
+    // block score, then one kernel for block top-k + token selection; the
+    // token-score stage events bracket the fused kernel
+    int32_t* to = token_ids_out ? token_ids_out : at<int32_t>(ws, W.tids);
+    const float* bsc = nullptr;
+    if (sel_blocks) {
+      e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.bscores), err_word(ws), stream);
+      bsc = at<float>(ws, W.bscores);
+    }
+    mark(1);
+    mark(2);
+    if (e == hipSuccess)
+      e = tls::launch_token_select_fused(P, q, codes, qparams, channels, bsc, block_ids_in,
+                                         sel_blocks ? block_ids_out : nullptr, ctx_lens, K_b, K_t, to, nullptr,
+                                         err_word(ws), stream);
+    mark(3);
+    mark(4);
+    mark(5);
+    if (e != hipSuccess) return TLS_ERR_HIP;
+    return finish_decode(P, W, q, kv, ctx_lens, K_t, to, out, lse, ws, requested, ev, stream);
+  }
   if (sel_blocks) {
     int32_t* bo = block_ids_out ? block_ids_out : at<int32_t>(ws, W.bids);
     e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.bscores), err_word(ws), stream);
@@ -274,14 +313,7 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
   }
   mark(5);
   if (e != hipSuccess) return TLS_ERR_HIP;
-  const int nsplit = tls::attn_splits_for(P, K_t, requested);
-  tls::KvView view{kv->k, kv->v, kv->slot_map, kv->n_slots};
-  e = tls::launch_attention(P, q, view, tids, ctx_lens, K_t, nsplit, at<float>(ws, W.po), at<float>(ws, W.plse),
-                            err_word(ws), stream);
-  mark(6);
-  if (e == hipSuccess) e = tls::launch_merge(P, at<float>(ws, W.po), at<float>(ws, W.plse), nsplit, out, lse, stream);
-  mark(7);
-  return hip_status(e);
+  return finish_decode(P, W, q, kv, ctx_lens, K_t, tids, out, lse, ws, requested, ev, stream);
 }
 
 tls_status tls_prefetch_blocks(const tls_layout* layout, const void* host_k, const void* host_v,

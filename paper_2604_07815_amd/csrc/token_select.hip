@@ -14,35 +14,12 @@
 // token_alpha_kernel: per-head normalisers over all candidates, then
 //   alpha_j = (1/G) sum_h exp(l_hj - m_h) / Z_h as an orderable key.
 // token_topk_kernel: the K_t largest alpha, ascending token positions.
-#include "kernels.hpp"
+#include "token_common.hpp"
 
 namespace tls {
 
 constexpr int kMaxG = 32;
 constexpr int kMaxGroups = 8;  // d_c <= 256
-
-__device__ inline void unpack_nibbles8(uint32_t w, float* f) {
-  const uint32_t lo = w & 0x0f0f0f0fu, hi = (w >> 4) & 0x0f0f0f0fu;
-  f[0] = float(lo & 0xffu);         f[1] = float(hi & 0xffu);
-  f[2] = float((lo >> 8) & 0xffu);  f[3] = float((hi >> 8) & 0xffu);
-  f[4] = float((lo >> 16) & 0xffu); f[5] = float((hi >> 16) & 0xffu);
-  f[6] = float(lo >> 24);           f[7] = float(hi >> 24);
-}
-
-__device__ inline bool slot_token(const int32_t* bl, int K_b, int B, int m, int n, int slot, int* tok,
-                                  uint32_t* err) {
-  const int i = slot / B, o = slot % B;
-  if (i >= K_b) return false;
-  const int blk = bl[i];
-  if (blk < 0) return false;
-  if (blk >= m) {
-    set_error(err, 2u);
-    return false;
-  }
-  const int t = blk * B + o;
-  *tok = t;
-  return t < n;
-}
 
 template <class E>
 __global__ __launch_bounds__(256) void token_score_kernel(
@@ -197,17 +174,20 @@ __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __rest
                                                            int B, int K_t, int32_t* __restrict__ token_ids,
                                                            float* __restrict__ token_scores) {
   extern __shared__ uint32_t smem[];
-  uint32_t* hist = smem;
-  int32_t* s_bl = reinterpret_cast<int32_t*>(smem + 288);
-  uint32_t* s_keys = smem + 288 + K_b;
-  const int unit = blockIdx.x;
+  uint32_t* scratch = smem;
+  int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(1024));
   const int S = K_b * B;
+  uint32_t* s_keys = smem + topk_scratch_words(1024) + K_b;
+  int32_t* stage = reinterpret_cast<int32_t*>(s_keys + S);
+  float* stage_sc = reinterpret_cast<float*>(stage + K_t);
+  const int unit = blockIdx.x;
   for (int i = threadIdx.x; i < K_b; i += 1024) s_bl[i] = block_ids[size_t(unit) * K_b + i];
   for (int i = threadIdx.x; i < S; i += 1024) s_keys[i] = keys[size_t(unit) * S + i];
   __syncthreads();
   wg_topk_ascending<1024>(s_keys, S, K_t, token_ids + size_t(unit) * K_t, K_t,
                           token_scores ? token_scores + size_t(unit) * K_t : nullptr,
-                          [=](int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, hist);
+                          [=](int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch, stage,
+                          stage_sc);
 }
 
 hipError_t launch_token_score(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,
@@ -238,7 +218,13 @@ hipError_t launch_token_alpha(const Problem& P, const float* logits, const float
 
 hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32_t* block_ids, int K_b,
                              int K_t, int32_t* token_ids, float* token_scores, hipStream_t st) {
-  const size_t lds = (288 + size_t(K_b) + size_t(K_b) * P.B) * sizeof(uint32_t);
+  const size_t lds =
+      (topk_scratch_words(1024) + size_t(K_b) + size_t(K_b) * P.B + 2 * size_t(K_t)) * sizeof(uint32_t);
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(token_topk_kernel),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (e != hipSuccess) return e;
+  }
   token_topk_kernel<<<P.units, 1024, lds, st>>>(keys, block_ids, K_b, P.B, K_t, token_ids, token_scores);
   return hipGetLastError();
 }
