@@ -203,6 +203,7 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t v, size_t n, hipStream_t st) {
 }
 
 int gqa_tokens_per_split(const Problem& P);
+int gqa_auto_splits(const Problem& P, int K_t);
 hipError_t launch_attention_gqa(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
                                 const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
                                 uint32_t* err, hipStream_t st);
@@ -213,7 +214,10 @@ int attn_splits_for(const Problem& P, int K_t, int requested) {
   const int cap = attn_tokens_per_split(P);
   const int need = (K_t + cap - 1) / cap;  // fewest splits the work-group capacity allows
   int ns = requested > 0 ? requested : need;
-  if (requested <= 0) {
+  const int tuned = (requested <= 0 && !P.mla) ? gqa_auto_splits(P, K_t) : 0;
+  if (tuned > 0) {
+    ns = tuned;
+  } else if (requested <= 0) {
     // small batches: more, shorter splits so the launch fills the chip
     while (ns * 2 <= kMaxSplits && long(P.units) * ns < 1024 && K_t / (ns * 2) >= 32) ns *= 2;
   }

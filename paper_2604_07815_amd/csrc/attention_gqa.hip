@@ -3,13 +3,13 @@
 //   o_h = softmax(sigma q_h K_S^T) V_S,   lse_h = log sum_j exp(sigma q_h . k_j)
 // for the G query heads of each (sequence, KV head) unit.
 //
-// One work-group handles CT consecutive entries of a unit's token list.
-// A row group of LPR = D/VEC lanes owns one token row at a time (VEC channels
-// per lane, 16-byte loads), and owns TPR = 8 tokens.  Every K and V row of the
-// work-group is requested before any arithmetic, so each work-group waits on
-// memory once.  Scores are reduced across the row group with a transposing
-// butterfly, normalised once per (head, token) in LDS against the
-// work-group's per-head max, and P.V is accumulated in registers.  The
+// One work-group handles `tpw` consecutive entries of a unit's token list in
+// chunks of 64 tokens.  The chunk's K and V rows are gathered straight into
+// LDS with global_load_lds_dwordx4 (one 16-byte piece per lane, rows picked
+// per lane), double-buffered: while a chunk is consumed the next one is in
+// flight, and only LDS-side waits separate the stages.  Per chunk: scores
+// (row groups of LPR lanes, reduced with a transposing butterfly), an online
+// softmax update per head, then P.V into register accumulators.  The
 // work-group writes its normalised partial output and log-sum-exp; the merge
 // kernel combines the splits.  HBM-bound: (d_qk + d_v) * sizeof(elem) bytes
 // per token.
@@ -17,11 +17,40 @@
 
 namespace tls {
 
-constexpr int kGqaTPR = 8;
+constexpr int kAttnCT = 64;      // tokens per chunk
+constexpr int kAttnMaxTPW = 512;  // tokens per work-group (fp32 kernel)
+constexpr int kAttnMaxTPWBf16 = 1024;  // tokens per work-group (bf16 matrix-core kernel)
+constexpr int kAttnNW = 4;             // waves per work-group (bf16 matrix-core kernel)
 
-template <class E, int D>
-constexpr int gqa_ct() {
-  return (256 / (D / E::kVec)) * kGqaTPR;
+// s_waitcnt immediates (gfx9 encoding): vmcnt in [3:0] and [15:14],
+// expcnt in [6:4], lgkmcnt in [11:8].
+__host__ __device__ constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int kWaitLgkm0 = 0xC07F;
+
+// Work-group barrier for LDS traffic only: completes this wave's LDS
+// accesses, then synchronises, leaving global loads (including the
+// asynchronous LDS gathers of the next chunk) in flight.  The
+// wavefront-scope fences keep the compiler from moving memory accesses
+// across it.
+__device__ inline void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Asynchronous 16-byte-per-lane gather into LDS: lane i reads 16 bytes at
+// `src` and the wave writes them to lds + 16*i.  Issued through inline asm so
+// that the compiler does not order later LDS accesses behind it; completion
+// is tracked explicitly with s_waitcnt vmcnt and a work-group barrier before
+// the data is read, and the target buffer is not read or rewritten while a
+// gather into it is in flight.
+__device__ inline void gather16_to_lds(const void* src, const void* lds) {
+  // the LDS destination is wave-uniform; readfirstlane puts it in an SGPR
+  const uint32_t off = uint32_t(__builtin_amdgcn_readfirstlane(int(reinterpret_cast<uintptr_t>((lds_void*)lds))));
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(off), "v"(src) : "m0");
 }
 
 template <class E, int D, int G>
@@ -29,53 +58,67 @@ __global__ __launch_bounds__(256) void attn_gqa_kernel(
     const typename E::T* __restrict__ q, const typename E::T* __restrict__ Kp,
     const typename E::T* __restrict__ Vp, const int32_t* __restrict__ slot_map, int64_t n_slots,
     const int32_t* __restrict__ token_ids, const int32_t* __restrict__ ctx_lens, int H_q, int H_kv, int T,
-    int B, int m_max, int K_t, int ct, float sigma, float* __restrict__ po, float* __restrict__ plse,
+    int B, int m_max, int K_t, int tpw, float sigma, float* __restrict__ po, float* __restrict__ plse,
     uint32_t* err) {
   using S = typename E::T;
-  constexpr int V = E::kVec;
-  constexpr int LPR = D / V;          // lanes per token row
-  constexpr int RG = 256 / LPR;       // row groups per work-group
-  constexpr int RPW = 64 / LPR;       // row groups per wave
-  constexpr int TPR = kGqaTPR;        // tokens per row group
-  constexpr int CT = RG * TPR;        // token capacity of a work-group
-  constexpr int NZ = TPR * G;         // (token, head) scores per row group
+  constexpr int V = E::kVec;                // elements per 16-byte piece
+  constexpr int ROWB = D * int(sizeof(S));  // bytes per K or V row
+  constexpr int LPR = ROWB / 16;            // lanes per row
+  constexpr int RPI = 64 / LPR;             // rows per wave-wide gather = row groups per wave
+  constexpr int CT = kAttnCT;
+  constexpr int RPW = CT / 4;               // rows per wave per chunk
+  constexpr int NI = RPW / RPI;             // gathers per wave per chunk, for K and again for V
+  constexpr int TPG = NI;                   // rows per row group per chunk
+  constexpr int NZ = TPG * G;
   constexpr int NRES = NZ / LPR > 0 ? NZ / LPR : 1;
+  static_assert(LPR * 16 == ROWB && RPI * LPR == 64 && NI * RPI == RPW, "row geometry");
+  __shared__ __attribute__((aligned(16))) uint8_t sK0[CT * ROWB];
+  __shared__ __attribute__((aligned(16))) uint8_t sV0[CT * ROWB];
+  __shared__ __attribute__((aligned(16))) uint8_t sK1[CT * ROWB];
+  __shared__ __attribute__((aligned(16))) uint8_t sV1[CT * ROWB];
   __shared__ float s_z[G][CT];
-  __shared__ float s_m[G], s_l[G];
-  __shared__ float s_acc[4][G * D];
+  __shared__ float s_m[G], s_l[G], s_sc[G];
 
   const int unit = blockIdx.y, split = blockIdx.x, nsplit = gridDim.x;
   const int s = unit / H_kv, g = unit % H_kv;
-  const int tid = threadIdx.x, li = tid % LPR, rg = tid / LPR, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int li = lane % LPR, rgi = lane / LPR;
   int n = ctx_lens[s];
   n = n < 0 ? 0 : (n > T ? T : n);
-  const int p0 = split * ct, p1 = min(K_t, p0 + ct);
-  const int32_t* ids = token_ids + size_t(unit) * K_t;
+  const int p0 = split * tpw;
+  const int cnt = max(0, min(tpw, K_t - p0));
+  const int nch = (cnt + CT - 1) / CT;
+  const int32_t* ids = token_ids + size_t(unit) * K_t + p0;
 
-  // token rows of this row group, then every K/V load
-  uint4 kv[TPR], vv[TPR];
-  uint32_t okmask = 0;
+  // this lane's gather rows for every chunk (row index within the unit's K/V
+  // base, -1: skip); the lane's row group scores exactly these rows
+  constexpr int NCH = kAttnMaxTPW / CT;
+  int rreg[NCH][NI];
 #pragma unroll
-  for (int i = 0; i < TPR; ++i) {
-    const int p = p0 + rg + RG * i;
-    kv[i] = vv[i] = make_uint4(0, 0, 0, 0);
-    const int tok = p < p1 ? ids[p] : -1;
-    if (tok >= 0) {
-      if (tok >= n) {
-        if (li == 0) set_error(err, 4u);
-      } else {
-        bool good = true;
-        const S* kr = kv_row(Kp, slot_map, n_slots, unit, T, B, m_max, D, tok, &good);
-        const S* vr = kv_row(Vp, slot_map, n_slots, unit, T, B, m_max, D, tok, &good);
-        if (good) {
-          kv[i] = ld16_stream(kr + li * V);
-          vv[i] = ld16_stream(vr + li * V);
-          okmask |= 1u << i;
-        } else if (li == 0) {
-          set_error(err, 8u);
+  for (int c = 0; c < NCH; ++c)
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int idx = c * CT + wid * RPW + i * RPI + rgi;
+      int row = -1;
+      if (idx < cnt) {
+        const int tok = ids[idx];
+        if (tok >= n) {
+          if (li == 0) set_error(err, 4u);
+        } else if (tok >= 0) {
+          if (!slot_map) {
+            row = tok;
+          } else {
+            const int slot = slot_map[size_t(unit) * m_max + tok / B];
+            if (slot >= 0 && slot < n_slots) row = slot * B + tok % B;
+            else if (li == 0) set_error(err, 8u);
+          }
         }
       }
+      rreg[c][i] = row;
     }
+  if (tid < G) {
+    s_m[tid] = -INFINITY;
+    s_l[tid] = 0.f;
   }
   float qr[G][V];
   {
@@ -87,90 +130,484 @@ __global__ __launch_bounds__(256) void attn_gqa_kernel(
       for (int e = 0; e < V; ++e) qr[h][e] *= sigma;
     }
   }
-  // partial dot products, reduced across the row group
-  float z[NZ];
-#pragma unroll
-  for (int i = 0; i < TPR; ++i) {
-    float kf[V];
-    unpack16<E>(kv[i], kf);
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float dot = 0.f;
-#pragma unroll
-      for (int e = 0; e < V; ++e) dot = fmaf(qr[h][e], kf[e], dot);
-      z[i * G + h] = dot;
-    }
-  }
-  XReduce<NZ, LPR / 2>::run(z, li);
-#pragma unroll
-  for (int j = 0; j < NRES; ++j) {
-    const int idx = xreduce_index<NZ, LPR>(li, j);
-    const int i = idx / G, h = idx % G;
-    s_z[h][rg + RG * i] = ((okmask >> i) & 1u) ? z[j] : -INFINITY;
-  }
+  const S* Kb = Kp + (slot_map ? size_t(unit) * size_t(n_slots) * B : size_t(unit) * T) * D;
+  const S* Vb = Vp + (slot_map ? size_t(unit) * size_t(n_slots) * B : size_t(unit) * T) * D;
   __syncthreads();
-  // per-head max and exponentials over the work-group's tokens
-  for (int h = wid; h < G; h += 4) {
-    float mx = -INFINITY;
-    for (int t = lane; t < CT; t += 64) mx = fmaxf(mx, s_z[h][t]);
-    mx = wave_max<64>(mx);
-    float sum = 0.f;
-    for (int t = lane; t < CT; t += 64) {
-      const float p = mx == -INFINITY ? 0.f : exp_or_zero(s_z[h][t] - mx);
-      s_z[h][t] = p;
-      sum += p;
+
+  auto issue = [&](const int (&rows)[NI], uint8_t* bk, uint8_t* bv) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = wid * RPW + i * RPI;  // first row of this gather within the chunk
+      const int row = rows[i];
+      const size_t off = size_t(row < 0 ? 0 : row) * D + li * V;  // skipped rows read row 0 (masked later)
+      gather16_to_lds(Kb + off, bk + r * ROWB);
+      gather16_to_lds(Vb + off, bv + r * ROWB);
     }
-    sum = wave_sum<64>(sum);
-    if (lane == 0) {
-      s_m[h] = mx;
-      s_l[h] = sum;
-    }
-  }
-  __syncthreads();
-  // P.V for this row group's tokens
+  };
+
   float acc[G][V];
 #pragma unroll
   for (int h = 0; h < G; ++h)
 #pragma unroll
     for (int e = 0; e < V; ++e) acc[h][e] = 0.f;
+
+  // one chunk: wait for it, score, softmax update, P.V; prefetch the next
+  auto step = [&](const int c, const int (&rows)[NI], const int (&next)[NI], const uint8_t* bk, const uint8_t* bv,
+                  uint8_t* nk, uint8_t* nv) {
+    if (c + 1 < nch) {
+      issue(next, nk, nv);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NI));  // chunk c has landed
+    } else {
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    }
+    lds_barrier();
+    uint32_t okmask = 0;
+    float z[NZ];
 #pragma unroll
-  for (int i = 0; i < TPR; ++i) {
-    float vf[V];
-    unpack16<E>(vv[i], vf);
+    for (int j = 0; j < TPG; ++j) {
+      const int row = wid * RPW + j * RPI + rgi;
+      if (rows[j] >= 0) okmask |= 1u << j;
+      float kf[V];
+      unpack16<E>(*reinterpret_cast<const uint4*>(bk + row * ROWB + li * 16), kf);
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float dot = 0.f;
+#pragma unroll
+        for (int e = 0; e < V; ++e) dot = fmaf(qr[h][e], kf[e], dot);
+        z[j * G + h] = dot;
+      }
+    }
+    XReduceDpp<NZ, LPR>::run(z, li);
+#pragma unroll
+    for (int jj = 0; jj < NRES; ++jj) {
+      const int idx = xreduce_index<NZ, LPR>(li, jj);
+      const int j = idx / G, h = idx % G;
+      s_z[h][wid * RPW + j * RPI + rgi] = ((okmask >> j) & 1u) ? z[jj] : -INFINITY;
+    }
+    lds_barrier();
+    // online softmax update, one wave per head
+    for (int h = wid; h < G; h += 4) {
+      const float zz = s_z[h][lane];
+      const float cmax = wave_max_f32(zz);
+      const float m_old = s_m[h];
+      const float m_new = fmaxf(m_old, cmax);
+      const float p = zz == -INFINITY ? 0.f : expf(zz - m_new);
+      const float csum = wave_sum_f32(p);
+      s_z[h][lane] = p;
+      if (lane == 0) {
+        const float sc = m_old == -INFINITY ? 0.f : expf(m_old - m_new);
+        s_sc[h] = sc;
+        s_m[h] = m_new;
+        s_l[h] = s_l[h] * sc + csum;
+      }
+    }
+    lds_barrier();
+    // P.V into the register accumulators
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const float p = s_z[h][rg + RG * i];
+      const float sc = s_sc[h];
 #pragma unroll
-      for (int e = 0; e < V; ++e) acc[h][e] = fmaf(p, vf[e], acc[h][e]);
+      for (int e = 0; e < V; ++e) acc[h][e] *= sc;
+    }
+#pragma unroll
+    for (int j = 0; j < TPG; ++j) {
+      if ((okmask >> j) & 1u) {
+        const int row = wid * RPW + j * RPI + rgi;
+        float vf[V];
+        unpack16<E>(*reinterpret_cast<const uint4*>(bv + row * ROWB + li * 16), vf);
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          const float p = s_z[h][row];
+#pragma unroll
+          for (int e = 0; e < V; ++e) acc[h][e] = fmaf(p, vf[e], acc[h][e]);
+        }
+      }
+    }
+    lds_barrier();  // chunk buffers and scores free for reuse
+  };
+  if (nch > 0) issue(rreg[0], sK0, sV0);
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    if (c < nch) {
+      const int cn = c + 1 < NCH ? c + 1 : c;
+      if ((c & 1) == 0) step(c, rreg[c], rreg[cn], sK0, sV0, sK1, sV1);
+      else step(c, rreg[c], rreg[cn], sK1, sV1, sK0, sV0);
     }
   }
+  // combine the row groups of a wave, then the four waves through LDS
 #pragma unroll
   for (int mask = LPR; mask < 64; mask <<= 1)
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
       for (int e = 0; e < V; ++e) acc[h][e] += __shfl_xor(acc[h][e], mask, 64);
+  float* s_acc = reinterpret_cast<float*>(sK0);  // 4 * G * D floats fit in the chunk buffers
+  static_assert(4 * G * D * 4 <= CT * ROWB, "accumulator staging fits in one chunk buffer");
   if (lane < LPR) {
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
-      for (int e = 0; e < V; ++e) s_acc[wid][h * D + li * V + e] = acc[h][e];
+      for (int e = 0; e < V; ++e) s_acc[(wid * G + h) * D + li * V + e] = acc[h][e];
   }
   __syncthreads();
   const size_t pbase = (size_t(unit) * nsplit + split) * G;
   for (int idx = tid; idx < G * D; idx += 256) {
     const int h = idx / D;
-    const float o = (s_acc[0][idx] + s_acc[1][idx]) + (s_acc[2][idx] + s_acc[3][idx]);
+    const float o = (s_acc[idx] + s_acc[G * D + idx]) + (s_acc[2 * G * D + idx] + s_acc[3 * G * D + idx]);
     const float L = s_l[h];
     po[pbase * D + idx] = L > 0.f ? o / L : 0.f;
     if (idx % D == 0) plse[pbase + h] = L > 0.f ? s_m[h] + logf(L) : -INFINITY;
   }
-  (void)RPW;
 }
 
-int gqa_tokens_per_split(const Problem& P) {
-  const int V = P.dtype == 1 ? 8 : 4;
-  return (256 / (P.d_qk / V)) * kGqaTPR;
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+
+// Compiler-level ordering point for LDS accesses around the inline-asm
+// gathers (emits no instruction at wavefront scope).
+__device__ inline void wave_fence() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
+
+// Max / sum over the lanes i, i^16, i^32, i^48 (one per DPP row) through the
+// gfx950 row-swap permutes; every lane gets the same bits.
+__device__ inline float xrows_max(float v) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ inline float xrows_sum(float v) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// bf16 grouped-query attention with both products on the matrix cores.
+//
+// Each wave owns a contiguous run of the work-group's token entries and walks
+// it in tiles of 16 tokens, so the waves never wait for each other inside the
+// loop.  Per tile:
+//   * the tile's 16 K rows and 16 V rows are gathered into the wave's LDS
+//     buffers with global_load_lds_dwordx4 (16 bytes per lane).  V is double
+//     buffered and requested a full tile ahead; K has one buffer, refilled as
+//     soon as the score product has read it.  Pieces are stored XOR-swizzled
+//     by row so that the operand reads below spread over the LDS banks;
+//   * transposed scores S^T = K Q^T by D/32 v_mfma_f32_16x16x32_bf16
+//     (A = the tile's K rows, B = the G query heads padded to 16 columns).
+//     Lane (g, i) then holds head i's scores of tokens 4g..4g+3, which is
+//     exactly the A-operand layout of the second product;
+//   * online softmax per head in base 2 (the running maximum is only raised
+//     when a tile exceeds it by more than 2^8, so the accumulators are
+//     rarely rescaled); the probabilities are rounded to bf16;
+//   * O += P V by D/16 v_mfma_f32_16x16x16_bf16, with the V operand read
+//     column-wise straight from the row-major tile by ds_read_b64_tr_b16.
+// At the end the waves' (max, sum, accumulator) triples are merged in LDS
+// and the work-group writes one normalised partial and its log-sum-exp.
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
+
+__device__ inline short bf16_bits_rne(float f) {
+  uint32_t u = __float_as_uint(f);  // finite, non-negative here
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return short(u >> 16);
+}
+
+template <int D, int G, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_gqa_mfma_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp, const uint16_t* __restrict__ Vp,
+    const int32_t* __restrict__ slot_map, int64_t n_slots, const int32_t* __restrict__ token_ids,
+    const int32_t* __restrict__ ctx_lens, int H_q, int H_kv, int T, int B, int m_max, int K_t, int tpw,
+    float sigma, float* __restrict__ po, float* __restrict__ plse, uint32_t* err) {
+  constexpr int ROWB = D * 2;     // bytes per K or V row
+  constexpr int LPR = ROWB / 16;  // 16-byte pieces per row
+  constexpr int RPI = 64 / LPR;   // rows per wave-wide gather
+  constexpr int CT = 16;          // tokens per tile
+  constexpr int NI = CT / RPI;    // gathers per tile, for K and again for V
+  constexpr int NKK = D / 32;     // score steps per tile
+  constexpr int NNT = D / 16;     // channel tiles of the output
+  constexpr int TPWV = kAttnMaxTPWBf16 / NW;
+  constexpr float kLog2e = 1.4426950408889634f;
+  constexpr float kRaise = 8.0f;  // base-2 headroom before the running maximum is raised
+  static_assert(G <= 8 && (D == 64 || D == 128) && NI * RPI == CT, "tile geometry");
+  __shared__ __attribute__((aligned(16))) uint8_t sK[NW][CT * ROWB];
+  __shared__ __attribute__((aligned(16))) uint8_t sV[NW][2][CT * ROWB];
+  __shared__ int s_rows[NW][TPWV];
+  __shared__ float s_ml[NW][2][8];
+
+  const int unit = blockIdx.y, split = blockIdx.x, nsplit = gridDim.x;
+  const int s = unit / H_kv, g = unit % H_kv;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int li = lane % LPR, rgi = lane / LPR;  // gather geometry
+  const int t = lane & 15, lg = lane >> 4;      // matrix-core geometry
+  int n = ctx_lens[s];
+  n = n < 0 ? 0 : (n > T ? T : n);
+  const int p0 = split * tpw;
+  const int cnt = max(0, min(tpw, K_t - p0));
+  const int tpwv = tpw / NW;
+  const int cw = max(0, min(tpwv, cnt - w * tpwv));
+  const int nch = (cw + CT - 1) / CT;
+
+  // resolve this wave's entries to rows of the unit's K/V base (-1: skip)
+  {
+    const int32_t* ids = token_ids + size_t(unit) * K_t + p0 + size_t(w) * tpwv;
+    for (int i = lane; i < nch * CT; i += 64) {
+      int row = -1;
+      if (i < cw) {
+        const int tok = ids[i];
+        if (tok >= n) {
+          set_error(err, 4u);
+        } else if (tok >= 0) {
+          if (!slot_map) {
+            row = tok;
+          } else {
+            const int slot = slot_map[size_t(unit) * m_max + tok / B];
+            if (slot >= 0 && slot < n_slots) row = slot * B + tok % B;
+            else set_error(err, 8u);
+          }
+        }
+      }
+      s_rows[w][i] = row;
+    }
+  }
+  // B operand of the score product: lane (lg, t) holds channels
+  // kk*32 + lg*8 .. +8 of head t (zero for padding heads)
+  bf16x8_t qb[NKK];
+  {
+    const uint16_t* qg = q + (size_t(s) * H_q + size_t(g) * G) * D;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      if (t < G) {
+        qb[kk] = *reinterpret_cast<const bf16x8_t*>(qg + size_t(t) * D + kk * 32 + lg * 8);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qb[kk][e] = __bf16(0.0f);
+      }
+    }
+  }
+  const size_t ubase = slot_map ? size_t(unit) * size_t(n_slots) * B : size_t(unit) * T;
+  const uint8_t* Kb = reinterpret_cast<const uint8_t*>(Kp + ubase * D);
+  const uint8_t* Vb = reinterpret_cast<const uint8_t*>(Vp + ubase * D);
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // prologue loads done before the gathers are counted
+  wave_fence();
+
+  // Tile c's 16-bit valid-token mask and this lane's gather rows; skipped
+  // entries are replaced by a valid row of the same tile (its probability is
+  // zero and its values are finite), or by row 0 when the tile has none (the
+  // tile is then not consumed).
+  struct Tile {
+    uint32_t mask;
+    int rows[NI];
+  };
+  auto tile_info = [&](const int c) {
+    Tile tl;
+    const int row_t = s_rows[w][c * CT + t];
+    int rows[NI];
+#pragma unroll
+    for (int j = 0; j < NI; ++j) rows[j] = s_rows[w][c * CT + j * RPI + rgi];
+    tl.mask = uint32_t(__builtin_amdgcn_ballot_w64(row_t >= 0)) & 0xffffu;
+    const int safe = tl.mask ? __builtin_amdgcn_readlane(row_t, __builtin_ctz(tl.mask)) : 0;
+#pragma unroll
+    for (int j = 0; j < NI; ++j) tl.rows[j] = rows[j] < 0 ? safe : rows[j];
+    return tl;
+  };
+  auto issue_v = [&](const Tile& tl, const int b) {
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const int r = j * RPI + rgi;
+      gather16_to_lds(Vb + size_t(tl.rows[j]) * ROWB + (li ^ ((2 * r) % LPR)) * 16, &sV[w][b][j * 1024]);
+    }
+  };
+  auto issue_k = [&](const Tile& tl) {
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const int r = j * RPI + rgi;
+      gather16_to_lds(Kb + size_t(tl.rows[j]) * ROWB + (li ^ (r % LPR)) * 16, &sK[w][j * 1024]);
+    }
+  };
+
+  f32x4_t acc[NNT];
+#pragma unroll
+  for (int nt = 0; nt < NNT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;  // head t, base-2 units
+  const float sl2 = sigma * kLog2e;
+  Tile cur = {};
+  if (nch > 0) {
+    cur = tile_info(0);
+    issue_v(cur, 0);
+    issue_k(cur);
+  }
+  for (int c = 0; c < nch; ++c) {
+    const int b = c & 1;
+    const bool more = c + 1 < nch;
+    Tile nxt = {};
+    wave_fence();
+    if (more) {
+      nxt = tile_info(c + 1);
+      issue_v(nxt, b ^ 1);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(NI));  // K and V of tile c have landed
+    } else {
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    }
+    wave_fence();
+    const uint32_t mask_cur = cur.mask;
+    // S^T: lane (lg, t) gets head t's scores of tokens 4lg + r
+    f32x4_t st = {0.f, 0.f, 0.f, 0.f};
+    if (mask_cur != 0u) {
+      bf16x8_t ka[NKK];
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk)
+        ka[kk] = *reinterpret_cast<const bf16x8_t*>(&sK[w][t * ROWB + (((kk * 4 + lg) ^ (t % LPR)) * 16)]);
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[kk], qb[kk], st, 0, 0, 0);
+    }
+    // the K buffer is free once its reads have returned: refill it
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    wave_fence();
+    if (more) issue_k(nxt);
+    wave_fence();
+    if (mask_cur != 0u) {
+      float z[4];
+      float cm = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        z[r] = ((mask_cur >> (lg * 4 + r)) & 1u) ? st[r] * sl2 : -INFINITY;
+        cm = fmaxf(cm, z[r]);
+      }
+      cm = xrows_max(cm);  // > -inf: the tile has a valid token
+      const float m_new = cm > m_run + kRaise ? cm : m_run;
+      const float sc = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      float ps = 0.f;
+      short pb[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = z[r] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(z[r] - m_new);
+        ps += p;
+        pb[r] = bf16_bits_rne(p);
+      }
+      l_run = l_run * sc + xrows_sum(ps);
+      // rescale the accumulators when a real head's maximum moved
+      if (__builtin_amdgcn_ballot_w64(t < G && m_new != m_run) != 0) {
+        float f[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          f[r] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sc), r));
+          if constexpr (G > 4) {
+            const float f1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sc), 4 + r));
+            f[r] = lg == 1 ? f1 : f[r];
+          }
+        }
+#pragma unroll
+        for (int nt = 0; nt < NNT; ++nt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[nt][r] *= f[r];
+      }
+      m_run = m_new;
+      const i16x4_t pa = {pb[0], pb[1], pb[2], pb[3]};
+      // O += P V; the V operand of channel tile nt for lane (lg, t) is
+      // rows 4lg + (t/4), channels 16nt + 4(t%4) .. +4, transposed on read
+      const int vr = lg * 4 + (t >> 2);
+#pragma unroll
+      for (int nt = 0; nt < NNT; ++nt) {
+        const int piece = 2 * nt + ((t & 3) >> 1);
+        const int off = vr * ROWB + ((piece ^ ((2 * vr) % LPR)) * 16) + (t & 1) * 8;
+        const i16x4_t vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(&sV[w][b][off]));
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, vb, acc[nt], 0, 0, 0);
+      }
+    }
+    cur = nxt;
+  }
+  // merge the waves through LDS: lane (lg, t) holds O rows (heads) 4lg + r,
+  // channel 16nt + t
+  __syncthreads();  // every wave is done with its tile buffers
+  float* s_acc = reinterpret_cast<float*>(&sV[0][0][0]);
+  static_assert(NW * G * D * 4 <= int(sizeof(sV)), "accumulator staging fits in the V buffers");
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int h = lg * 4 + r;
+    if (h < G) {
+#pragma unroll
+      for (int nt = 0; nt < NNT; ++nt) s_acc[(w * G + h) * D + nt * 16 + t] = acc[nt][r];
+    }
+  }
+  if (lg == 0 && t < G) {
+    s_ml[w][0][t] = m_run;
+    s_ml[w][1][t] = l_run;
+  }
+  __syncthreads();
+  const size_t pbase = (size_t(unit) * nsplit + split) * G;
+  for (int idx = threadIdx.x; idx < G * D; idx += 64 * NW) {
+    const int h = idx / D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) M = fmaxf(M, s_ml[v][0][h]);
+    float o = 0.f, L = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int v = 0; v < NW; ++v) {
+        const float f = __builtin_amdgcn_exp2f(s_ml[v][0][h] - M);
+        L += f * s_ml[v][1][h];
+        o += f * s_acc[(v * G) * D + idx];
+      }
+    }
+    po[pbase * D + idx] = L > 0.f ? o / L : 0.f;
+    if (idx % D == 0) plse[pbase + h] = L > 0.f ? (M + __log2f(L)) * 0.6931471805599453f : -INFINITY;
+  }
+}
+
+int gqa_tokens_per_split(const Problem& P) { return P.dtype == 1 ? kAttnMaxTPWBf16 : kAttnMaxTPW; }
+
+// Work-groups of the bf16 kernel resident per compute unit (LDS-bound).
+template <int D, int G>
+static int mfma_wgs_per_cu() {
+  static const int occ = [] {
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, attn_gqa_mfma_kernel<D, G, kAttnNW>, 64 * kAttnNW, 0) !=
+            hipSuccess ||
+        nb < 1)
+      nb = 1;
+    return nb;
+  }();
+  return occ;
+}
+
+template <int D>
+static int mfma_wgs_per_cu_g(int G) {
+  switch (G) {
+    case 1: return mfma_wgs_per_cu<D, 1>();
+    case 2: return mfma_wgs_per_cu<D, 2>();
+    case 4: return mfma_wgs_per_cu<D, 4>();
+    default: return mfma_wgs_per_cu<D, 8>();
+  }
+}
+
+// Split count for the bf16 kernel: the work-groups of one launch are
+// scheduled in rounds of (compute units x resident work-groups); pick the
+// split count that minimises rounds x (tokens per work-group + a fixed
+// per-work-group cost), fewest splits on ties.  0: not this kernel.
+int gqa_auto_splits(const Problem& P, int K_t) {
+  if (P.dtype != 1 || K_t < 1) return 0;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    cus = 256;
+  const int occ = P.d_qk == 64 ? mfma_wgs_per_cu_g<64>(P.G) : mfma_wgs_per_cu_g<128>(P.G);
+  const long slots = long(cus) * occ;
+  constexpr long kFixedTokens = 64;  // prologue and merge cost of one work-group, in tokens
+  const int step = 16 * kAttnNW;
+  const int need = (K_t + kAttnMaxTPWBf16 - 1) / kAttnMaxTPWBf16;
+  int best = need;
+  long best_cost = -1;
+  for (int ns = need; ns <= kMaxSplits; ++ns) {
+    const int tpw = ((K_t + ns - 1) / ns + step - 1) / step * step;
+    if (long(ns - 1) * tpw >= K_t) break;  // more splits would only add empty work-groups
+    const long rounds = (long(P.units) * ns + slots - 1) / slots;
+    const long cost = rounds * (tpw + kFixedTokens);
+    if (best_cost < 0 || cost < best_cost) {
+      best_cost = cost;
+      best = ns;
+    }
+  }
+  return best;
 }
 
 template <class E, int D, int G>
@@ -178,11 +615,20 @@ static void launch_t(const Problem& P, const void* q, const KvView& kv, const in
                      const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse, uint32_t* err,
                      hipStream_t st) {
   using S = typename E::T;
-  const int ct = (K_t + nsplit - 1) / nsplit;
   dim3 grid(nsplit, P.units);
-  attn_gqa_kernel<E, D, G><<<grid, 256, 0, st>>>((const S*)q, (const S*)kv.k, (const S*)kv.v, kv.slot_map,
-                                                 kv.n_slots, token_ids, ctx_lens, P.H_q, P.H_kv, P.T, P.B,
-                                                 P.m_max, K_t, ct, P.sigma, po, plse, err);
+  int tpw = (K_t + nsplit - 1) / nsplit;
+  if constexpr (E::kIsBf16) {
+    constexpr int step = 16 * kAttnNW;  // whole tiles for every wave
+    tpw = (tpw + step - 1) / step * step;
+    attn_gqa_mfma_kernel<D, G, kAttnNW><<<grid, 64 * kAttnNW, 0, st>>>(
+        (const uint16_t*)q, (const uint16_t*)kv.k, (const uint16_t*)kv.v, kv.slot_map, kv.n_slots, token_ids,
+        ctx_lens, P.H_q, P.H_kv, P.T, P.B, P.m_max, K_t, tpw, P.sigma, po, plse, err);
+  } else {
+    tpw = (tpw + kAttnCT - 1) / kAttnCT * kAttnCT;
+    attn_gqa_kernel<E, D, G><<<grid, 256, 0, st>>>((const S*)q, (const S*)kv.k, (const S*)kv.v, kv.slot_map,
+                                                   kv.n_slots, token_ids, ctx_lens, P.H_q, P.H_kv, P.T, P.B,
+                                                   P.m_max, K_t, tpw, P.sigma, po, plse, err);
+  }
 }
 
 template <class E, int D>

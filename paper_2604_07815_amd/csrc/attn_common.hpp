@@ -50,6 +50,48 @@ struct XReduce {
   }
 };
 
+// The same transposing reduction with the partner lane chosen by DPP mirror
+// patterns inside 16-lane rows (row_mirror, row_half_mirror, quad reverse,
+// quad swap): a VALU lane move instead of an LDS-routed shuffle.  Within a
+// group of W lanes the mirror partner has the opposite W/2 bit and the same
+// higher bits, so the kept halves and the resulting index map are those of
+// XReduce.  A 32-lane first step (W = 32) uses one xor-16 shuffle.
+template <int CTRL>
+__device__ inline float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+template <int W>
+__device__ inline float mirror_partner(float v) {
+  if constexpr (W == 32) return __shfl_xor(v, 16, 64);
+  else if constexpr (W == 16) return dpp_mov<0x140>(v);  // row_mirror
+  else if constexpr (W == 8) return dpp_mov<0x141>(v);   // row_half_mirror
+  else if constexpr (W == 4) return dpp_mov<0x1B>(v);    // quad_perm [3,2,1,0]
+  else return dpp_mov<0xB1>(v);                          // quad_perm [1,0,3,2]
+}
+
+template <int NV, int W>
+struct XReduceDpp {
+  __device__ static inline void run(float* v, int lane) {
+    if constexpr (W < 2) {
+      return;
+    } else if constexpr (NV > 1) {
+      constexpr int H = NV / 2;
+      const bool upper = (lane & (W / 2)) != 0;
+#pragma unroll
+      for (int j = 0; j < H; ++j) {
+        const float send = upper ? v[j] : v[j + H];
+        const float keep = upper ? v[j + H] : v[j];
+        v[j] = keep + mirror_partner<W>(send);
+      }
+      XReduceDpp<H, W / 2>::run(v, lane);
+    } else {
+      v[0] += mirror_partner<W>(v[0]);
+      XReduceDpp<1, W / 2>::run(v, lane);
+    }
+  }
+};
+
 template <int NV, int W>
 __device__ inline int xreduce_index(int lane, int j) {
   int idx = j, cur = NV;

@@ -106,7 +106,7 @@ __global__ __launch_bounds__(1024) void block_topk_kernel(const float* __restric
   extern __shared__ uint32_t smem[];
   uint32_t* scratch = smem;
   int32_t* stage = reinterpret_cast<int32_t*>(smem + topk_scratch_words(1024));
-  uint32_t* keys = smem + topk_scratch_words(1024) + K_b;
+  uint32_t* keys = smem + topk_scratch_words(1024) + align4w(K_b);
   const int unit = blockIdx.x;
   const int s = unit / H_kv;
   int n = ctx_lens[s];
@@ -153,7 +153,7 @@ hipError_t launch_block_score(const Problem& P, const void* q, const void* kmax,
 hipError_t launch_block_topk(const Problem& P, const float* scores, const int32_t* ctx_lens, int K_b,
                              int32_t* block_ids, uint32_t* err, hipStream_t st) {
   (void)err;
-  const size_t lds = (topk_scratch_words(1024) + size_t(K_b) + size_t(P.m_max)) * sizeof(uint32_t);
+  const size_t lds = (topk_scratch_words(1024) + size_t(align4w(K_b)) + size_t(P.m_max)) * sizeof(uint32_t);
   block_topk_kernel<<<P.units, 1024, lds, st>>>(scores, ctx_lens, P.H_kv, P.T, P.B, P.m_max, K_b, block_ids);
   return hipGetLastError();
 }

@@ -14,12 +14,14 @@ constexpr int kWave = 64;
 struct F32 {
   using T = float;
   static constexpr int kVec = 4;  // elements per 16-byte load
+  static constexpr bool kIsBf16 = false;
   __device__ static inline float to_f(T x) { return x; }
 };
 
 struct BF16 {
   using T = uint16_t;
   static constexpr int kVec = 8;
+  static constexpr bool kIsBf16 = true;
   __device__ static inline float to_f(T x) { return __uint_as_float(uint32_t(x) << 16); }
 };
 
@@ -94,6 +96,58 @@ __device__ inline int lane_id() { return __lane_id(); }
 // Number of set bits of `mask` in lanes below the calling lane.
 __device__ inline int lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi(uint32_t(mask >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(mask), 0));
+}
+
+// ---------------------------------------------------------------------------
+// Whole-wave reductions on DPP lane moves (VALU latency) plus four lane
+// reads, instead of LDS-routed shuffles.  Every lane of the wave must be
+// active.  The result is wave-uniform.
+//   quad_perm [1,0,3,2] / [2,3,0,1]: xor 1 / xor 2 inside a quad
+//   row_half_mirror / row_mirror: the other quad of 8 / the other 8 of 16
+// ---------------------------------------------------------------------------
+template <class Op>
+__device__ inline uint32_t wave_reduce_bits(uint32_t x, Op op) {
+  int v = int(x);
+  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false))));
+  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false))));
+  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false))));
+  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false))));
+  const uint32_t r0 = uint32_t(__builtin_amdgcn_readlane(v, 0)), r1 = uint32_t(__builtin_amdgcn_readlane(v, 16));
+  const uint32_t r2 = uint32_t(__builtin_amdgcn_readlane(v, 32)), r3 = uint32_t(__builtin_amdgcn_readlane(v, 48));
+  return op(op(r0, r1), op(r2, r3));
+}
+
+__device__ inline uint32_t wave_max_u32(uint32_t x) {
+  return wave_reduce_bits(x, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+}
+__device__ inline uint32_t wave_min_u32(uint32_t x) {
+  return wave_reduce_bits(x, [](uint32_t a, uint32_t b) { return a < b ? a : b; });
+}
+__device__ inline float wave_max_f32(float x) {
+  return __uint_as_float(wave_reduce_bits(__float_as_uint(x), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
+  }));
+}
+__device__ inline float wave_sum_f32(float x) {
+  return __uint_as_float(wave_reduce_bits(__float_as_uint(x), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+  }));
+}
+
+// Inclusive prefix sum over the wave of small non-negative integers
+// (v < 2^BITS), one ballot per bit; *total receives the wave sum.
+template <int BITS>
+__device__ inline uint32_t wave_incl_scan_small(uint32_t v, uint32_t* total) {
+  uint32_t incl = 0, tot = 0;
+#pragma unroll
+  for (int b = 0; b < BITS; ++b) {
+    const uint32_t bit = (v >> b) & 1u;
+    const uint64_t m = __ballot(bit != 0);
+    incl += (uint32_t(lanes_below(m)) + bit) << b;
+    tot += uint32_t(__popcll(m)) << b;
+  }
+  *total = tot;
+  return incl;
 }
 
 // ---------------------------------------------------------------------------

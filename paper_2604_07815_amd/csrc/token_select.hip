@@ -177,7 +177,7 @@ __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __rest
   uint32_t* scratch = smem;
   int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(1024));
   const int S = K_b * B;
-  uint32_t* s_keys = smem + topk_scratch_words(1024) + K_b;
+  uint32_t* s_keys = smem + topk_scratch_words(1024) + align4w(K_b);
   int32_t* stage = reinterpret_cast<int32_t*>(s_keys + S);
   float* stage_sc = reinterpret_cast<float*>(stage + K_t);
   const int unit = blockIdx.x;
@@ -219,7 +219,7 @@ hipError_t launch_token_alpha(const Problem& P, const float* logits, const float
 hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32_t* block_ids, int K_b,
                              int K_t, int32_t* token_ids, float* token_scores, hipStream_t st) {
   const size_t lds =
-      (topk_scratch_words(1024) + size_t(K_b) + size_t(K_b) * P.B + 2 * size_t(K_t)) * sizeof(uint32_t);
+      (topk_scratch_words(1024) + size_t(align4w(K_b)) + size_t(K_b) * P.B + 2 * size_t(K_t)) * sizeof(uint32_t);
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(token_topk_kernel),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));

@@ -62,7 +62,8 @@ static size_t region_words(int S, int K_t, int m_max) {
 }
 
 size_t mfma_select_lds_bytes(int S, int K_b, int K_t, int m_max) {
-  return (size_t(topk_scratch_words(kSelNT)) + 2 * size_t(K_b) + 4 + kSelNW * 4 + region_words(S, K_t, m_max)) *
+  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(2 * K_b)) + 4 + kSelNW * 4 +
+          region_words(S, K_t, m_max)) *
          sizeof(uint32_t);
 }
 
@@ -78,7 +79,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   uint32_t* scratch = smem;
   int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(NT));
   int32_t* s_bstage = s_bl + K_b;
-  float* s_qs = reinterpret_cast<float*>(s_bstage + K_b);  // [4]
+  float* s_qs = reinterpret_cast<float*>(s_bl + align4w(2 * K_b));  // [4]
   float* s_red = s_qs + 4;                                 // [NW][4]
   uint32_t* R = reinterpret_cast<uint32_t*>(s_red + NW * 4);
 
@@ -220,14 +221,16 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   }
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    const float w = wave_max<64>(mx[h]);
+    const float w = wave_max_f32(mx[h]);
     if (lane == 0) s_red[wid * 4 + h] = w;
   }
   __syncthreads();
 #pragma unroll
   for (int h = 0; h < G; ++h) {
+    const float v = s_red[(lane & 15) * 4 + h];
     float M = -INFINITY;
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, s_red[w * 4 + h]);
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, __uint_as_float(__builtin_amdgcn_readlane(__float_as_int(v), w)));
     mx[h] = M;
   }
   __syncthreads();
@@ -245,15 +248,17 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
     }
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    const float w = wave_sum<64>(sum[h]);
+    const float w = wave_sum_f32(sum[h]);
     if (lane == 0) s_red[wid * 4 + h] = w;
   }
   __syncthreads();
   float iz[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
+    const float v = s_red[(lane & 15) * 4 + h];
     float Z = 0.f;
-    for (int w = 0; w < NW; ++w) Z += s_red[w * 4 + h];
+#pragma unroll
+    for (int w = 0; w < NW; ++w) Z += __uint_as_float(__builtin_amdgcn_readlane(__float_as_int(v), w));
     iz[h] = Z > 0.f ? 1.0f / Z : 0.f;
   }
   // 4. alpha keys over R[0, S), top-K_t

@@ -8,18 +8,12 @@ namespace tls {
 constexpr int kTopkMaxEPT = 16;  // keys per thread: n <= NT * kTopkMaxEPT
 
 // LDS words the selection needs: four 256-bin histograms (one per radix
-// pass, cleared once up front) and two sets of broadcast slots.
+// pass, cleared once up front) and broadcast slots.
 __host__ __device__ constexpr int topk_scratch_words(int /*nt*/) { return 4 * 256 + 64 + 32; }
 
-__device__ inline uint32_t wave_incl_scan(uint32_t v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t t = __shfl_up(v, o, 64);
-    if (lane >= o) v += t;
-  }
-  return v;
-}
+// Round a count of 32-bit LDS words up to a multiple of 4 (16 bytes), so the
+// region that follows can be read with 16-byte accesses.
+__host__ __device__ constexpr int align4w(int words) { return (words + 3) & ~3; }
 
 // Selects the k largest keys among keys[0, n) (LDS; kInvalidKey entries never
 // count), ties resolved toward the lower position, and writes map(position)
@@ -28,14 +22,17 @@ __device__ inline uint32_t wave_incl_scan(uint32_t v) {
 // receives key_float of each selected key.  `stage` (LDS, out_cap ints) and
 // `stage_sc` (LDS, out_cap floats, when scores are wanted) hold the result
 // until one final copy, because a work-group barrier waits for outstanding
-// global stores.  Every thread of the work-group must call it.
+// global stores.  Every thread of the work-group must call it, with n and k
+// uniform.
 //
 // Method: each thread keeps the keys of positions [tid*ept, tid*ept + ept)
 // in registers.  An MSB-first radix select over the bits where the valid keys
 // differ (8-bit digits, LDS histograms) finds the k'-th largest key T and the
 // number r of keys equal to T to take; an ordered compaction (one prefix sum
 // of per-thread counts) then emits every key > T and the first r keys == T.
-// The output is ordered by position, so no sort is needed.
+// The output is ordered by position, so no sort is needed.  Wave-level
+// reductions and scans use DPP moves, ballots and lane reads; cross-wave
+// values go through one LDS word per wave.
 template <int NT, class Map>
 __device__ void wg_topk_ascending(const uint32_t* keys, int n, int k, int32_t* out, int out_cap,
                                   float* out_scores, Map map, uint32_t* scratch, int32_t* stage,
@@ -50,46 +47,61 @@ __device__ void wg_topk_ascending(const uint32_t* keys, int n, int k, int32_t* o
   const int p0 = tid * ept;
 
   uint32_t kr[kTopkMaxEPT];
-  int cnt = 0;
-  uint32_t kmx = 0u, kmn = 0xffffffffu;
+  if ((ept & 3) == 0 && (reinterpret_cast<uintptr_t>(keys) & 15u) == 0) {
+    // 16-byte reads; p0 is a multiple of 4, so they are aligned
+#pragma unroll
+    for (int v = 0; v < kTopkMaxEPT / 4; ++v) {
+      uint4 w = make_uint4(kInvalidKey, kInvalidKey, kInvalidKey, kInvalidKey);
+      if (4 * v < ept && p0 + 4 * v + 3 < n) {
+        w = *reinterpret_cast<const uint4*>(keys + p0 + 4 * v);
+      } else if (4 * v < ept) {
+        if (p0 + 4 * v < n) w.x = keys[p0 + 4 * v];
+        if (p0 + 4 * v + 1 < n) w.y = keys[p0 + 4 * v + 1];
+        if (p0 + 4 * v + 2 < n) w.z = keys[p0 + 4 * v + 2];
+      }
+      kr[4 * v] = w.x;
+      kr[4 * v + 1] = w.y;
+      kr[4 * v + 2] = w.z;
+      kr[4 * v + 3] = w.w;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kTopkMaxEPT; ++j) kr[j] = (j < ept && p0 + j < n) ? keys[p0 + j] : kInvalidKey;
+  }
+  for (int i = tid; i < 1024; i += NT) hist[i] = 0u;
+
+  // valid count, max and min valid key over the work-group
+  uint32_t cnt = 0, kmx = 0u, kmn = 0xffffffffu;
 #pragma unroll
   for (int j = 0; j < kTopkMaxEPT; ++j) {
-    const int p = p0 + j;
-    const uint32_t key = (j < ept && p < n) ? keys[p] : kInvalidKey;
-    kr[j] = key;
+    const uint32_t key = kr[j];
+    cnt += uint32_t(__popcll(__ballot(key != kInvalidKey)));
     if (key != kInvalidKey) {
-      ++cnt;
       kmx = max(kmx, key);
       kmn = min(kmn, key);
     }
   }
-  for (int i = tid; i < 1024; i += NT) hist[i] = 0u;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    cnt += __shfl_xor(cnt, o, 64);
-    kmx = max(kmx, (uint32_t)__shfl_xor((int)kmx, o, 64));
-    kmn = min(kmn, (uint32_t)__shfl_xor((int)kmn, o, 64));
-  }
+  kmx = wave_max_u32(kmx);
+  kmn = wave_min_u32(kmn);
   if (lane == 0) {
-    misc[wid] = uint32_t(cnt);
+    misc[wid] = cnt;
     misc[16 + wid] = kmx;
     misc[32 + wid] = kmn;
   }
   __syncthreads();
   {
-    const int w = lane & 15;
-    const bool in = w < NW;
-    cnt = in ? int(misc[w]) : 0;
-    kmx = in ? misc[16 + w] : 0u;
-    kmn = in ? misc[32 + w] : 0xffffffffu;
+    const uint32_t a = misc[lane & 15], b = misc[16 + (lane & 15)], c = misc[32 + (lane & 15)];
+    cnt = 0;
+    kmx = 0u;
+    kmn = 0xffffffffu;
 #pragma unroll
-    for (int o = 8; o > 0; o >>= 1) {
-      cnt += __shfl_xor(cnt, o, 64);
-      kmx = max(kmx, (uint32_t)__shfl_xor((int)kmx, o, 64));
-      kmn = min(kmn, (uint32_t)__shfl_xor((int)kmn, o, 64));
+    for (int w = 0; w < NW; ++w) {
+      cnt += uint32_t(__builtin_amdgcn_readlane(int(a), w));
+      kmx = max(kmx, uint32_t(__builtin_amdgcn_readlane(int(b), w)));
+      kmn = min(kmn, uint32_t(__builtin_amdgcn_readlane(int(c), w)));
     }
   }
-  const int kk = min(k, cnt);
+  const int kk = min(k, int(cnt));
 
   uint32_t prefix = 0u, pmask = 0u;
   int remaining = kk;
@@ -120,7 +132,8 @@ __device__ void wg_topk_ascending(const uint32_t* keys, int n, int k, int32_t* o
         c[j] = h[255 - 4 * lane - j];
         local += c[j];
       }
-      const uint32_t incl = wave_incl_scan(local);
+      uint32_t tot;
+      const uint32_t incl = wave_incl_scan_small<15>(local, &tot);
       uint32_t run = incl - local;
       int found = -1;
       uint32_t found_above = 0;
@@ -134,11 +147,9 @@ __device__ void wg_topk_ascending(const uint32_t* keys, int n, int k, int32_t* o
       }
       const uint64_t hit = __ballot(found >= 0);
       const int src = __ffsll((unsigned long long)hit) - 1;
-      const int dig = __shfl(found, src, 64);
-      const uint32_t ab = __shfl(found_above, src, 64);
-      if (lane == 0) {
-        misc[48] = uint32_t(dig);
-        misc[49] = ab;
+      if (lane == src) {
+        misc[48] = uint32_t(found);
+        misc[49] = found_above;
       }
     }
     __syncthreads();
@@ -158,14 +169,22 @@ __device__ void wg_topk_ascending(const uint32_t* keys, int n, int k, int32_t* o
       gt += (key != kInvalidKey && key > T) ? 1u : 0u;
       eq += (key != kInvalidKey && key == T) ? 1u : 0u;
     }
-    const uint32_t v = (gt << 16) | eq;  // both counts < 2^16
-    const uint32_t incl = wave_incl_scan(v);
-    if (lane == 63) comp[wid] = incl;
+    uint32_t gtot, etot;
+    const uint32_t gin = wave_incl_scan_small<5>(gt, &gtot);
+    const uint32_t ein = wave_incl_scan_small<5>(eq, &etot);
+    if (lane == 0) comp[wid] = (gtot << 16) | etot;  // totals < 2^16
     __syncthreads();
-    const uint32_t wsc = wave_incl_scan(lane < NW ? comp[lane] : 0u);
-    const uint32_t before = wid > 0 ? __shfl(wsc, wid - 1, 64) : 0u;
-    const uint32_t excl = before + incl - v;
-    int gb = int(excl >> 16), eb = int(excl & 0xffffu);
+    const uint32_t cw = comp[lane & 15];
+    uint32_t gb0 = 0, eb0 = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const uint32_t t = uint32_t(__builtin_amdgcn_readlane(int(cw), w));
+      if (w < wid) {
+        gb0 += t >> 16;
+        eb0 += t & 0xffffu;
+      }
+    }
+    int gb = int(gb0 + gin - gt), eb = int(eb0 + ein - eq);
 #pragma unroll
     for (int j = 0; j < kTopkMaxEPT; ++j) {
       const uint32_t key = kr[j];
