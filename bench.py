@@ -47,6 +47,12 @@ def parse():
     ap.add_argument("--cpu-units", type=int, default=48, help="units of the oracle sample")
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + steps of the decode only (for rocprofv3), print nothing else")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="with --profile-only: first copy a 1 GiB buffer three times (the known-size "
+                         "reference for the PMC byte counters)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc csv runs (FETCH_SIZE, WRITE_SIZE) of "
+                         "'--profile-only --calibrate-copy' into the committed traffic summary, then exit")
     return ap.parse_args()
 
 
@@ -142,10 +148,68 @@ def _cpu_unit(args):
     return int(len(r["token_ids"]))
 
 
+ATTN_SOURCES = ["attention_gqa.hip", "attn_common.hpp", "common.hpp", "kernels.hpp"]
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "attention_gqa_b32_ctx96k_traffic.json")
+COPY_BYTES = 1 << 30
+
+
+def attention_source_hash():
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2604_07815_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
+def pmc_summary(fetch_dir, write_dir):
+    """Average FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the attention
+    kernel and of the 1 GiB reference copy, from the csv output of two
+    rocprofv3 --pmc runs of the same command; the copy (the dispatches that
+    write 1 GiB, found in the WRITE_SIZE run; the same dispatch ids in the
+    FETCH_SIZE run) converts counter KiB to bytes."""
+    import csv
+    import glob
+
+    def dispatches(d, counter):
+        files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        if not files:
+            raise SystemExit(f"no counter_collection.csv under {d}")
+        vals, names = {}, {}
+        for f in files:
+            for row in csv.DictReader(open(f)):
+                if row.get("Counter_Name") != counter:
+                    continue
+                i = int(row["Dispatch_Id"])
+                vals[i] = vals.get(i, 0.0) + float(row["Counter_Value"])
+                names[i] = row["Kernel_Name"]
+        return vals, names
+
+    wv, wn = dispatches(write_dir, "WRITE_SIZE")
+    fv, fn = dispatches(fetch_dir, "FETCH_SIZE")
+    true_kib = COPY_BYTES / 1024
+    ref = [i for i, v in wv.items() if "copy" in wn[i].lower() and abs(v - true_kib) < 0.01 * true_kib]
+    if not ref or any(i not in fv or fn[i] != wn[i] for i in ref):
+        raise SystemExit(f"reference copies not found consistently ({len(ref)})")
+    out = {}
+    for counter, vals, names in (("FETCH_SIZE", fv, fn), ("WRITE_SIZE", wv, wn)):
+        attn = [v for i, v in vals.items() if "attn_gqa_mfma_kernel" in names[i]]
+        copy_kib = sum(vals[i] for i in ref) / len(ref)
+        attn_kib = sum(attn) / len(attn)
+        scale = true_kib / copy_kib
+        out[counter] = {"attention_kib_per_dispatch": round(attn_kib, 1), "reference_copy_kib": round(copy_kib, 1),
+                        "reference_true_kib": true_kib, "scale": round(scale, 4),
+                        "attention_bytes_per_launch": round(attn_kib * 1024 * scale), "dispatches": len(attn)}
+    traffic = out["FETCH_SIZE"]["attention_bytes_per_launch"] + out["WRITE_SIZE"]["attention_bytes_per_launch"]
+    rec = {"kernel": "attn_gqa_mfma_kernel<128, 4, 4>", "workload": "gqa_b32_ctx96k",
+           "kernel_src_sha256": attention_source_hash(), "traffic_bytes_per_launch": traffic,
+           "counters": out}
+    json.dump(rec, open(TRAFFIC_JSON, "w"), indent=1)
+    print(json.dumps(rec))
+
+
 def traffic_from_profiles(kernel_src_hash):
     """HBM traffic per launch of the dominant kernel from committed PMC runs,
     valid only while the kernel source is unchanged."""
-    p = os.path.join(ROOT, "profiles", "attention_gqa_b32_ctx96k_traffic.json")
+    p = TRAFFIC_JSON
     if not os.path.exists(p):
         return None
     try:
@@ -159,6 +223,9 @@ def traffic_from_profiles(kernel_src_hash):
 
 def main():
     args = parse()
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               "the operator shards by (sequence, KV head) without cross-GPU exchange, "
@@ -222,6 +289,13 @@ def main():
         step(i)
     torch.cuda.synchronize()
     if args.profile_only:
+        if args.calibrate_copy:
+            src_b = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+            dst_b = torch.empty_like(src_b)
+            for _ in range(3):
+                dst_b.copy_(src_b)
+            torch.cuda.synchronize()
+            del src_b, dst_b
         for i in range(args.steps):
             step(i)
         torch.cuda.synchronize()
@@ -262,8 +336,7 @@ def main():
     attn_ms = float(stage_ms[STAGES.index("attention")])
     attn_bytes = nb["gathered_kv"] + cfg.batch * cfg.h_q * cfg.d_qk * e
     attn_gbps = attn_bytes / (attn_ms * 1e-3) / 1e9
-    src = open(os.path.join(ROOT, "paper_2604_07815_amd", "csrc", "attention.hip"), "rb").read()
-    traffic = traffic_from_profiles(hashlib.sha256(src).hexdigest())
+    traffic = traffic_from_profiles(attention_source_hash()) if args.workload == "gqa_b32_ctx96k" else None
 
     result = {
         "metric": METRIC,
@@ -292,7 +365,8 @@ def main():
         "index_build_ms": round(index_build_ms, 3),
         "device_error_flags": err,
         "roofline": {
-            "kernel": "attn_gqa_kernel" if not cfg.mla else "attn_mla_kernel",
+            "kernel": "attn_mla_kernel" if cfg.mla else
+                      ("attn_gqa_mfma_kernel" if cfg.dtype == "bf16" else "attn_gqa_kernel"),
             "bound": "hbm", "achieved": round(attn_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
             "frac": round(attn_gbps / PEAK_HBM_GBPS, 4), "traffic": traffic,
             "bytes_per_launch": attn_bytes, "avg_launch_us": round(attn_ms * 1e3, 2),
