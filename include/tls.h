@@ -214,7 +214,12 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
  * the pool over PCIe by device-side reads, and slot_map/slot_owner are
  * updated.  transfer_count (nullable) [units] receives |T_t|.  n_slots must
  * be >= 2*K_b when block_ids_live is given (>= K_b otherwise).  Enqueue on a
- * side stream and order it against the attention step with events. */
+ * side stream and order it against the attention step with events: while it
+ * runs, the in-flight step may read only blocks of block_ids_live, whose
+ * slot_map entries and slots this call leaves untouched.  The workspace
+ * (sized for K_b and any K_t) may be the one the concurrent decode step
+ * uses: the transfer lists live in a region no other call touches, and both
+ * calls only set bits of the shared error word. */
 tls_status tls_prefetch_blocks(const tls_layout* layout, const void* host_k, const void* host_v,
                                const int32_t* ctx_lens, const int32_t* block_ids_new,
                                const int32_t* block_ids_live, int32_t K_b, void* pool_k,

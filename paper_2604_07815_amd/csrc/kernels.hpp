@@ -26,7 +26,7 @@ constexpr int kTokenSlotsPerWG = 256;
 
 // Workspace carving (byte offsets from the workspace base, 256-aligned).
 struct Workspace {
-  size_t err, bscores, bids, logits, stats, keys, tids, po, plse, total;
+  size_t err, xfer, bscores, bids, logits, stats, keys, tids, po, plse, total;
   int n_tchunks;  // token-score work-groups per unit
 };
 Workspace plan_workspace(const Problem& P, int K_b, int K_t);

@@ -90,6 +90,7 @@ Workspace plan_workspace(const Problem& P, int K_b, int K_t) {
   w.n_tchunks = int((S + kTokenSlotsPerWG - 1) / kTokenSlotsPerWG);
   size_t off = 0;
   w.err = off;      off += kHeaderBytes;
+  w.xfer = off;     off = align_up(off + U * (2 * size_t(K_b) + 1) * sizeof(int32_t));  // prefetch lists
   w.bscores = off;  off = align_up(off + U * P.m_max * sizeof(float));
   w.bids = off;     off = align_up(off + U * K_b * sizeof(int32_t));
   w.logits = off;   off = align_up(off + U * P.G * S * sizeof(float));
@@ -98,7 +99,7 @@ Workspace plan_workspace(const Problem& P, int K_b, int K_t) {
   w.tids = off;     off = align_up(off + U * size_t(K_t) * sizeof(int32_t));
   w.po = off;       off = align_up(off + U * kMaxSplits * P.G * size_t(P.d_v) * sizeof(float));
   w.plse = off;     off = align_up(off + U * kMaxSplits * P.G * sizeof(float));
-  w.total = off + align_up(U * (2 * size_t(K_b) + 1) * sizeof(int32_t));  // prefetch transfer lists
+  w.total = off;
   return w;
 }
 
@@ -351,7 +352,7 @@ tls_status tls_prefetch_blocks(const tls_layout* layout, const void* host_k, con
   }
   const tls::Workspace W = tls::plan_workspace(P, K_b, 1);
   if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
-  int32_t* xfer = at<int32_t>(ws, W.total - align_up(size_t(P.units) * (2 * size_t(K_b) + 1) * sizeof(int32_t)));
+  int32_t* xfer = at<int32_t>(ws, W.xfer);
   return hip_status(tls::launch_prefetch(P, dk, dv, ctx_lens, block_ids_new, block_ids_live, K_b, pool_k, pool_v,
                                          n_slots, slot_map, slot_owner, transfer_count, xfer, err_word(ws), stream));
 }
