@@ -6,74 +6,53 @@
 namespace tls {
 
 constexpr int kTopkMaxEPT = 16;  // keys per thread: n <= NT * kTopkMaxEPT
+constexpr int kTopkMaxNW = 16;   // waves per work-group
 
-// LDS words the selection needs: four 256-bin histograms (one per radix
-// pass, cleared once up front) and broadcast slots.
-__host__ __device__ constexpr int topk_scratch_words(int /*nt*/) { return 4 * 256 + 64 + 32; }
+// LDS words of the scratch area: four 256-bin histograms (one per radix
+// pass, cleared on entry), broadcast slots, and the per-(key slot, wave)
+// counts of the ordered compaction.
+__host__ __device__ constexpr int topk_scratch_words(int /*nt*/) {
+  return 4 * 256 + 64 + 2 * kTopkMaxEPT * kTopkMaxNW;
+}
 
 // Round a count of 32-bit LDS words up to a multiple of 4 (16 bytes), so the
 // region that follows can be read with 16-byte accesses.
 __host__ __device__ constexpr int align4w(int words) { return (words + 3) & ~3; }
 
-// Selects the k largest keys among keys[0, n) (LDS; kInvalidKey entries never
-// count), ties resolved toward the lower position, and writes map(position)
-// of the selected positions in ascending position order to out[0, k'),
-// k' = min(k, #valid keys), then -1 up to out_cap.  out_scores (nullable)
-// receives key_float of each selected key.  `stage` (LDS, out_cap ints) and
-// `stage_sc` (LDS, out_cap floats, when scores are wanted) hold the result
-// until one final copy, because a work-group barrier waits for outstanding
-// global stores.  Every thread of the work-group must call it, with n and k
-// uniform.
+// Selects the k largest of the keys held in registers, ties resolved toward
+// the lower position, and writes map(position) of the selected positions in
+// ascending position order to out[0, k'), k' = min(k, #valid keys), then -1
+// up to out_cap.  Thread t holds the keys of positions t + j*NT, j < EPT
+// (kInvalidKey marks an empty position, never selected).  out_scores
+// (nullable) receives key_float of each selected key.  `list` (LDS, as many
+// words as there are valid keys) is clobbered; `stage` / `stage_sc` (LDS,
+// out_cap entries) hold the result until one final copy, because a
+// work-group barrier waits for outstanding global stores.  Every thread of
+// the work-group must call it, with k uniform.
 //
-// Method: each thread keeps the keys of positions [tid*ept, tid*ept + ept)
-// in registers.  An MSB-first radix select over the bits where the valid keys
+// Method: an MSB-first radix select over the bits where the valid keys
 // differ (8-bit digits, LDS histograms) finds the k'-th largest key T and the
-// number r of keys equal to T to take; an ordered compaction (one prefix sum
-// of per-thread counts) then emits every key > T and the first r keys == T.
-// The output is ordered by position, so no sort is needed.  Wave-level
-// reductions and scans use DPP moves, ballots and lane reads; cross-wave
-// values go through one LDS word per wave.
-template <int NT, class Map>
-__device__ void wg_topk_ascending(const uint32_t* keys, int n, int k, int32_t* out, int out_cap,
-                                  float* out_scores, Map map, uint32_t* scratch, int32_t* stage,
-                                  float* stage_sc) {
+// number r of keys equal to T to take.  The first pass reads the registers;
+// the keys still in play after it are gathered into `list`, so the later
+// passes touch only those.  An ordered compaction then emits every key > T
+// and the first r keys == T: per (key slot j, wave) counts in position order
+// (j-major, then wave, then lane) give every key its output index with one
+// barrier, so the output is ordered by position without a sort.
+template <int NT, int EPT, class Map>
+__device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int out_cap, float* out_scores,
+                             Map map, uint32_t* scratch, uint32_t* list, int32_t* stage, float* stage_sc) {
   constexpr int NW = NT / 64;
-  static_assert(NW >= 1 && NW <= 16, "work-group of 64..1024 threads");
+  static_assert(NW >= 1 && NW <= kTopkMaxNW && EPT >= 1 && EPT <= kTopkMaxEPT, "work-group shape");
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  uint32_t* hist = scratch;           // [4][256]
-  uint32_t* misc = scratch + 1024;    // [64] count / radix broadcast slots
-  uint32_t* comp = misc + 64;         // [16] compaction wave totals
-  const int ept = (n + NT - 1) / NT;
-  const int p0 = tid * ept;
-
-  uint32_t kr[kTopkMaxEPT];
-  if ((ept & 3) == 0 && (reinterpret_cast<uintptr_t>(keys) & 15u) == 0) {
-    // 16-byte reads; p0 is a multiple of 4, so they are aligned
-#pragma unroll
-    for (int v = 0; v < kTopkMaxEPT / 4; ++v) {
-      uint4 w = make_uint4(kInvalidKey, kInvalidKey, kInvalidKey, kInvalidKey);
-      if (4 * v < ept && p0 + 4 * v + 3 < n) {
-        w = *reinterpret_cast<const uint4*>(keys + p0 + 4 * v);
-      } else if (4 * v < ept) {
-        if (p0 + 4 * v < n) w.x = keys[p0 + 4 * v];
-        if (p0 + 4 * v + 1 < n) w.y = keys[p0 + 4 * v + 1];
-        if (p0 + 4 * v + 2 < n) w.z = keys[p0 + 4 * v + 2];
-      }
-      kr[4 * v] = w.x;
-      kr[4 * v + 1] = w.y;
-      kr[4 * v + 2] = w.z;
-      kr[4 * v + 3] = w.w;
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < kTopkMaxEPT; ++j) kr[j] = (j < ept && p0 + j < n) ? keys[p0 + j] : kInvalidKey;
-  }
-  for (int i = tid; i < 1024; i += NT) hist[i] = 0u;
+  uint32_t* hist = scratch;         // [4][256]
+  uint32_t* misc = scratch + 1024;  // [64]: 0..47 wave partials, 48/49 pass result, 50 list length
+  uint32_t* cg = misc + 64;         // [EPT][NW] keys > T per (slot, wave)
+  uint32_t* ce = cg + kTopkMaxEPT * kTopkMaxNW;  // [EPT][NW] keys == T
 
   // valid count, max and min valid key over the work-group
   uint32_t cnt = 0, kmx = 0u, kmn = 0xffffffffu;
 #pragma unroll
-  for (int j = 0; j < kTopkMaxEPT; ++j) {
+  for (int j = 0; j < EPT; ++j) {
     const uint32_t key = kr[j];
     cnt += uint32_t(__popcll(__ballot(key != kInvalidKey)));
     if (key != kInvalidKey) {
@@ -83,11 +62,13 @@ __device__ void wg_topk_ascending(const uint32_t* keys, int n, int k, int32_t* o
   }
   kmx = wave_max_u32(kmx);
   kmn = wave_min_u32(kmn);
+  for (int i = tid; i < 1024; i += NT) hist[i] = 0u;
   if (lane == 0) {
     misc[wid] = cnt;
     misc[16 + wid] = kmx;
     misc[32 + wid] = kmn;
   }
+  if (tid == 0) misc[50] = 0u;
   __syncthreads();
   {
     const uint32_t a = misc[lane & 15], b = misc[16 + (lane & 15)], c = misc[32 + (lane & 15)];
@@ -112,15 +93,23 @@ __device__ void wg_topk_ascending(const uint32_t* keys, int n, int k, int32_t* o
     pmask = bits_left >= 32 ? 0u : ~((1u << bits_left) - 1u);
     prefix = kmx & pmask;
   }
+  int list_n = -1;  // < 0: the keys in play are still the registers
   for (int pass = 0; bits_left > 0; ++pass) {
     const int nb = bits_left < 8 ? bits_left : 8;
     const int shift = bits_left - nb;
     const uint32_t dmask = (1u << nb) - 1u;
     uint32_t* h = hist + 256 * pass;
+    if (list_n < 0) {
 #pragma unroll
-    for (int j = 0; j < kTopkMaxEPT; ++j) {
-      const uint32_t key = kr[j];
-      if (key != kInvalidKey && (key & pmask) == prefix) atomicAdd(&h[(key >> shift) & dmask], 1u);
+      for (int j = 0; j < EPT; ++j) {
+        const uint32_t key = kr[j];
+        if (key != kInvalidKey && (key & pmask) == prefix) atomicAdd(&h[(key >> shift) & dmask], 1u);
+      }
+    } else {
+      for (int i = tid; i < list_n; i += NT) {
+        const uint32_t key = list[i];
+        if ((key & pmask) == prefix) atomicAdd(&h[(key >> shift) & dmask], 1u);
+      }
     }
     __syncthreads();
     if (wid == 0) {
@@ -157,46 +146,89 @@ __device__ void wg_topk_ascending(const uint32_t* keys, int n, int k, int32_t* o
     remaining -= int(misc[49]);
     pmask |= dmask << shift;
     bits_left -= nb;
+    if (list_n < 0 && bits_left > 0) {
+      // gather the keys still in play; one list reservation per wave
+      uint32_t wcount = 0;
+#pragma unroll
+      for (int j = 0; j < EPT; ++j) {
+        const uint32_t key = kr[j];
+        wcount += uint32_t(__popcll(__ballot(key != kInvalidKey && (key & pmask) == prefix)));
+      }
+      uint32_t base = 0;
+      if (lane == 0 && wcount) base = atomicAdd(&misc[50], wcount);
+      base = uint32_t(__builtin_amdgcn_readfirstlane(int(base)));
+#pragma unroll
+      for (int j = 0; j < EPT; ++j) {
+        const uint32_t key = kr[j];
+        const bool in = key != kInvalidKey && (key & pmask) == prefix;
+        const uint64_t bal = __ballot(in);
+        if (in) list[base + lanes_below(bal)] = key;
+        base += uint32_t(__popcll(bal));
+      }
+      __syncthreads();
+      list_n = int(misc[50]);
+    }
   }
   const uint32_t T = prefix;
   const int r = remaining;  // keys equal to T still to take, lowest positions first
 
   if (kk > 0) {
-    uint32_t gt = 0, eq = 0;
 #pragma unroll
-    for (int j = 0; j < kTopkMaxEPT; ++j) {
+    for (int j = 0; j < EPT; ++j) {
       const uint32_t key = kr[j];
-      gt += (key != kInvalidKey && key > T) ? 1u : 0u;
-      eq += (key != kInvalidKey && key == T) ? 1u : 0u;
-    }
-    uint32_t gtot, etot;
-    const uint32_t gin = wave_incl_scan_small<5>(gt, &gtot);
-    const uint32_t ein = wave_incl_scan_small<5>(eq, &etot);
-    if (lane == 0) comp[wid] = (gtot << 16) | etot;  // totals < 2^16
-    __syncthreads();
-    const uint32_t cw = comp[lane & 15];
-    uint32_t gb0 = 0, eb0 = 0;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const uint32_t t = uint32_t(__builtin_amdgcn_readlane(int(cw), w));
-      if (w < wid) {
-        gb0 += t >> 16;
-        eb0 += t & 0xffffu;
+      const uint64_t bg = __ballot(key != kInvalidKey && key > T);
+      const uint64_t be = __ballot(key != kInvalidKey && key == T);
+      if (lane == 0) {
+        cg[j * NW + wid] = uint32_t(__popcll(bg));
+        ce[j * NW + wid] = uint32_t(__popcll(be));
       }
     }
-    int gb = int(gb0 + gin - gt), eb = int(eb0 + ein - eq);
+    __syncthreads();
+    // exclusive prefix of the (slot, wave) counts in position order; lane L
+    // holds entries L*PER .. L*PER+PER-1
+    constexpr int NE = EPT * NW;
+    constexpr int PER = (NE + 63) / 64;
+    uint32_t xg[PER], xe[PER];
+    uint32_t sg = 0, se = 0;
 #pragma unroll
-    for (int j = 0; j < kTopkMaxEPT; ++j) {
+    for (int q = 0; q < PER; ++q) {
+      const int t = lane * PER + q;
+      xg[q] = sg;
+      xe[q] = se;
+      if (t < NE) {
+        sg += cg[t];
+        se += ce[t];
+      }
+    }
+    uint32_t tg, te;
+    const uint32_t lg0 = wave_incl_scan_small<14>(sg, &tg) - sg;
+    const uint32_t le0 = wave_incl_scan_small<14>(se, &te) - se;
+    // entry (j, wid) sits at t = j*NW + wid: lane t / PER, slot t % PER = wid % PER
+    uint32_t pg = xg[0], pe = xe[0];
+#pragma unroll
+    for (int q = 1; q < PER; ++q) {
+      if ((wid % PER) == q) {
+        pg = xg[q];
+        pe = xe[q];
+      }
+    }
+    pg += lg0;
+    pe += le0;
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) {
+      const int src = (j * NW + wid) / PER;
       const uint32_t key = kr[j];
       const bool g = key != kInvalidKey && key > T;
       const bool e = key != kInvalidKey && key == T;
+      const uint64_t bg = __ballot(g);
+      const uint64_t be = __ballot(e);
+      const int gb = __builtin_amdgcn_readlane(int(pg), src) + lanes_below(bg);
+      const int eb = __builtin_amdgcn_readlane(int(pe), src) + lanes_below(be);
       if (g || (e && eb < r)) {
         const int pos = gb + min(eb, r);
-        stage[pos] = map(p0 + j);
+        stage[pos] = map(tid + j * NT);
         if (out_scores) stage_sc[pos] = key_float(key);
       }
-      gb += g ? 1 : 0;
-      eb += e ? 1 : 0;
     }
     __syncthreads();
   }
@@ -204,6 +236,32 @@ __device__ void wg_topk_ascending(const uint32_t* keys, int n, int k, int32_t* o
     out[i] = i < kk ? stage[i] : -1;
     if (out_scores) out_scores[i] = i < kk ? stage_sc[i] : 0.0f;
   }
+}
+
+template <int NT, int EPT, class Map>
+__device__ void wg_topk_lds_ept(uint32_t* keys, int n, int k, int32_t* out, int out_cap, float* out_scores, Map map,
+                                uint32_t* scratch, int32_t* stage, float* stage_sc) {
+  uint32_t kr[EPT];
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const int p = threadIdx.x + j * NT;
+    kr[j] = p < n ? keys[p] : kInvalidKey;
+  }
+  // the key array becomes the list of keys in play once every thread has
+  // read it (the selection's first barrier comes before any list write)
+  wg_topk_regs<NT, EPT>(kr, k, out, out_cap, out_scores, map, scratch, keys, stage, stage_sc);
+}
+
+// The same selection over keys[0, n) in LDS (clobbered), n <= NT*kTopkMaxEPT.
+template <int NT, class Map>
+__device__ void wg_topk_ascending(uint32_t* keys, int n, int k, int32_t* out, int out_cap, float* out_scores,
+                                  Map map, uint32_t* scratch, int32_t* stage, float* stage_sc) {
+  const int ept = (n + NT - 1) / NT;
+  if (ept <= 1) wg_topk_lds_ept<NT, 1>(keys, n, k, out, out_cap, out_scores, map, scratch, stage, stage_sc);
+  else if (ept <= 2) wg_topk_lds_ept<NT, 2>(keys, n, k, out, out_cap, out_scores, map, scratch, stage, stage_sc);
+  else if (ept <= 4) wg_topk_lds_ept<NT, 4>(keys, n, k, out, out_cap, out_scores, map, scratch, stage, stage_sc);
+  else if (ept <= 8) wg_topk_lds_ept<NT, 8>(keys, n, k, out, out_cap, out_scores, map, scratch, stage, stage_sc);
+  else wg_topk_lds_ept<NT, 16>(keys, n, k, out, out_cap, out_scores, map, scratch, stage, stage_sc);
 }
 
 }  // namespace tls
