@@ -3,67 +3,58 @@
 //   1. top-K_b over the unit's block scores (or takes a given block list);
 //   2. the approximate logits of every candidate token,
 //        l_hj = sigma * q~_h . dequant(k~_j)
-//             = sigma * (min_j * sum_c q~_hc + scale_j * sum_c q~_hc code_jc),
-//      where the integer-code contraction runs on MFMA
-//      (v_mfma_f32_16x16x32_bf16: A = q~, G heads padded to 16 rows x 32
-//      channels, exact in bf16; B = the codes of 16 slots, exact small
-//      integers; fp32 accumulation);
+//             = sigma * (min_j * sum_c q~_hc + scale_j * sum_c q~_hc code_jc);
 //   3. per-head max and sum of exponentials over all candidates and
 //      alpha_j = (1/G) sum_h exp(l_hj - m_h) / Z_h;
 //   4. top-K_t of alpha (ties to the lower position), ascending positions.
 //
-// Data movement: every thread owns slots t, t+1024, ...; all candidates'
-// index rows (16 B codes + 8 B params per slot) are requested at once with
-// wide coalesced loads (one 64-slot block per wave instruction), the codes
-// are staged in LDS, each wave turns 16-slot tiles of them into raw dot
-// products written back in place (16 B per slot either way), and the owning
-// threads finish the logits in registers.
+// Everything a thread computes stays in its registers: thread t owns the
+// candidate slots t + 1024 i (i < 8), so each wave reads 64 consecutive
+// tokens' index rows (coalesced 16-byte code and 8-byte parameter loads) and
+// hands its alpha keys straight to the register top-k, whose ordered
+// compaction works on exactly this strided ownership.
+//
+// The code contraction runs on v_mfma_f32_4x4x4_16b_bf16: sixteen 4x4x4
+// blocks per instruction, block b = lanes 4b..4b+3, A = the (up to) four
+// heads' q~ on 4 channels (the same in every block), B = 4 channels of the
+// four slots of the block, so lane l receives the four heads' dots of its own
+// slot.  Eight instructions cover the 32 channels of one index group.  A code
+// c enters as the bf16 number 128 + c (bit pattern 0x4300 | c, built with one
+// byte permute per two codes), so the product gives sum_c q~_c (128 + c_c);
+// the 128 sum_c q~_c part is folded into the offset term:
+//   l_hj = sigma * (scale_j * dot_hj + (min_j - 128 scale_j) * sum_c q~_hc).
+// All products are exact in fp32; accumulation is fp32.
 #include "token_common.hpp"
 
 namespace tls {
 
-typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
-typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4_t;
 
 constexpr int kSelNT = 1024;
 constexpr int kSelNW = kSelNT / 64;
-constexpr int kSelSPT = 8;  // slots per thread
+constexpr int kSelSPT = 8;  // candidate slots per thread
 constexpr int kSelMaxSlots = kSelNT * kSelSPT;
+constexpr int kSelBPT = 2;  // block scores per thread
+constexpr int kSelMaxBlocks = kSelNT * kSelBPT;
 constexpr int kSelMaxG = 4;
 constexpr size_t kSelMaxLds = 160 * 1024;
+constexpr uint32_t kBf16Base = 0x43434343u;  // high byte of bf16(128 + c), c < 16
 
-// Channel order of the eight codes of one packed dword as they enter the
-// MFMA k-slice: low nibbles (channels 0,2,4,6) then high nibbles (1,3,5,7).
-// The contraction is order-free, so A uses the same order.
-__device__ constexpr int kSlicePerm[8] = {0, 2, 4, 6, 1, 3, 5, 7};
+// Element order of one 4-channel k-slice: within the 8 channels of code dword
+// w, slice 2w holds channels (0, 2, 1, 3) and slice 2w+1 channels (4, 6, 5, 7)
+// (offsets from 8w): the low nibbles of two bytes, then their high nibbles.
+__device__ constexpr int kSliceChan[8] = {0, 2, 1, 3, 4, 6, 5, 7};
 
-// bf16 bit pattern of a small non-negative integer (exact).
-__device__ inline uint32_t int_bf16(uint32_t c) { return __float_as_uint(float(c)) >> 16; }
-
-__device__ inline bf16x8_t codes_operand(uint32_t w) {
-  const uint32_t lo = w & 0x0f0f0f0fu, hi = (w >> 4) & 0x0f0f0f0fu;
-  u32x4_t p;
-  p[0] = int_bf16(lo & 0xffu) | (int_bf16((lo >> 8) & 0xffu) << 16);
-  p[1] = int_bf16((lo >> 16) & 0xffu) | (int_bf16(lo >> 24) << 16);
-  p[2] = int_bf16(hi & 0xffu) | (int_bf16((hi >> 8) & 0xffu) << 16);
-  p[3] = int_bf16((hi >> 16) & 0xffu) | (int_bf16(hi >> 24) << 16);
-  return __builtin_bit_cast(bf16x8_t, p);
-}
-
-// LDS words: top-k scratch | block list | block-list stage | q sums | reduce
-// slots | region R.  R holds the block keys, then the codes / raw dots
-// (4 words per slot), then the alpha keys and the top-K_t stage.
-static size_t region_words(int S, int K_t, int m_max) {
-  size_t r = size_t(4) * S;
-  if (size_t(m_max) > r) r = m_max;
-  if (size_t(S) + 2 * size_t(K_t) > r) r = size_t(S) + 2 * size_t(K_t);
-  return r;
-}
+// LDS words: top-k scratch | block list | block-list stage | q~ table (4 heads
+// x 32 channels of bf16, in slice order) | per-wave partials | key list
+// (max(m_max, S)) | top-K_t stage (K_t ids, K_t scores).
+__host__ __device__ inline size_t list_words(int S, int m_max) { return size_t(S > m_max ? S : m_max); }
 
 size_t mfma_select_lds_bytes(int S, int K_b, int K_t, int m_max) {
-  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(2 * K_b)) + 4 + kSelNW * 4 +
-          region_words(S, K_t, m_max)) *
+  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(2 * K_b)) + 64 + kSelNW * 8 +
+          align4w(int(list_words(S, m_max))) + 2 * size_t(K_t)) *
          sizeof(uint32_t);
 }
 
@@ -79,9 +70,12 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   uint32_t* scratch = smem;
   int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(NT));
   int32_t* s_bstage = s_bl + K_b;
-  float* s_qs = reinterpret_cast<float*>(s_bl + align4w(2 * K_b));  // [4]
-  float* s_red = s_qs + 4;                                 // [NW][4]
-  uint32_t* R = reinterpret_cast<uint32_t*>(s_red + NW * 4);
+  uint16_t* s_qt = reinterpret_cast<uint16_t*>(s_bl + align4w(2 * K_b));  // [4][32] (64 words)
+  float* s_red = reinterpret_cast<float*>(s_qt + 128);                    // [NW][8]
+  uint32_t* list = reinterpret_cast<uint32_t*>(s_red + NW * 8);
+  const int S = K_b * B;
+  int32_t* stage = reinterpret_cast<int32_t*>(list + align4w(int(list_words(S, m_max))));
+  float* stage_sc = reinterpret_cast<float*>(stage + K_t);
 
   const int unit = blockIdx.x;
   const int s = unit / H_kv, g = unit % H_kv;
@@ -92,149 +86,141 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
     n = n < 0 ? 0 : T;
   }
   const int m = (n + B - 1) / B;
-  const int S = K_b * B;
-  const uint16_t* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
-  const int32_t* chs = channels + g * 32;
 
-  // A operand: row = head (lane % 16; zero rows past G), k-slice lane / 16
-  bf16x8_t a_op;
-  {
-    const int h = lane & 15, ks = lane >> 4;
-    u32x4_t pa;
-#pragma unroll
-    for (int e2 = 0; e2 < 4; ++e2) {
-      uint32_t v[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        int ch = chs[8 * ks + kSlicePerm[2 * e2 + t]];
-        if (ch < 0 || ch >= d) {
-          set_error(err, 32u);
-          ch = 0;
-        }
-        v[t] = h < G ? qg[size_t(h) * d + ch] : 0u;
-      }
-      pa[e2] = v[0] | (v[1] << 16);
-    }
-    a_op = __builtin_bit_cast(bf16x8_t, pa);
-  }
-  if (tid < G) {
-    float a = 0.f;
-    for (int c = 0; c < 32; ++c) {
-      int ch = chs[c];
-      ch = (ch < 0 || ch >= d) ? 0 : ch;
-      a += BF16::to_f(qg[size_t(tid) * d + ch]);
-    }
-    s_qs[tid] = a;
-  }
-  // block list
+  // block scores as keys (requested first: the longest dependency)
+  uint32_t bk[kSelBPT];
   if (block_scores) {
     const float* sc = block_scores + size_t(unit) * m_max;
-    for (int i = tid; i < m; i += NT) R[i] = float_key(sc[i]);
-    __syncthreads();
-    wg_topk_ascending<NT>(R, m, K_b, s_bl, K_b, nullptr, [](int i) { return int32_t(i); }, scratch, s_bstage,
-                          nullptr);
+#pragma unroll
+    for (int j = 0; j < kSelBPT; ++j) {
+      const int i = tid + j * NT;
+      bk[j] = i < m ? float_key(sc[i]) : kInvalidKey;
+    }
   } else {
-    for (int i = tid; i < K_b; i += NT) s_bl[i] = block_ids_in[size_t(unit) * K_b + i];
+    for (int i = tid; i < K_b; i += NT) {
+      int b = block_ids_in[size_t(unit) * K_b + i];
+      if (b >= m) {
+        set_error(err, 2u);
+        b = -1;
+      }
+      s_bl[i] = b < 0 ? -1 : b;
+    }
+  }
+  // q~ table in slice order: entry (h, 4k + e) = q[h][C[8(k/2) + kSliceChan[4(k%2) + e]]]
+  if (tid < 4 * 32) {
+    const int h = tid >> 5, x = tid & 31;
+    uint16_t v = 0;
+    if (h < G) {
+      const int k = x >> 2, e = x & 3;
+      int ch = channels[g * 32 + 8 * (k >> 1) + kSliceChan[4 * (k & 1) + e]];
+      if (ch < 0 || ch >= d) {
+        set_error(err, 32u);
+        ch = 0;
+      }
+      v = q[(size_t(s) * H_q + size_t(g) * G + h) * d + ch];
+    }
+    s_qt[tid] = v;
+  }
+  if (block_scores) {
+    wg_topk_regs<NT, kSelBPT>(bk, K_b, s_bl, K_b, nullptr, [](int i) { return int32_t(i); }, scratch, list,
+                              s_bstage, nullptr);
   }
   __syncthreads();
 
-  // 1. request every index row of this thread's slots, stage codes in LDS
+  // A operands (row = head lane%4, slice k) and the per-head q~ sums
+  i16x4_t qa[8];
+  float qsum[4];
+  {
+    const uint4* row = reinterpret_cast<const uint4*>(s_qt + (lane & 3) * 32);
+    float own = 0.f;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const uint4 w = row[v];
+      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        i16x4_t a;
+        a[0] = short(ws[2 * k2] & 0xffffu);
+        a[1] = short(ws[2 * k2] >> 16);
+        a[2] = short(ws[2 * k2 + 1] & 0xffffu);
+        a[3] = short(ws[2 * k2 + 1] >> 16);
+        qa[2 * v + k2] = a;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) own += __uint_as_float(ws[e] << 16) + __uint_as_float(ws[e] & 0xffff0000u);
+    }
+    // broadcast the four heads' sums inside each quad (lane 4b + h holds head h)
+    const int oi = __float_as_int(own);
+    qsum[0] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0x00, 0xF, 0xF, false));
+    qsum[1] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0x55, 0xF, 0xF, false));
+    qsum[2] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0xAA, 0xF, 0xF, false));
+    qsum[3] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0xFF, 0xF, 0xF, false));
+  }
+
+  // 1. index rows of the owned slots
+  uint4 cw[kSelSPT];
   float2 qp[kSelSPT];
   uint32_t vmask = 0;
-  {
-    uint4 cw[kSelSPT];
 #pragma unroll
-    for (int i = 0; i < kSelSPT; ++i) {
-      const int slot = tid + i * NT;
-      int tok = 0;
-      const bool valid = slot < S && slot_token(s_bl, K_b, B, m, n, slot, &tok, err);
-      cw[i] = make_uint4(0, 0, 0, 0);
-      qp[i] = make_float2(0.f, 0.f);
-      if (valid) {
-        const size_t row = size_t(unit) * T + tok;
-        cw[i] = ld16_stream(codes + row * 16);
-        qp[i] = *reinterpret_cast<const float2*>(qparams + row * 2);
+  for (int i = 0; i < kSelSPT; ++i) {
+    const int slot = tid + i * NT;
+    const int e = slot / B, o = slot % B;
+    cw[i] = make_uint4(0, 0, 0, 0);
+    qp[i] = make_float2(0.f, 0.f);
+    if (slot < S) {
+      const int blk = s_bl[e];
+      const int tok = blk * B + o;
+      if (blk >= 0 && tok < n) {
+        const size_t r = size_t(unit) * T + tok;
+        cw[i] = *reinterpret_cast<const uint4*>(codes + r * 16);
+        qp[i] = *reinterpret_cast<const float2*>(qparams + r * 2);
         vmask |= 1u << i;
       }
     }
-#pragma unroll
-    for (int i = 0; i < kSelSPT; ++i) {
-      const int slot = tid + i * NT;
-      if (slot < S) *reinterpret_cast<uint4*>(R + size_t(slot) * 4) = cw[i];
-    }
   }
-  __syncthreads();
 
-  // 2. raw dots on MFMA, 16-slot tiles, written back over their own codes
-  {
-    const int ntiles = S / 16;
-    const int r16 = lane & 15, ks = lane >> 4;
-    for (int t0 = wid; t0 < ntiles; t0 += NW * 4) {
-      uint32_t w4[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int tile = t0 + u * NW;
-        w4[u] = tile < ntiles ? R[(tile * 16 + r16) * 4 + ks] : 0u;
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int tile = t0 + u * NW;
-        if (tile >= ntiles) break;
-        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_op, codes_operand(w4[u]), acc, 0, 0, 0);
-        if (lane < 16) {
-          // rows 0..3 of the result are heads 0..3 of slot tile*16 + lane
-          uint4 o;
-          o.x = __float_as_uint(acc[0]);
-          o.y = __float_as_uint(acc[1]);
-          o.z = __float_as_uint(acc[2]);
-          o.w = __float_as_uint(acc[3]);
-          *reinterpret_cast<uint4*>(R + size_t(tile * 16 + lane) * 4) = o;
-        }
-      }
-    }
-  }
-  __syncthreads();
-
-  // 3. logits of the owned slots, per-head max over the work-group
+  // 2. dots on the matrix cores, logits, per-head max
   float lg[kSelSPT][G];
   float mx[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) mx[h] = -INFINITY;
 #pragma unroll
   for (int i = 0; i < kSelSPT; ++i) {
-    const int slot = tid + i * NT;
-    const bool valid = (vmask >> i) & 1u;
-    float raw[4] = {0.f, 0.f, 0.f, 0.f};
-    if (slot < S) {
-      const uint4 o = *reinterpret_cast<const uint4*>(R + size_t(slot) * 4);
-      raw[0] = __uint_as_float(o.x);
-      raw[1] = __uint_as_float(o.y);
-      raw[2] = __uint_as_float(o.z);
-      raw[3] = __uint_as_float(o.w);
+    const uint32_t wd[4] = {cw[i].x, cw[i].y, cw[i].z, cw[i].w};
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t lo = wd[w] & 0x0f0f0f0fu, hi = (wd[w] >> 4) & 0x0f0f0f0fu;
+      const u32x2_t b0 = {__builtin_amdgcn_perm(kBf16Base, lo, 0x04010400u),
+                          __builtin_amdgcn_perm(kBf16Base, hi, 0x04010400u)};
+      const u32x2_t b1 = {__builtin_amdgcn_perm(kBf16Base, lo, 0x04030402u),
+                          __builtin_amdgcn_perm(kBf16Base, hi, 0x04030402u)};
+      acc = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(qa[2 * w], __builtin_bit_cast(i16x4_t, b0), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(qa[2 * w + 1], __builtin_bit_cast(i16x4_t, b1), acc, 0, 0, 0);
     }
+    const bool valid = (vmask >> i) & 1u;
+    const float sc = qp[i].x, off = qp[i].y - 128.0f * qp[i].x;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      lg[i][h] = valid ? sigma * (qp[i].y * s_qs[h] + qp[i].x * raw[h]) : -INFINITY;
+      lg[i][h] = valid ? sigma * fmaf(sc, acc[h], off * qsum[h]) : -INFINITY;
       mx[h] = fmaxf(mx[h], lg[i][h]);
     }
   }
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     const float w = wave_max_f32(mx[h]);
-    if (lane == 0) s_red[wid * 4 + h] = w;
+    if (lane == 0) s_red[wid * 8 + h] = w;
   }
   __syncthreads();
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    const float v = s_red[(lane & 15) * 4 + h];
+    const float v = s_red[(lane & 15) * 8 + h];
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < NW; ++w) M = fmaxf(M, __uint_as_float(__builtin_amdgcn_readlane(__float_as_int(v), w)));
     mx[h] = M;
   }
-  __syncthreads();
-  // exponentials and their per-head sums
+  // 3. exponentials and their per-head sums
   float sum[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) sum[h] = 0.f;
@@ -249,45 +235,40 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     const float w = wave_sum_f32(sum[h]);
-    if (lane == 0) s_red[wid * 4 + h] = w;
+    if (lane == 0) s_red[wid * 8 + 4 + h] = w;
   }
   __syncthreads();
   float iz[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    const float v = s_red[(lane & 15) * 4 + h];
+    const float v = s_red[(lane & 15) * 8 + 4 + h];
     float Z = 0.f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) Z += __uint_as_float(__builtin_amdgcn_readlane(__float_as_int(v), w));
     iz[h] = Z > 0.f ? 1.0f / Z : 0.f;
   }
-  // 4. alpha keys over R[0, S), top-K_t
+  // 4. alpha keys in registers, top-K_t
   const float invG = 1.0f / float(G);
+  uint32_t keys[kSelSPT];
 #pragma unroll
   for (int i = 0; i < kSelSPT; ++i) {
-    const int slot = tid + i * NT;
-    if (slot < S) {
-      float a = 0.f;
+    float a = 0.f;
 #pragma unroll
-      for (int h = 0; h < G; ++h) a += lg[i][h] * iz[h];
-      R[slot] = ((vmask >> i) & 1u) ? float_key(a * invG) : kInvalidKey;
-    }
+    for (int h = 0; h < G; ++h) a += lg[i][h] * iz[h];
+    keys[i] = ((vmask >> i) & 1u) ? float_key(a * invG) : kInvalidKey;
   }
-  __syncthreads();
-  int32_t* stage = reinterpret_cast<int32_t*>(R + S);
-  float* stage_sc = reinterpret_cast<float*>(R + S + K_t);
-  wg_topk_ascending<NT>(R, S, K_t, token_ids + size_t(unit) * K_t, K_t,
-                        token_scores ? token_scores + size_t(unit) * K_t : nullptr,
-                        [=](int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch, stage,
-                        stage_sc);
+  wg_topk_regs<NT, kSelSPT>(keys, K_t, token_ids + size_t(unit) * K_t, K_t,
+                            token_scores ? token_scores + size_t(unit) * K_t : nullptr,
+                            [=](int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch, list,
+                            stage, stage_sc);
   if (block_scores && block_ids_out)
     for (int i = tid; i < K_b; i += NT) block_ids_out[size_t(unit) * K_b + i] = s_bl[i];
 }
 
 bool fused_token_select_ok(const Problem& P, int K_b, int K_t) {
   const int S = K_b * P.B;
-  return P.dtype == 1 && P.G >= 1 && P.G <= kSelMaxG && P.d_c == 32 && S <= kSelMaxSlots && S % 16 == 0 &&
-         mfma_select_lds_bytes(S, K_b, K_t, P.m_max) <= kSelMaxLds;
+  return P.dtype == 1 && P.G >= 1 && P.G <= kSelMaxG && P.d_c == 32 && S <= kSelMaxSlots &&
+         P.m_max <= kSelMaxBlocks && mfma_select_lds_bytes(S, K_b, K_t, P.m_max) <= kSelMaxLds;
 }
 
 template <int G>
