@@ -134,6 +134,21 @@ __device__ inline float wave_sum_f32(float x) {
   }));
 }
 
+// Inclusive prefix sum over the wave on DPP lane moves: a Hillis-Steele scan
+// inside each 16-lane row (row_shr 1, 2, 4, 8), then row 0's total into row 1
+// and row 2's into row 3 (row_bcast:15), then rows 0-1 into rows 2-3
+// (row_bcast:31).  Lanes without a source add 0.  Every lane must be active.
+__device__ inline uint32_t wave_incl_scan_u32(uint32_t v) {
+  int x = int(v);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);
+  return uint32_t(x);
+}
+
 // Inclusive prefix sum over the wave of small non-negative integers
 // (v < 2^BITS), one ballot per bit; *total receives the wave sum.
 template <int BITS>

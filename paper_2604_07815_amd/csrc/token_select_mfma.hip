@@ -86,6 +86,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
     n = n < 0 ? 0 : T;
   }
   const int m = (n + B - 1) / B;
+  const int lgB = __builtin_ctz(unsigned(B));  // B is a power of two here
 
   // block scores as keys (requested first: the longest dependency)
   uint32_t bk[kSelBPT];
@@ -164,7 +165,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
 #pragma unroll
   for (int i = 0; i < kSelSPT; ++i) {
     const int slot = tid + i * NT;
-    const int e = slot / B, o = slot % B;
+    const int e = slot >> lgB, o = slot & (B - 1);
     cw[i] = make_uint4(0, 0, 0, 0);
     qp[i] = make_float2(0.f, 0.f);
     if (slot < S) {
@@ -259,7 +260,8 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   }
   wg_topk_regs<NT, kSelSPT>(keys, K_t, token_ids + size_t(unit) * K_t, K_t,
                             token_scores ? token_scores + size_t(unit) * K_t : nullptr,
-                            [=](int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch, list,
+                            [=](int slot) { return int32_t((s_bl[slot >> lgB] << lgB) | (slot & (B - 1))); },
+                            scratch, list,
                             stage, stage_sc);
   if (block_scores && block_ids_out)
     for (int i = tid; i < K_b; i += NT) block_ids_out[size_t(unit) * K_b + i] = s_bl[i];
@@ -267,7 +269,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
 
 bool fused_token_select_ok(const Problem& P, int K_b, int K_t) {
   const int S = K_b * P.B;
-  return P.dtype == 1 && P.G >= 1 && P.G <= kSelMaxG && P.d_c == 32 && S <= kSelMaxSlots &&
+  return P.dtype == 1 && P.G >= 1 && P.G <= kSelMaxG && P.d_c == 32 && (P.B & (P.B - 1)) == 0 && S <= kSelMaxSlots &&
          P.m_max <= kSelMaxBlocks && mfma_select_lds_bytes(S, K_b, K_t, P.m_max) <= kSelMaxLds;
 }
 

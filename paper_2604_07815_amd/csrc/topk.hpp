@@ -121,8 +121,7 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
         c[j] = h[255 - 4 * lane - j];
         local += c[j];
       }
-      uint32_t tot;
-      const uint32_t incl = wave_incl_scan_small<15>(local, &tot);
+      const uint32_t incl = wave_incl_scan_u32(local);
       uint32_t run = incl - local;
       int found = -1;
       uint32_t found_above = 0;
@@ -200,9 +199,8 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
         se += ce[t];
       }
     }
-    uint32_t tg, te;
-    const uint32_t lg0 = wave_incl_scan_small<14>(sg, &tg) - sg;
-    const uint32_t le0 = wave_incl_scan_small<14>(se, &te) - se;
+    const uint32_t lg0 = wave_incl_scan_u32(sg) - sg;
+    const uint32_t le0 = wave_incl_scan_u32(se) - se;
     // entry (j, wid) sits at t = j*NW + wid: lane t / PER, slot t % PER = wid % PER
     uint32_t pg = xg[0], pe = xe[0];
 #pragma unroll
