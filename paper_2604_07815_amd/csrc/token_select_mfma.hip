@@ -173,8 +173,9 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
       const int tok = blk * B + o;
       if (blk >= 0 && tok < n) {
         const size_t r = size_t(unit) * T + tok;
-        cw[i] = *reinterpret_cast<const uint4*>(codes + r * 16);
-        qp[i] = *reinterpret_cast<const float2*>(qparams + r * 2);
+        cw[i] = ld16_stream(codes + r * 16);
+        const float* pr = qparams + r * 2;
+        qp[i] = make_float2(__builtin_nontemporal_load(pr), __builtin_nontemporal_load(pr + 1));
         vmask |= 1u << i;
       }
     }
