@@ -50,7 +50,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 __device__ inline void gather16_to_lds(const void* src, const void* lds) {
   // the LDS destination is wave-uniform; readfirstlane puts it in an SGPR
   const uint32_t off = uint32_t(__builtin_amdgcn_readfirstlane(int(reinterpret_cast<uintptr_t>((lds_void*)lds))));
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(off), "v"(src) : "m0");
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off nt" : : "s"(off), "v"(src) : "m0");
 }
 
 template <class E, int D, int G>
