@@ -221,6 +221,7 @@ int attn_splits_for(const Problem& P, int K_t, int requested) {
     // small batches: more, shorter splits so the launch fills the chip
     while (ns * 2 <= kMaxSplits && long(P.units) * ns < 1024 && K_t / (ns * 2) >= 32) ns *= 2;
   }
+  if (ns <= 1 && gqa_whole_ok(P, K_t)) return 1;  // one work-group per unit takes every token
   if (ns < need) ns = need;
   if (ns > K_t) ns = K_t;
   return ns < 1 ? 1 : ns;

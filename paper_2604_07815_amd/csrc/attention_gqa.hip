@@ -20,7 +20,9 @@ namespace tls {
 constexpr int kAttnCT = 64;      // tokens per chunk
 constexpr int kAttnMaxTPW = 512;  // tokens per work-group (fp32 kernel)
 constexpr int kAttnMaxTPWBf16 = 1024;  // tokens per work-group (bf16 matrix-core kernel)
-constexpr int kAttnNW = 4;             // waves per work-group (bf16 matrix-core kernel)
+constexpr int kAttnNW = 4;             // waves per work-group (bf16 matrix-core kernel, split mode)
+constexpr int kWholeNW = 12;           // waves per work-group when one work-group takes a whole unit
+constexpr int kWholeTPWV = 176;        // tokens per wave in that mode: K_t <= 12 * 176 = 2112
 
 // s_waitcnt immediates (gfx9 encoding): vmcnt in [3:0] and [15:14],
 // expcnt in [6:4], lgkmcnt in [11:8].
@@ -301,8 +303,11 @@ __device__ inline float xrows_sum(float v) {
 //     rarely rescaled); the probabilities are rounded to bf16;
 //   * O += P V by D/16 v_mfma_f32_16x16x16_bf16, with the V operand read
 //     column-wise straight from the row-major tile by ds_read_b64_tr_b16.
-// At the end the waves' (max, sum, accumulator) triples are merged in LDS
-// and the work-group writes one normalised partial and its log-sum-exp.
+// At the end the waves' (max, sum, accumulator) triples are merged in LDS.
+// Split mode (WHOLE = false): the work-group writes one normalised partial
+// and its log-sum-exp for the merge kernel.  Whole-unit mode (WHOLE = true,
+// one work-group of 12 waves per unit, grid.x = 1): it writes the final
+// output row in the input dtype and the lse directly.
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4;
 
@@ -312,12 +317,13 @@ __device__ inline short bf16_bits_rne(float f) {
   return short(u >> 16);
 }
 
-template <int D, int G, int NW>
+template <int D, int G, int NW, int TPWV, bool WHOLE>
 __global__ __launch_bounds__(64 * NW) void attn_gqa_mfma_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp, const uint16_t* __restrict__ Vp,
     const int32_t* __restrict__ slot_map, int64_t n_slots, const int32_t* __restrict__ token_ids,
     const int32_t* __restrict__ ctx_lens, int H_q, int H_kv, int T, int B, int m_max, int K_t, int tpw,
-    float sigma, float* __restrict__ po, float* __restrict__ plse, uint32_t* err) {
+    float sigma, float* __restrict__ po, float* __restrict__ plse, uint16_t* __restrict__ out,
+    float* __restrict__ lse, uint32_t* err) {
   constexpr int ROWB = D * 2;     // bytes per K or V row
   constexpr int LPR = ROWB / 16;  // 16-byte pieces per row
   constexpr int RPI = 64 / LPR;   // rows per wave-wide gather
@@ -325,7 +331,6 @@ __global__ __launch_bounds__(64 * NW) void attn_gqa_mfma_kernel(
   constexpr int NI = CT / RPI;    // gathers per tile, for K and again for V
   constexpr int NKK = D / 32;     // score steps per tile
   constexpr int NNT = D / 16;     // channel tiles of the output
-  constexpr int TPWV = kAttnMaxTPWBf16 / NW;
   constexpr float kLog2e = 1.4426950408889634f;
   constexpr float kRaise = 8.0f;  // base-2 headroom before the running maximum is raised
   static_assert(G <= 8 && (D == 64 || D == 128) && NI * RPI == CT, "tile geometry");
@@ -549,10 +554,19 @@ __global__ __launch_bounds__(64 * NW) void attn_gqa_mfma_kernel(
         o += f * s_acc[(v * G) * D + idx];
       }
     }
-    po[pbase * D + idx] = L > 0.f ? o / L : 0.f;
-    if (idx % D == 0) plse[pbase + h] = L > 0.f ? (M + __log2f(L)) * 0.6931471805599453f : -INFINITY;
+    const float lv = L > 0.f ? (M + __log2f(L)) * 0.6931471805599453f : -INFINITY;
+    if constexpr (WHOLE) {
+      const size_t row = size_t(s) * H_q + size_t(g) * G + h;
+      out[row * D + idx % D] = f32_to_bf16(L > 0.f ? o / L : 0.f);
+      if (lse && idx % D == 0) lse[row] = lv;
+    } else {
+      po[pbase * D + idx] = L > 0.f ? o / L : 0.f;
+      if (idx % D == 0) plse[pbase + h] = lv;
+    }
   }
 }
+
+bool gqa_whole_ok(const Problem& P, int K_t);
 
 int gqa_tokens_per_split(const Problem& P) { return P.dtype == 1 ? kAttnMaxTPWBf16 : kAttnMaxTPW; }
 
@@ -561,7 +575,8 @@ template <int D, int G>
 static int mfma_wgs_per_cu() {
   static const int occ = [] {
     int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, attn_gqa_mfma_kernel<D, G, kAttnNW>, 64 * kAttnNW, 0) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &nb, attn_gqa_mfma_kernel<D, G, kAttnNW, kAttnMaxTPWBf16 / kAttnNW, false>, 64 * kAttnNW, 0) !=
             hipSuccess ||
         nb < 1)
       nb = 1;
@@ -590,6 +605,9 @@ int gqa_auto_splits(const Problem& P, int K_t) {
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
     cus = 256;
+  // whole units (one 12-wave work-group each, no partials, no merge) when
+  // they fill the compute units in whole rounds
+  if (gqa_whole_ok(P, K_t) && P.units % cus == 0) return 1;
   const int occ = P.d_qk == 64 ? mfma_wgs_per_cu_g<64>(P.G) : mfma_wgs_per_cu_g<128>(P.G);
   const long slots = long(cus) * occ;
   constexpr long kFixedTokens = 64;  // prologue and merge cost of one work-group, in tokens
@@ -620,9 +638,9 @@ static void launch_t(const Problem& P, const void* q, const KvView& kv, const in
   if constexpr (E::kIsBf16) {
     constexpr int step = 16 * kAttnNW;  // whole tiles for every wave
     tpw = (tpw + step - 1) / step * step;
-    attn_gqa_mfma_kernel<D, G, kAttnNW><<<grid, 64 * kAttnNW, 0, st>>>(
+    attn_gqa_mfma_kernel<D, G, kAttnNW, kAttnMaxTPWBf16 / kAttnNW, false><<<grid, 64 * kAttnNW, 0, st>>>(
         (const uint16_t*)q, (const uint16_t*)kv.k, (const uint16_t*)kv.v, kv.slot_map, kv.n_slots, token_ids,
-        ctx_lens, P.H_q, P.H_kv, P.T, P.B, P.m_max, K_t, tpw, P.sigma, po, plse, err);
+        ctx_lens, P.H_q, P.H_kv, P.T, P.B, P.m_max, K_t, tpw, P.sigma, po, plse, nullptr, nullptr, err);
   } else {
     tpw = (tpw + kAttnCT - 1) / kAttnCT * kAttnCT;
     attn_gqa_kernel<E, D, G><<<grid, 256, 0, st>>>((const S*)q, (const S*)kv.k, (const S*)kv.v, kv.slot_map,
@@ -642,6 +660,43 @@ static bool launch_d(const Problem& P, const void* q, const KvView& kv, const in
     case 8: launch_t<E, D, 8>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
     default: return false;
   }
+}
+
+// One work-group of 12 waves per unit, output written directly: bf16 GQA
+// with K_t <= 12 * 176.
+bool gqa_whole_ok(const Problem& P, int K_t) {
+  return P.dtype == 1 && !P.mla && (P.d_qk == 64 || P.d_qk == 128) && P.d_v == P.d_qk &&
+         (P.G == 1 || P.G == 2 || P.G == 4 || P.G == 8) && K_t >= 1 && K_t <= kWholeNW * kWholeTPWV;
+}
+
+template <int D, int G>
+static void launch_whole_t(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+                           const int32_t* ctx_lens, int K_t, void* out, float* lse, uint32_t* err, hipStream_t st) {
+  constexpr int step = 16 * kWholeNW;
+  const int tpw = (K_t + step - 1) / step * step;
+  attn_gqa_mfma_kernel<D, G, kWholeNW, kWholeTPWV, true><<<dim3(1, P.units), 64 * kWholeNW, 0, st>>>(
+      (const uint16_t*)q, (const uint16_t*)kv.k, (const uint16_t*)kv.v, kv.slot_map, kv.n_slots, token_ids,
+      ctx_lens, P.H_q, P.H_kv, P.T, P.B, P.m_max, K_t, tpw, P.sigma, nullptr, nullptr, (uint16_t*)out, lse, err);
+}
+
+template <int D>
+static void launch_whole_d(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+                           const int32_t* ctx_lens, int K_t, void* out, float* lse, uint32_t* err, hipStream_t st) {
+  switch (P.G) {
+    case 1: launch_whole_t<D, 1>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st); break;
+    case 2: launch_whole_t<D, 2>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st); break;
+    case 4: launch_whole_t<D, 4>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st); break;
+    default: launch_whole_t<D, 8>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st); break;
+  }
+}
+
+hipError_t launch_attention_gqa_whole(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+                                      const int32_t* ctx_lens, int K_t, void* out, float* lse, uint32_t* err,
+                                      hipStream_t st) {
+  if (!gqa_whole_ok(P, K_t)) return hipErrorInvalidValue;
+  if (P.d_qk == 128) launch_whole_d<128>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st);
+  else launch_whole_d<64>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st);
+  return hipGetLastError();
 }
 
 hipError_t launch_attention_gqa(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,

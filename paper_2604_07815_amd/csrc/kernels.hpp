@@ -69,6 +69,12 @@ struct KvView {
 };
 int attn_tokens_per_split(const Problem& P);  // token capacity of one attention work-group
 int attn_splits_for(const Problem& P, int K_t, int requested);
+// Whole-unit attention (one work-group per unit writes the output directly;
+// no partials, no merge).  Valid when gqa_whole_ok().
+bool gqa_whole_ok(const Problem& P, int K_t);
+hipError_t launch_attention_gqa_whole(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+                                      const int32_t* ctx_lens, int K_t, void* out, float* lse, uint32_t* err,
+                                      hipStream_t st);
 hipError_t launch_attention(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
                             const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
                             uint32_t* err, hipStream_t st);

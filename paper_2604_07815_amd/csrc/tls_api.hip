@@ -220,6 +220,13 @@ static tls_status finish_decode(const Problem& P, const tls::Workspace& W, const
                                 void* ws, int requested, hipEvent_t* ev, hipStream_t stream) {
   const int nsplit = tls::attn_splits_for(P, K_t, requested);
   tls::KvView view{kv->k, kv->v, kv->slot_map, kv->n_slots};
+  if (nsplit == 1 && tls::gqa_whole_ok(P, K_t)) {
+    const hipError_t e = tls::launch_attention_gqa_whole(P, q, view, tids, ctx_lens, K_t, out, lse, err_word(ws),
+                                                         stream);
+    if (ev) hipEventRecord(ev[6], stream);
+    if (ev) hipEventRecord(ev[7], stream);
+    return hip_status(e);
+  }
   hipError_t e = tls::launch_attention(P, q, view, tids, ctx_lens, K_t, nsplit, at<float>(ws, W.po),
                                        at<float>(ws, W.plse), err_word(ws), stream);
   if (ev) hipEventRecord(ev[6], stream);

@@ -21,10 +21,12 @@ def test_dense_mode_equals_dense_attention():
         assert len(ref["token_ids"]) == 4096
 
 
-def test_empty_and_tiny_contexts():
+@pytest.mark.parametrize("splits", [0, 1])
+def test_empty_and_tiny_contexts(splits):
+    """splits=1 takes the whole-unit attention (one work-group per unit)."""
     cfg = synth.config("qwen3_gqa_48k").replace(batch=3, ctx_lo=0, ctx_hi=200, clusters=0, k_b=4, k_t=64, seed=5)
     c = H.Case(cfg, backend="host", ctx_lens=np.array([0, 1, 200], dtype=np.int32)).build_index()
-    r = c.decode()
+    r = c.decode(attn_splits=splits)
     G = cfg.group
     # empty sequence: no ids, zero output, lse = -inf
     assert torch.all(r["bids"][0] == -1) and torch.all(r["tids"][0] == -1)
@@ -46,6 +48,26 @@ def test_split_merge_invariance(splits):
     r = c.decode(attn_splits=splits)
     np.testing.assert_allclose(r["out"].cpu().numpy(), base["out"].cpu().numpy(), rtol=2e-6, atol=2e-6)
     np.testing.assert_allclose(r["lse"].cpu().numpy(), base["lse"].cpu().numpy(), rtol=2e-6, atol=2e-6)
+
+
+@pytest.mark.parametrize("splits", [1, 2, 5, 64])
+def test_split_merge_invariance_bf16(splits):
+    """bf16: one work-group per unit (splits=1, output written directly) and
+    split partials merged by LSE agree to bf16 rounding, and each matches the
+    oracle on the same token ids."""
+    cfg = synth.config("qwen3_gqa_48k").replace(ctx_lo=3000, ctx_hi=3000, clusters=2, k_b=16, k_t=700)
+    c = H.Case(cfg, backend="host").build_index()
+    base = c.decode(attn_splits=1)
+    r = c.decode(attn_splits=splits)
+    np.testing.assert_allclose(r["out"].float().cpu().numpy(), base["out"].float().cpu().numpy(), rtol=8e-3,
+                               atol=8e-3)
+    np.testing.assert_allclose(r["lse"].cpu().numpy(), base["lse"].cpu().numpy(), rtol=1e-5, atol=1e-5)
+    for (s, g) in c.units():
+        ids = H.valid_ids(r["tids"][s, g].cpu().numpy())
+        ref = c.oracle_unit(s, g, token_ids=ids)
+        G = cfg.group
+        H.check_close(r["out"][s, g * G:(g + 1) * G].float().cpu().numpy(), ref["out"], cfg.dtype, "out")
+        H.check_close(r["lse"][s, g * G:(g + 1) * G].cpu().numpy(), ref["lse"], cfg.dtype, "lse")
 
 
 def test_out_of_range_token_id_sets_error_flag():
