@@ -154,6 +154,11 @@ hipError_t launch_block_topk(const Problem& P, const float* scores, const int32_
                              int32_t* block_ids, uint32_t* err, hipStream_t st) {
   (void)err;
   const size_t lds = (topk_scratch_words(1024) + size_t(align4w(K_b)) + size_t(P.m_max)) * sizeof(uint32_t);
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(block_topk_kernel),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (e != hipSuccess) return e;
+  }
   block_topk_kernel<<<P.units, 1024, lds, st>>>(scores, ctx_lens, P.H_kv, P.T, P.B, P.m_max, K_b, block_ids);
   return hipGetLastError();
 }

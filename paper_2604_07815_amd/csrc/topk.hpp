@@ -5,14 +5,24 @@
 
 namespace tls {
 
+__host__ __device__ constexpr int align4w_c(int words) { return (words + 3) & ~3; }
+
 constexpr int kTopkMaxEPT = 16;  // keys per thread: n <= NT * kTopkMaxEPT
 constexpr int kTopkMaxNW = 16;   // waves per work-group
 
-// LDS words of the scratch area: four 256-bin histograms (one per radix
-// pass, cleared on entry), broadcast slots, and the per-(key slot, wave)
-// counts of the ordered compaction.
+// Each radix pass counts into kTopkHistCopies interleaved copies of a 256-bin
+// histogram (lane l uses copy l % kTopkHistCopies; copies kTopkHistStride
+// words apart so equal digits land in different LDS banks): keys of one
+// instruction that share a digit then collide only within their copy.
+constexpr int kTopkHistCopies = 4;
+constexpr int kTopkHistStride = 257;
+constexpr int kTopkHistWords = kTopkHistCopies * kTopkHistStride;  // per pass
+
+// LDS words of the scratch area: the four passes' histograms (cleared on
+// entry), broadcast slots, and the per-(key slot, wave) counts of the ordered
+// compaction.
 __host__ __device__ constexpr int topk_scratch_words(int /*nt*/) {
-  return 4 * 256 + 64 + 2 * kTopkMaxEPT * kTopkMaxNW;
+  return align4w_c(4 * kTopkHistWords) + 64 + 2 * kTopkMaxEPT * kTopkMaxNW;
 }
 
 // Round a count of 32-bit LDS words up to a multiple of 4 (16 bytes), so the
@@ -44,9 +54,10 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
   constexpr int NW = NT / 64;
   static_assert(NW >= 1 && NW <= kTopkMaxNW && EPT >= 1 && EPT <= kTopkMaxEPT, "work-group shape");
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  uint32_t* hist = scratch;         // [4][256]
-  uint32_t* misc = scratch + 1024;  // [64]: 0..47 wave partials, 48/49 pass result, 50 list length
-  uint32_t* cg = misc + 64;         // [EPT][NW] keys > T per (slot, wave)
+  constexpr int kHistAll = align4w_c(4 * kTopkHistWords);
+  uint32_t* hist = scratch;             // [4 passes][copies][stride]
+  uint32_t* misc = scratch + kHistAll;  // [64]: 0..47 wave partials, 48/49 pass result, 50 list length
+  uint32_t* cg = misc + 64;             // [EPT][NW] keys > T per (slot, wave)
   uint32_t* ce = cg + kTopkMaxEPT * kTopkMaxNW;  // [EPT][NW] keys == T
 
   // valid count, max and min valid key over the work-group
@@ -62,7 +73,7 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
   }
   kmx = wave_max_u32(kmx);
   kmn = wave_min_u32(kmn);
-  for (int i = tid; i < 1024; i += NT) hist[i] = 0u;
+  for (int i = tid; i < kHistAll; i += NT) hist[i] = 0u;
   if (lane == 0) {
     misc[wid] = cnt;
     misc[16 + wid] = kmx;
@@ -98,17 +109,18 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
     const int nb = bits_left < 8 ? bits_left : 8;
     const int shift = bits_left - nb;
     const uint32_t dmask = (1u << nb) - 1u;
-    uint32_t* h = hist + 256 * pass;
+    uint32_t* h = hist + kTopkHistWords * pass;
+    uint32_t* hc = h + (lane % kTopkHistCopies) * kTopkHistStride;
     if (list_n < 0) {
 #pragma unroll
       for (int j = 0; j < EPT; ++j) {
         const uint32_t key = kr[j];
-        if (key != kInvalidKey && (key & pmask) == prefix) atomicAdd(&h[(key >> shift) & dmask], 1u);
+        if (key != kInvalidKey && (key & pmask) == prefix) atomicAdd(&hc[(key >> shift) & dmask], 1u);
       }
     } else {
       for (int i = tid; i < list_n; i += NT) {
         const uint32_t key = list[i];
-        if ((key & pmask) == prefix) atomicAdd(&h[(key >> shift) & dmask], 1u);
+        if ((key & pmask) == prefix) atomicAdd(&hc[(key >> shift) & dmask], 1u);
       }
     }
     __syncthreads();
@@ -118,7 +130,9 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
       uint32_t local = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        c[j] = h[255 - 4 * lane - j];
+        c[j] = 0;
+#pragma unroll
+        for (int cp = 0; cp < kTopkHistCopies; ++cp) c[j] += h[cp * kTopkHistStride + 255 - 4 * lane - j];
         local += c[j];
       }
       const uint32_t incl = wave_incl_scan_u32(local);
