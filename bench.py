@@ -365,7 +365,7 @@ def main():
         "index_build_ms": round(index_build_ms, 3),
         "device_error_flags": err,
         "roofline": {
-            "kernel": "attn_mla_kernel" if cfg.mla else
+            "kernel": "attn_mla_mfma_kernel" if cfg.mla else
                       ("attn_gqa_mfma_kernel" if cfg.dtype == "bf16" else "attn_gqa_kernel"),
             "bound": "hbm", "achieved": round(attn_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
             "frac": round(attn_gbps / PEAK_HBM_GBPS, 4), "traffic": traffic,

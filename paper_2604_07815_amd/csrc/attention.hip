@@ -167,27 +167,36 @@ template <class E>
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ po, const float* __restrict__ plse,
                                                     int nsplit, int G, int d_v, int H_q, int H_kv,
                                                     typename E::T* __restrict__ out, float* __restrict__ lse) {
+  __shared__ float s_w[kMaxSplits];
+  __shared__ float s_lse;
   const int unit = blockIdx.x / G, h = blockIdx.x % G;
   const int s = unit / H_kv, g = unit % H_kv;
   const float* ls = plse + size_t(unit) * nsplit * G + h;
-  float M = -INFINITY;
-  for (int i = 0; i < nsplit; ++i) M = fmaxf(M, ls[size_t(i) * G]);
-  float W = 0.f;
-  if (M != -INFINITY)
-    for (int i = 0; i < nsplit; ++i) W += exp_or_zero(ls[size_t(i) * G] - M);
-  const size_t orow = size_t(s) * H_q + size_t(g) * G + h;
-  for (int dd = threadIdx.x; dd < d_v; dd += blockDim.x) {
-    float O = 0.f;
-    if (W > 0.f) {
-      for (int i = 0; i < nsplit; ++i) {
-        const float w = exp_or_zero(ls[size_t(i) * G] - M);
-        if (w != 0.f) O = fmaf(w, po[((size_t(unit) * nsplit + i) * G + h) * d_v + dd], O);
-      }
-      O /= W;
-    }
-    store_out<E>(out + orow * d_v + dd, O);
+  if (threadIdx.x < 64) {  // split weights e^{lse_i - M} / sum_j e^{lse_j - M}, one lane per split
+    const float l = int(threadIdx.x) < nsplit ? ls[size_t(threadIdx.x) * G] : -INFINITY;
+    const float M = wave_max_f32(l);
+    const float e = (M == -INFINITY) ? 0.f : exp_or_zero(l - M);
+    const float W = wave_sum_f32(e);
+    s_w[threadIdx.x] = W > 0.f ? e / W : 0.f;
+    if (threadIdx.x == 0) s_lse = W > 0.f ? M + logf(W) : -INFINITY;
   }
-  if (threadIdx.x == 0 && lse) lse[orow] = W > 0.f ? M + logf(W) : -INFINITY;
+  __syncthreads();
+  const size_t orow = size_t(s) * H_q + size_t(g) * G + h;
+  const float* base = po + (size_t(unit) * nsplit * G + h) * d_v;
+  const size_t stride = size_t(G) * d_v;  // between splits
+  for (int dd = threadIdx.x; dd < d_v; dd += blockDim.x) {
+    float o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;
+    int i = 0;
+    for (; i + 4 <= nsplit; i += 4) {
+      o0 = fmaf(s_w[i], base[size_t(i) * stride + dd], o0);
+      o1 = fmaf(s_w[i + 1], base[size_t(i + 1) * stride + dd], o1);
+      o2 = fmaf(s_w[i + 2], base[size_t(i + 2) * stride + dd], o2);
+      o3 = fmaf(s_w[i + 3], base[size_t(i + 3) * stride + dd], o3);
+    }
+    for (; i < nsplit; ++i) o0 = fmaf(s_w[i], base[size_t(i) * stride + dd], o0);
+    store_out<E>(out + orow * d_v + dd, (o0 + o1) + (o2 + o3));
+  }
+  if (threadIdx.x == 0 && lse) lse[orow] = s_lse;
 }
 
 __global__ void fill_u32_kernel(uint32_t* p, uint32_t v, size_t n) {
@@ -204,17 +213,27 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t v, size_t n, hipStream_t st) {
 
 int gqa_tokens_per_split(const Problem& P);
 int gqa_auto_splits(const Problem& P, int K_t);
+bool mla_mfma_ok(const Problem& P);
+int mla_mfma_tokens_per_split();
+int mla_mfma_splits(const Problem& P, int K_t);
+hipError_t launch_attention_mla_mfma(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+                                     const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
+                                     uint32_t* err, hipStream_t st);
 hipError_t launch_attention_gqa(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
                                 const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
                                 uint32_t* err, hipStream_t st);
 
-int attn_tokens_per_split(const Problem& P) { return P.mla ? kMlaCt : gqa_tokens_per_split(P); }
+int attn_tokens_per_split(const Problem& P) {
+  if (P.mla) return mla_mfma_ok(P) ? mla_mfma_tokens_per_split() : kMlaCt;
+  return gqa_tokens_per_split(P);
+}
 
 int attn_splits_for(const Problem& P, int K_t, int requested) {
   const int cap = attn_tokens_per_split(P);
   const int need = (K_t + cap - 1) / cap;  // fewest splits the work-group capacity allows
   int ns = requested > 0 ? requested : need;
-  const int tuned = (requested <= 0 && !P.mla) ? gqa_auto_splits(P, K_t) : 0;
+  const int tuned = requested > 0 ? 0 : (P.mla ? (mla_mfma_ok(P) ? mla_mfma_splits(P, K_t) : 0)
+                                                : gqa_auto_splits(P, K_t));
   if (tuned > 0) {
     ns = tuned;
   } else if (requested <= 0) {
@@ -230,6 +249,8 @@ int attn_splits_for(const Problem& P, int K_t, int requested) {
 hipError_t launch_attention(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
                             const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
                             uint32_t* err, hipStream_t st) {
+  if (P.mla && mla_mfma_ok(P))
+    return launch_attention_mla_mfma(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
   if (P.mla) {
     dim3 grid(nsplit, P.units);
     const int ct = (K_t + nsplit - 1) / nsplit;
