@@ -15,9 +15,51 @@ namespace tls {
 
 constexpr int kBlkUnroll = 4;  // blocks in flight per lane group
 
+// Q+ and Q- of every unit, once, for wide groups (the absorbed MLA layout:
+// 32 heads x 576 dims), so the scoring work-groups do not each re-reduce
+// the group's queries.  qpn: [units][2][d] fp32; the heads are summed in a
+// fixed order (each quarter sequentially, then the quarters pairwise).
+template <class E>
+__global__ __launch_bounds__(256) void qsum_kernel(const typename E::T* __restrict__ q, int H_q, int H_kv, int G,
+                                                   int d, float* __restrict__ qpn) {
+  // work-group (channel chunk of 64, unit); thread (quarter, channel): the
+  // heads quarter, quarter + 4, ... of one channel, then a 4-way LDS sum
+  __shared__ float s_p[4][64], s_n[4][64];
+  const int unit = blockIdx.y, c = blockIdx.x * 64 + (threadIdx.x & 63), qt = threadIdx.x >> 6;
+  const int s = unit / H_kv, g = unit % H_kv;
+  const typename E::T* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
+  float p = 0.f, ng = 0.f;
+  if (c < d) {
+    float x[8];
+    int h = qt;
+    for (; h + 28 < G; h += 32) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = E::to_f(qg[size_t(h + 4 * j) * d + c]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        p += fmaxf(x[j], 0.f);
+        ng += fminf(x[j], 0.f);
+      }
+    }
+    for (; h < G; h += 4) {
+      const float v = E::to_f(qg[size_t(h) * d + c]);
+      p += fmaxf(v, 0.f);
+      ng += fminf(v, 0.f);
+    }
+  }
+  s_p[qt][threadIdx.x & 63] = p;
+  s_n[qt][threadIdx.x & 63] = ng;
+  __syncthreads();
+  if (qt == 0 && c < d) {
+    const int i = threadIdx.x;
+    qpn[(size_t(unit) * 2) * d + c] = (s_p[0][i] + s_p[1][i]) + (s_p[2][i] + s_p[3][i]);
+    qpn[(size_t(unit) * 2 + 1) * d + c] = (s_n[0][i] + s_n[1][i]) + (s_n[2][i] + s_n[3][i]);
+  }
+}
+
 template <class E, int LPB, int CPL>
 __global__ __launch_bounds__(256) void block_score_kernel(
-    const typename E::T* __restrict__ q, const typename E::T* __restrict__ kmax,
+    const typename E::T* __restrict__ q, const float* __restrict__ qpn, const typename E::T* __restrict__ kmax,
     const typename E::T* __restrict__ kmin, const int32_t* __restrict__ ctx_lens, int H_q, int H_kv,
     int G, int d, int B, int T, int m_max, int bpw, float* __restrict__ scores, uint32_t* err) {
   using S = typename E::T;
@@ -38,16 +80,23 @@ __global__ __launch_bounds__(256) void block_score_kernel(
     for (int i = c0 + threadIdx.x; i < c1; i += 256) out[i] = -INFINITY;
     return;
   }
-  const S* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
-  for (int c = threadIdx.x; c < d; c += 256) {
-    float p = 0.f, ng = 0.f;
-    for (int h = 0; h < G; ++h) {
-      float x = E::to_f(qg[size_t(h) * d + c]);
-      p += fmaxf(x, 0.f);
-      ng += fminf(x, 0.f);
+  if (qpn) {
+    for (int c = threadIdx.x; c < d; c += 256) {
+      s_qp[c] = qpn[(size_t(unit) * 2) * d + c];
+      s_qn[c] = qpn[(size_t(unit) * 2 + 1) * d + c];
     }
-    s_qp[c] = p;
-    s_qn[c] = ng;
+  } else {
+    const S* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
+    for (int c = threadIdx.x; c < d; c += 256) {
+      float p = 0.f, ng = 0.f;
+      for (int h = 0; h < G; ++h) {
+        float x = E::to_f(qg[size_t(h) * d + c]);
+        p += fmaxf(x, 0.f);
+        ng += fminf(x, 0.f);
+      }
+      s_qp[c] = p;
+      s_qn[c] = ng;
+    }
   }
   __syncthreads();
   const int li = threadIdx.x % LPB, grp = threadIdx.x / LPB;
@@ -121,31 +170,35 @@ __global__ __launch_bounds__(1024) void block_topk_kernel(const float* __restric
 
 template <class E, int LPB, int CPL>
 static void launch_score_t(const Problem& P, const void* q, const void* kmax, const void* kmin,
-                           const int32_t* ctx_lens, float* scores, uint32_t* err, hipStream_t st) {
+                           const int32_t* ctx_lens, float* qpn, float* scores, uint32_t* err, hipStream_t st) {
   using S = typename E::T;
   int bpw = 64;
   if (long(P.units) * ((P.m_max + 63) / 64) < 1024) bpw = 16;
   dim3 grid((P.m_max + bpw - 1) / bpw, P.units);
-  block_score_kernel<E, LPB, CPL><<<grid, 256, 0, st>>>((const S*)q, (const S*)kmax, (const S*)kmin,
-                                                        ctx_lens, P.H_q, P.H_kv, P.G, P.d_qk, P.B, P.T,
-                                                        P.m_max, bpw, scores, err);
+  // wide groups: reduce the queries once per unit instead of in every work-group
+  const bool pre = qpn && long(P.G) * P.d_qk > 2048;
+  if (pre)
+    qsum_kernel<E><<<dim3((P.d_qk + 63) / 64, P.units), 256, 0, st>>>((const S*)q, P.H_q, P.H_kv, P.G, P.d_qk, qpn);
+  block_score_kernel<E, LPB, CPL><<<grid, 256, 0, st>>>((const S*)q, pre ? qpn : nullptr, (const S*)kmax,
+                                                        (const S*)kmin, ctx_lens, P.H_q, P.H_kv, P.G, P.d_qk, P.B,
+                                                        P.T, P.m_max, bpw, scores, err);
 }
 
 hipError_t launch_block_score(const Problem& P, const void* q, const void* kmax, const void* kmin,
-                              const int32_t* ctx_lens, float* scores, uint32_t* err, hipStream_t st) {
+                              const int32_t* ctx_lens, float* qpn, float* scores, uint32_t* err, hipStream_t st) {
   const int V = P.dtype == 1 ? 8 : 4;
   const int nch = P.d_qk / V;
   if (P.dtype == 1) {
-    if (nch <= 16) launch_score_t<BF16, 16, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
-    else if (nch <= 32) launch_score_t<BF16, 32, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
-    else if (nch <= 64) launch_score_t<BF16, 64, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
-    else launch_score_t<BF16, 64, 2>(P, q, kmax, kmin, ctx_lens, scores, err, st);
+    if (nch <= 16) launch_score_t<BF16, 16, 1>(P, q, kmax, kmin, ctx_lens, qpn, scores, err, st);
+    else if (nch <= 32) launch_score_t<BF16, 32, 1>(P, q, kmax, kmin, ctx_lens, qpn, scores, err, st);
+    else if (nch <= 64) launch_score_t<BF16, 64, 1>(P, q, kmax, kmin, ctx_lens, qpn, scores, err, st);
+    else launch_score_t<BF16, 64, 2>(P, q, kmax, kmin, ctx_lens, qpn, scores, err, st);
   } else {
-    if (nch <= 16) launch_score_t<F32, 16, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
-    else if (nch <= 32) launch_score_t<F32, 32, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
-    else if (nch <= 64) launch_score_t<F32, 64, 1>(P, q, kmax, kmin, ctx_lens, scores, err, st);
-    else if (nch <= 128) launch_score_t<F32, 64, 2>(P, q, kmax, kmin, ctx_lens, scores, err, st);
-    else launch_score_t<F32, 64, 4>(P, q, kmax, kmin, ctx_lens, scores, err, st);
+    if (nch <= 16) launch_score_t<F32, 16, 1>(P, q, kmax, kmin, ctx_lens, qpn, scores, err, st);
+    else if (nch <= 32) launch_score_t<F32, 32, 1>(P, q, kmax, kmin, ctx_lens, qpn, scores, err, st);
+    else if (nch <= 64) launch_score_t<F32, 64, 1>(P, q, kmax, kmin, ctx_lens, qpn, scores, err, st);
+    else if (nch <= 128) launch_score_t<F32, 64, 2>(P, q, kmax, kmin, ctx_lens, qpn, scores, err, st);
+    else launch_score_t<F32, 64, 4>(P, q, kmax, kmin, ctx_lens, qpn, scores, err, st);
   }
   return hipGetLastError();
 }

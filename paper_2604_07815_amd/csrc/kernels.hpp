@@ -26,7 +26,7 @@ constexpr int kTokenSlotsPerWG = 256;
 
 // Workspace carving (byte offsets from the workspace base, 256-aligned).
 struct Workspace {
-  size_t err, xfer, bscores, bids, logits, stats, keys, tids, po, plse, total;
+  size_t err, xfer, qpn, bscores, bids, logits, stats, keys, tids, po, plse, total;
   int n_tchunks;  // token-score work-groups per unit
 };
 Workspace plan_workspace(const Problem& P, int K_b, int K_t);
@@ -38,7 +38,7 @@ hipError_t launch_token_index(const Problem& P, const void* K, const int32_t* ct
                               float* qparams, uint32_t* err, hipStream_t st);
 
 hipError_t launch_block_score(const Problem& P, const void* q, const void* kmax, const void* kmin,
-                              const int32_t* ctx_lens, float* scores, uint32_t* err, hipStream_t st);
+                              const int32_t* ctx_lens, float* qpn, float* scores, uint32_t* err, hipStream_t st);
 hipError_t launch_block_topk(const Problem& P, const float* scores, const int32_t* ctx_lens, int K_b,
                              int32_t* block_ids, uint32_t* err, hipStream_t st);
 

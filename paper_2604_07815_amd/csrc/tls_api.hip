@@ -91,6 +91,7 @@ Workspace plan_workspace(const Problem& P, int K_b, int K_t) {
   size_t off = 0;
   w.err = off;      off += kHeaderBytes;
   w.xfer = off;     off = align_up(off + U * (2 * size_t(K_b) + 1) * sizeof(int32_t));  // prefetch lists
+  w.qpn = off;      off = align_up(off + U * 2 * size_t(P.d_qk) * sizeof(float));
   w.bscores = off;  off = align_up(off + U * P.m_max * sizeof(float));
   w.bids = off;     off = align_up(off + U * K_b * sizeof(int32_t));
   w.logits = off;   off = align_up(off + U * P.G * S * sizeof(float));
@@ -172,7 +173,7 @@ tls_status tls_select_blocks(const tls_layout* layout, const void* q, const void
   const tls::Workspace W = tls::plan_workspace(P, K_b, 1);
   if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
   float* scores = block_scores ? block_scores : at<float>(ws, W.bscores);
-  hipError_t e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, scores, err_word(ws), stream);
+  hipError_t e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.qpn), scores, err_word(ws), stream);
   if (e == hipSuccess) e = tls::launch_block_topk(P, scores, ctx_lens, K_b, block_ids, err_word(ws), stream);
   return hip_status(e);
 }
@@ -283,7 +284,7 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
     int32_t* to = token_ids_out ? token_ids_out : at<int32_t>(ws, W.tids);
     const float* bsc = nullptr;
     if (sel_blocks) {
-      e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.bscores), err_word(ws), stream);
+      e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.qpn), at<float>(ws, W.bscores), err_word(ws), stream);
       bsc = at<float>(ws, W.bscores);
     }
     mark(1);
@@ -300,7 +301,7 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
   }
   if (sel_blocks) {
     int32_t* bo = block_ids_out ? block_ids_out : at<int32_t>(ws, W.bids);
-    e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.bscores), err_word(ws), stream);
+    e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.qpn), at<float>(ws, W.bscores), err_word(ws), stream);
     mark(1);
     if (e == hipSuccess) e = tls::launch_block_topk(P, at<float>(ws, W.bscores), ctx_lens, K_b, bo, err_word(ws), stream);
     bids = bo;

@@ -128,6 +128,176 @@ __global__ __launch_bounds__(256) void token_score_kernel(
   }
 }
 
+// The same logits and statistics with the code contraction on the matrix
+// cores, for bf16 with G a multiple of 16 (the absorbed MLA layout: 32 heads
+// over d_c = 128 channels).  A work-group (4 waves) takes 256 slots; each
+// wave takes four 16-slot tiles.  Per tile and 32-channel group,
+// v_mfma_f32_16x16x32_bf16 with A = q~ (16 heads x 32 channels, exact in
+// bf16) and B = the tile's codes, entering as the bf16 number 128 + c (one
+// byte permute per two codes; exact) gives dot'_hj = dot_hj + 128 sum_c q~_hc,
+// so per group l gains sigma (scale_j dot'_hj + (min_j - 128 scale_j) qsum_h).
+// Lane (g, i) of the result holds slot i of the tile for heads 4g..4g+3.
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 ts_bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float ts_f32x4_t;
+typedef uint32_t ts_u32x4_t __attribute__((ext_vector_type(4)));
+
+template <int CTRL>
+__device__ inline float dpp_row_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+template <int HT, int NGR>
+__global__ __launch_bounds__(256) void token_score_mfma_kernel(
+    const uint16_t* __restrict__ q, const uint8_t* __restrict__ codes, const float* __restrict__ qparams,
+    const int32_t* __restrict__ channels, const int32_t* __restrict__ block_ids, int K_b,
+    const int32_t* __restrict__ ctx_lens, int H_q, int H_kv, int d, int B, int T, float sigma,
+    float* __restrict__ logits, float* __restrict__ stats, uint32_t* err) {
+  constexpr int G = 16 * HT, DC = 32 * NGR;
+  constexpr uint32_t kBase = 0x43434343u;  // high byte of bf16(128 + c), c < 16
+  // q~ in operand order: [head][group][lane group g][8], channel g*8 + {0,2,4,6,1,3,5,7}
+  __shared__ __attribute__((aligned(16))) uint16_t s_qt[G * DC];
+  __shared__ float s_qs[G * NGR];
+  __shared__ float s_red[4][G][2];
+  const int unit = blockIdx.y, chunk = blockIdx.x;
+  const int s = unit / H_kv, g = unit % H_kv;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int t16 = lane & 15, lg = lane >> 4;
+  int n = ctx_lens[s];
+  n = n < 0 ? 0 : (n > T ? T : n);
+  const int m = (n + B - 1) / B;
+  const int S = K_b * B;
+  const uint16_t* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
+  for (int i = tid; i < G * DC; i += 256) {
+    const int h = i / DC, x = i % DC;  // x = grp*32 + lg*8 + e (operand position)
+    const int e = x & 7;
+    const int c = (x & ~7) + ((e & 3) << 1) + (e >> 2);  // channel index of that position
+    int ch = channels[g * DC + c];
+    if (ch < 0 || ch >= d) {
+      set_error(err, 32u);
+      ch = 0;
+    }
+    s_qt[i] = qg[size_t(h) * d + ch];
+  }
+  __syncthreads();
+  for (int i = tid; i < G * NGR; i += 256) {
+    const int h = i / NGR, grp = i % NGR;
+    float a = 0.f;
+    for (int x = 0; x < 32; ++x) a += __uint_as_float(uint32_t(s_qt[h * DC + grp * 32 + x]) << 16);
+    s_qs[i] = a;
+  }
+  // A operands: head ht*16 + t16, channels of group grp at lane group lg
+  ts_bf16x8_t qa[HT][NGR];
+#pragma unroll
+  for (int ht = 0; ht < HT; ++ht)
+#pragma unroll
+    for (int grp = 0; grp < NGR; ++grp)
+      qa[ht][grp] = *reinterpret_cast<const ts_bf16x8_t*>(&s_qt[(ht * 16 + t16) * DC + grp * 32 + lg * 8]);
+  __syncthreads();
+  float qs[HT][4][NGR];  // heads ht*16 + 4lg + r
+#pragma unroll
+  for (int ht = 0; ht < HT; ++ht)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int grp = 0; grp < NGR; ++grp) qs[ht][r][grp] = s_qs[(ht * 16 + lg * 4 + r) * NGR + grp];
+
+  const int32_t* bl = block_ids + size_t(unit) * K_b;
+  float lgt[4][HT][4];  // [tile][ht][r]
+#pragma unroll
+  for (int tl = 0; tl < 4; ++tl) {
+    const int slot = chunk * kTokenSlotsPerWG + w * 64 + tl * 16 + t16;
+    int tok = 0;
+    const bool valid = slot < S && slot_token(bl, K_b, B, m, n, slot, &tok, err);
+    const size_t row = size_t(unit) * T + tok;
+    ts_f32x4_t acc[HT][NGR];
+#pragma unroll
+    for (int ht = 0; ht < HT; ++ht)
+#pragma unroll
+      for (int grp = 0; grp < NGR; ++grp) acc[ht][grp] = ts_f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float sc[NGR], off[NGR];
+#pragma unroll
+    for (int grp = 0; grp < NGR; ++grp) {
+      uint32_t x = 0;
+      sc[grp] = 0.f;
+      off[grp] = 0.f;
+      if (valid) {
+        x = *reinterpret_cast<const uint32_t*>(codes + row * (DC / 2) + grp * 16 + lg * 4);
+        const float2 pq = *reinterpret_cast<const float2*>(qparams + (row * NGR + grp) * 2);
+        sc[grp] = pq.x;
+        off[grp] = pq.y - 128.0f * pq.x;
+      }
+      const uint32_t lo = x & 0x0f0f0f0fu, hi = (x >> 4) & 0x0f0f0f0fu;
+      const ts_u32x4_t bw = {__builtin_amdgcn_perm(kBase, lo, 0x04010400u), __builtin_amdgcn_perm(kBase, lo, 0x04030402u),
+                             __builtin_amdgcn_perm(kBase, hi, 0x04010400u), __builtin_amdgcn_perm(kBase, hi, 0x04030402u)};
+      const ts_bf16x8_t b = __builtin_bit_cast(ts_bf16x8_t, bw);
+#pragma unroll
+      for (int ht = 0; ht < HT; ++ht)
+        acc[ht][grp] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[ht][grp], b, acc[ht][grp], 0, 0, 0);
+    }
+    // validity of slot t16 for the result lanes (lane (lg, t16) holds slot t16)
+#pragma unroll
+    for (int ht = 0; ht < HT; ++ht)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float v = 0.f;
+#pragma unroll
+        for (int grp = 0; grp < NGR; ++grp) v += fmaf(sc[grp], acc[ht][grp][r], off[grp] * qs[ht][r][grp]);
+        lgt[tl][ht][r] = valid ? sigma * v : -INFINITY;
+      }
+    if (slot < S) {
+      float* lg_out = logits + size_t(unit) * G * S + slot;
+#pragma unroll
+      for (int ht = 0; ht < HT; ++ht)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) lg_out[size_t(ht * 16 + lg * 4 + r) * S] = lgt[tl][ht][r];
+    }
+  }
+  // this work-group's per-head max and sum of exponentials (a DPP row holds
+  // the 16 slots of one head)
+  auto row16 = [](float v, bool is_max) {
+    float o = dpp_row_move<0xB1>(v);
+    v = is_max ? fmaxf(v, o) : v + o;
+    o = dpp_row_move<0x4E>(v);
+    v = is_max ? fmaxf(v, o) : v + o;
+    o = dpp_row_move<0x141>(v);
+    v = is_max ? fmaxf(v, o) : v + o;
+    o = dpp_row_move<0x140>(v);
+    return is_max ? fmaxf(v, o) : v + o;
+  };
+#pragma unroll
+  for (int ht = 0; ht < HT; ++ht)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float mx = fmaxf(fmaxf(lgt[0][ht][r], lgt[1][ht][r]), fmaxf(lgt[2][ht][r], lgt[3][ht][r]));
+      mx = row16(mx, true);
+      float sm = 0.f;
+      if (mx != -INFINITY) {
+#pragma unroll
+        for (int tl = 0; tl < 4; ++tl) sm += lgt[tl][ht][r] == -INFINITY ? 0.f : __expf(lgt[tl][ht][r] - mx);
+      }
+      sm = row16(sm, false);
+      if (t16 == 0) {
+        s_red[w][ht * 16 + lg * 4 + r][0] = mx;
+        s_red[w][ht * 16 + lg * 4 + r][1] = sm;
+      }
+    }
+  __syncthreads();
+  if (tid < G) {
+    float M = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) M = fmaxf(M, s_red[v][tid][0]);
+    float Z = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (s_red[v][tid][0] != -INFINITY) Z += s_red[v][tid][1] * __expf(s_red[v][tid][0] - M);
+    }
+    float* st = stats + ((size_t(unit) * gridDim.x + chunk) * G + tid) * 2;
+    st[0] = M;
+    st[1] = Z;
+  }
+}
+
 __global__ __launch_bounds__(256) void token_alpha_kernel(
     const float* __restrict__ logits, const float* __restrict__ stats, int n_tchunks,
     const int32_t* __restrict__ block_ids, int K_b, const int32_t* __restrict__ ctx_lens, int H_kv, int G,
@@ -169,6 +339,62 @@ __global__ __launch_bounds__(256) void token_alpha_kernel(
   }
 }
 
+// token_alpha_kernel with the head count fixed at compile time: 256/G lanes
+// combine each head's work-group statistics, and the per-slot sum over heads
+// is unrolled into independent loads.
+template <int G>
+__global__ __launch_bounds__(256) void token_alpha_kernel_g(
+    const float* __restrict__ logits, const float* __restrict__ stats, int n_tchunks,
+    const int32_t* __restrict__ block_ids, int K_b, const int32_t* __restrict__ ctx_lens, int H_kv, int B, int T,
+    uint32_t* __restrict__ keys) {
+  constexpr int TPH = 256 / G;  // lanes per head (a power of two)
+  __shared__ float s_m[G], s_iz[G];
+  const int unit = blockIdx.y, tid = threadIdx.x;
+  const int s = unit / H_kv;
+  int n = ctx_lens[s];
+  n = n < 0 ? 0 : (n > T ? T : n);
+  const int m = (n + B - 1) / B;
+  const int S = K_b * B;
+  {
+    const int h = tid / TPH, j = tid % TPH;
+    const float* st = stats + size_t(unit) * n_tchunks * G * 2;
+    float M = -INFINITY;
+    for (int c = j; c < n_tchunks; c += TPH) M = fmaxf(M, st[(c * G + h) * 2]);
+#pragma unroll
+    for (int o = TPH / 2; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
+    float Z = 0.f;
+    if (M != -INFINITY)
+      for (int c = j; c < n_tchunks; c += TPH) {
+        const float mc = st[(c * G + h) * 2], zc = st[(c * G + h) * 2 + 1];
+        if (mc != -INFINITY) Z += zc * __expf(mc - M);
+      }
+#pragma unroll
+    for (int o = TPH / 2; o > 0; o >>= 1) Z += __shfl_xor(Z, o, 64);
+    if (j == 0) {
+      s_m[h] = M;
+      s_iz[h] = Z > 0.f ? 1.0f / Z : 0.f;
+    }
+  }
+  __syncthreads();
+  const float invG = 1.0f / float(G);
+  const int32_t* bl = block_ids + size_t(unit) * K_b;
+  const float* lg = logits + size_t(unit) * G * S;
+  for (int slot = blockIdx.x * 256 + tid; slot < S; slot += gridDim.x * 256) {
+    int tok;
+    uint32_t key = kInvalidKey;
+    if (slot_token(bl, K_b, B, m, n, slot, &tok, nullptr)) {
+      float v[G];
+#pragma unroll
+      for (int h = 0; h < G; ++h) v[h] = lg[size_t(h) * S + slot];
+      float a = 0.f;
+#pragma unroll
+      for (int h = 0; h < G; ++h) a += __expf(v[h] - s_m[h]) * s_iz[h];
+      key = float_key(a * invG);
+    }
+    keys[size_t(unit) * S + slot] = key;
+  }
+}
+
 __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __restrict__ keys,
                                                            const int32_t* __restrict__ block_ids, int K_b,
                                                            int B, int K_t, int32_t* __restrict__ token_ids,
@@ -190,10 +416,26 @@ __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __rest
                           stage_sc);
 }
 
+template <int HT, int NGR>
+static void launch_score_mfma(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,
+                              const int32_t* channels, const int32_t* block_ids, int K_b, const int32_t* ctx_lens,
+                              float* logits, float* stats, int n_tchunks, uint32_t* err, hipStream_t st) {
+  token_score_mfma_kernel<HT, NGR><<<dim3(n_tchunks, P.units), 256, 0, st>>>(
+      (const uint16_t*)q, codes, qparams, channels, block_ids, K_b, ctx_lens, P.H_q, P.H_kv, P.d_qk, P.B, P.T,
+      P.sigma, logits, stats, err);
+}
+
 hipError_t launch_token_score(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,
                               const int32_t* channels, const int32_t* block_ids, int K_b,
                               const int32_t* ctx_lens, float* logits, float* stats, int n_tchunks,
                               uint32_t* err, hipStream_t st) {
+  if (P.dtype == 1 && (P.G == 16 || P.G == 32) && (P.d_c == 64 || P.d_c == 128)) {
+    if (P.G == 32 && P.d_c == 128) launch_score_mfma<2, 4>(P, q, codes, qparams, channels, block_ids, K_b, ctx_lens, logits, stats, n_tchunks, err, st);
+    else if (P.G == 32) launch_score_mfma<2, 2>(P, q, codes, qparams, channels, block_ids, K_b, ctx_lens, logits, stats, n_tchunks, err, st);
+    else if (P.d_c == 128) launch_score_mfma<1, 4>(P, q, codes, qparams, channels, block_ids, K_b, ctx_lens, logits, stats, n_tchunks, err, st);
+    else launch_score_mfma<1, 2>(P, q, codes, qparams, channels, block_ids, K_b, ctx_lens, logits, stats, n_tchunks, err, st);
+    return hipGetLastError();
+  }
   dim3 grid(n_tchunks, P.units);
   if (P.dtype == 1)
     token_score_kernel<BF16><<<grid, 256, 0, st>>>((const uint16_t*)q, codes, qparams, channels, block_ids,
@@ -211,8 +453,15 @@ hipError_t launch_token_alpha(const Problem& P, const float* logits, const float
                               hipStream_t st) {
   const int S = K_b * P.B;
   dim3 grid((S + 255) / 256, P.units);
-  token_alpha_kernel<<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.G,
-                                           P.B, P.T, keys);
+  switch (P.G) {
+    case 4: token_alpha_kernel_g<4><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys); break;
+    case 8: token_alpha_kernel_g<8><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys); break;
+    case 16: token_alpha_kernel_g<16><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys); break;
+    case 32: token_alpha_kernel_g<32><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys); break;
+    default:
+      token_alpha_kernel<<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.G,
+                                               P.B, P.T, keys);
+  }
   return hipGetLastError();
 }
 
