@@ -199,7 +199,7 @@ def pmc_summary(fetch_dir, write_dir):
                         "reference_true_kib": true_kib, "scale": round(scale, 4),
                         "attention_bytes_per_launch": round(attn_kib * 1024 * scale), "dispatches": len(attn)}
     traffic = out["FETCH_SIZE"]["attention_bytes_per_launch"] + out["WRITE_SIZE"]["attention_bytes_per_launch"]
-    rec = {"kernel": "attn_gqa_mfma_kernel<128, 4, 4>", "workload": "gqa_b32_ctx96k",
+    rec = {"kernel": "attn_gqa_mfma_kernel<128, 4, 12, 176, true>", "workload": "gqa_b32_ctx96k",
            "kernel_src_sha256": attention_source_hash(), "traffic_bytes_per_launch": traffic,
            "counters": out}
     json.dump(rec, open(TRAFFIC_JSON, "w"), indent=1)
