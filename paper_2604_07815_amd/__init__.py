@@ -5,7 +5,7 @@ Every function has the name of the C entry point it wraps and only
 marshals arguments: torch tensors are passed by ``data_ptr()`` and the
 stream defaults to torch's current stream.  All computation happens in the
 library's HIP kernels; importing this package fails loudly when the library
-has not been built (``python -m paper_2604_07815_amd.build``).
+has not been built (``python paper_2604_07815_amd/build.py``).
 """
 from __future__ import annotations
 
@@ -67,7 +67,7 @@ class DecodeOpts(ctypes.Structure):
 
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2604_07815_amd.build`")
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2604_07815_amd/build.py`")
     lib = ctypes.CDLL(LIB_PATH)
     P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     LP = ctypes.POINTER(Layout)

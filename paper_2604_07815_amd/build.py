@@ -1,6 +1,7 @@
 """Build libtls.so (hand-written HIP for gfx950) in-tree with hipcc.
 
-Usage: python -m paper_2604_07815_amd.build   (or __graft_entry__.build()).
+Usage: python paper_2604_07815_amd/build.py   (or __graft_entry__.build()).
+It imports nothing from the package, whose import needs the built library.
 Every call recompiles; objects go to _build/ at the repository root.
 """
 from __future__ import annotations
