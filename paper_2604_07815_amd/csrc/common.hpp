@@ -134,6 +134,48 @@ __device__ inline float wave_sum_f32(float x) {
   }));
 }
 
+// Reduction inside each 16-lane row on DPP lane moves (xor 1, xor 2, the
+// other quad of 8, the other 8 of 16): afterwards every lane of a row holds
+// the row's result.  Used to combine one value per wave (at most 16 waves),
+// read from LDS into lanes 0-15 of every row, with four instructions instead
+// of a read of every lane.  Every lane must be active.
+template <class Op>
+__device__ inline uint32_t row16_reduce_bits(uint32_t x, Op op) {
+  int v = int(x);
+  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false))));
+  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false))));
+  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false))));
+  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false))));
+  return uint32_t(v);
+}
+
+// Combines one value per wave, w_0..w_{nw-1} (nw <= 16): `mine` is lane l's
+// copy of w_{l mod 16} (the operation's identity where l mod 16 >= nw).  The
+// result is wave-uniform.
+template <class Op>
+__device__ inline uint32_t combine_waves_bits(uint32_t mine, Op op) {
+  return uint32_t(__builtin_amdgcn_readfirstlane(int(row16_reduce_bits(mine, op))));
+}
+__device__ inline float combine_waves_max_f32(float mine) {
+  return __uint_as_float(combine_waves_bits(__float_as_uint(mine), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
+  }));
+}
+__device__ inline float combine_waves_sum_f32(float mine) {
+  return __uint_as_float(combine_waves_bits(__float_as_uint(mine), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+  }));
+}
+__device__ inline uint32_t combine_waves_sum_u32(uint32_t mine) {
+  return combine_waves_bits(mine, [](uint32_t a, uint32_t b) { return a + b; });
+}
+__device__ inline uint32_t combine_waves_max_u32(uint32_t mine) {
+  return combine_waves_bits(mine, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+}
+__device__ inline uint32_t combine_waves_min_u32(uint32_t mine) {
+  return combine_waves_bits(mine, [](uint32_t a, uint32_t b) { return a < b ? a : b; });
+}
+
 // Inclusive prefix sum over the wave on DPP lane moves: a Hillis-Steele scan
 // inside each 16-lane row (row_shr 1, 2, 4, 8), then row 0's total into row 1
 // and row 2's into row 3 (row_bcast:15), then rows 0-1 into rows 2-3

@@ -48,8 +48,8 @@ constexpr uint32_t kBf16Base = 0x43434343u;  // high byte of bf16(128 + c), c < 
 __device__ constexpr int kSliceChan[8] = {0, 2, 1, 3, 4, 6, 5, 7};
 
 // LDS words: top-k scratch | block list | block-list stage | q~ table (4 heads
-// x 32 channels of bf16, in slice order) | per-wave partials | key list
-// (max(m_max, S)) | top-K_t stage (K_t ids, K_t scores).
+// x 32 channels of bf16, in slice order) | per-wave partials | list of keys in
+// play (max(m_max, S)) | top-K_t stage (K_t ids, K_t scores).
 __host__ __device__ inline size_t list_words(int S, int m_max) { return size_t(S > m_max ? S : m_max); }
 
 size_t mfma_select_lds_bytes(int S, int K_b, int K_t, int m_max) {
@@ -87,6 +87,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   }
   const int m = (n + B - 1) / B;
   const int lgB = __builtin_ctz(unsigned(B));  // B is a power of two here
+  const float sigma2 = sigma * 1.4426950408889634f;  // logits in base 2
 
   // block scores as keys (requested first: the longest dependency)
   uint32_t bk[kSelBPT];
@@ -204,7 +205,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
     const float sc = qp[i].x, off = qp[i].y - 128.0f * qp[i].x;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      lg[i][h] = valid ? sigma * fmaf(sc, acc[h], off * qsum[h]) : -INFINITY;
+      lg[i][h] = valid ? sigma2 * fmaf(sc, acc[h], off * qsum[h]) : -INFINITY;
       mx[h] = fmaxf(mx[h], lg[i][h]);
     }
   }
@@ -214,15 +215,10 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
     if (lane == 0) s_red[wid * 8 + h] = w;
   }
   __syncthreads();
+  static_assert(NW == 16, "one wave value per lane of a 16-lane row");
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const float v = s_red[(lane & 15) * 8 + h];
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, __uint_as_float(__builtin_amdgcn_readlane(__float_as_int(v), w)));
-    mx[h] = M;
-  }
-  // 3. exponentials and their per-head sums
+  for (int h = 0; h < G; ++h) mx[h] = combine_waves_max_f32(s_red[(lane & 15) * 8 + h]);
+  // 3. exponentials (base 2: the logits carry log2(e)) and their per-head sums
   float sum[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) sum[h] = 0.f;
@@ -230,7 +226,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   for (int i = 0; i < kSelSPT; ++i)
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const float e = ((vmask >> i) & 1u) ? __expf(lg[i][h] - mx[h]) : 0.f;
+      const float e = ((vmask >> i) & 1u) ? __builtin_amdgcn_exp2f(lg[i][h] - mx[h]) : 0.f;
       lg[i][h] = e;
       sum[h] += e;
     }
@@ -243,10 +239,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   float iz[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    const float v = s_red[(lane & 15) * 8 + 4 + h];
-    float Z = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) Z += __uint_as_float(__builtin_amdgcn_readlane(__float_as_int(v), w));
+    const float Z = combine_waves_sum_f32(s_red[(lane & 15) * 8 + 4 + h]);
     iz[h] = Z > 0.f ? 1.0f / Z : 0.f;
   }
   // 4. alpha keys in registers, top-K_t

@@ -56,7 +56,7 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   constexpr int kHistAll = align4w_c(4 * kTopkHistWords);
   uint32_t* hist = scratch;             // [4 passes][copies][stride]
-  uint32_t* misc = scratch + kHistAll;  // [64]: 0..47 wave partials, 48/49 pass result, 50 list length
+  uint32_t* misc = scratch + kHistAll;  // [64]: 0..47 wave partials, 48/49/51 pass result, 50 list length
   uint32_t* cg = misc + 64;             // [EPT][NW] keys > T per (slot, wave)
   uint32_t* ce = cg + kTopkMaxEPT * kTopkMaxNW;  // [EPT][NW] keys == T
 
@@ -82,16 +82,11 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
   if (tid == 0) misc[50] = 0u;
   __syncthreads();
   {
-    const uint32_t a = misc[lane & 15], b = misc[16 + (lane & 15)], c = misc[32 + (lane & 15)];
-    cnt = 0;
-    kmx = 0u;
-    kmn = 0xffffffffu;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      cnt += uint32_t(__builtin_amdgcn_readlane(int(a), w));
-      kmx = max(kmx, uint32_t(__builtin_amdgcn_readlane(int(b), w)));
-      kmn = min(kmn, uint32_t(__builtin_amdgcn_readlane(int(c), w)));
-    }
+    const int w = lane & 15;
+    const bool ok = w < NW;
+    cnt = combine_waves_sum_u32(ok ? misc[w] : 0u);
+    kmx = combine_waves_max_u32(ok ? misc[16 + w] : 0u);
+    kmn = combine_waves_min_u32(ok ? misc[32 + w] : 0xffffffffu);
   }
   const int kk = min(k, int(cnt));
 
@@ -138,12 +133,13 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
       const uint32_t incl = wave_incl_scan_u32(local);
       uint32_t run = incl - local;
       int found = -1;
-      uint32_t found_above = 0;
+      uint32_t found_above = 0, found_cnt = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         if (found < 0 && run + c[j] >= uint32_t(remaining)) {
           found = 255 - 4 * lane - j;
           found_above = run;
+          found_cnt = c[j];
         }
         run += c[j];
       }
@@ -152,6 +148,7 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
       if (lane == src) {
         misc[48] = uint32_t(found);
         misc[49] = found_above;
+        misc[51] = found_cnt == uint32_t(remaining) - found_above ? 1u : 0u;
       }
     }
     __syncthreads();
@@ -159,6 +156,13 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
     remaining -= int(misc[49]);
     pmask |= dmask << shift;
     bits_left -= nb;
+    if (misc[51] && bits_left > 0 && prefix != 0u) {
+      // the threshold's bucket is taken whole: every key >= prefix is
+      // selected, i.e. T = prefix - 1 with no equal keys to take
+      prefix -= 1u;
+      remaining = 0;
+      bits_left = 0;
+    }
     if (list_n < 0 && bits_left > 0) {
       // gather the keys still in play; one list reservation per wave
       uint32_t wcount = 0;
