@@ -89,10 +89,19 @@ __global__ __launch_bounds__(256) void block_score_kernel(
     const S* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
     for (int c = threadIdx.x; c < d; c += 256) {
       float p = 0.f, ng = 0.f;
-      for (int h = 0; h < G; ++h) {
-        float x = E::to_f(qg[size_t(h) * d + c]);
-        p += fmaxf(x, 0.f);
-        ng += fminf(x, 0.f);
+      // four heads' values requested together (one memory latency, not four)
+      for (int h0 = 0; h0 < G; h0 += 4) {
+        S x[4];
+#pragma unroll
+        for (int hh = 0; hh < 4; ++hh) x[hh] = qg[size_t(h0 + hh < G ? h0 + hh : G - 1) * d + c];
+#pragma unroll
+        for (int hh = 0; hh < 4; ++hh) {
+          if (h0 + hh < G) {
+            const float v = E::to_f(x[hh]);
+            p += fmaxf(v, 0.f);
+            ng += fminf(v, 0.f);
+          }
+        }
       }
       s_qp[c] = p;
       s_qn[c] = ng;
@@ -112,23 +121,27 @@ __global__ __launch_bounds__(256) void block_score_kernel(
     }
   }
   const size_t ubase = size_t(unit) * m_max;
+  // Loads are unconditional at clamped rows so that, with no branch around
+  // each load, all of them stay in flight together: a block past the
+  // work-group's last valid one re-reads that block (its result is replaced
+  // by -inf below), a lane past d reads channel 0 (its partial is dropped).
+  // Every row read is a written summary of the unit.
+  const int blk_hi = min(c1, m) - 1;  // >= c0 here
   for (int b0 = c0 + grp; b0 < c1; b0 += NG * kBlkUnroll) {
     uint4 vmax[kBlkUnroll][CPL], vmin[kBlkUnroll][CPL];
 #pragma unroll
     for (int u = 0; u < kBlkUnroll; ++u) {
       const int blk = b0 + u * NG;
+      const int rb = blk < blk_hi ? blk : blk_hi;
 #pragma unroll
       for (int k = 0; k < CPL; ++k) {
         const int c = li + k * LPB;
-        if (blk < c1 && blk < m && c < nch) {
-          vmax[u][k] = ld16_stream(kmax + (ubase + blk) * d + c * V);
-          vmin[u][k] = ld16_stream(kmin + (ubase + blk) * d + c * V);
-        } else {
-          vmax[u][k] = make_uint4(0, 0, 0, 0);
-          vmin[u][k] = make_uint4(0, 0, 0, 0);
-        }
+        const int rc = c < nch ? c : 0;
+        vmax[u][k] = ld16_stream(kmax + (ubase + rb) * d + rc * V);
+        vmin[u][k] = ld16_stream(kmin + (ubase + rb) * d + rc * V);
       }
     }
+    __builtin_amdgcn_sched_barrier(0);  // every load of the batch is issued before the first use
 #pragma unroll
     for (int u = 0; u < kBlkUnroll; ++u) {
       const int blk = b0 + u * NG;
@@ -138,8 +151,10 @@ __global__ __launch_bounds__(256) void block_score_kernel(
         float a[V], b[V];
         unpack16<E>(vmax[u][k], a);
         unpack16<E>(vmin[u][k], b);
+        float part = 0.f;
 #pragma unroll
-        for (int e = 0; e < V; ++e) acc = fmaf(qp[k][e], a[e], fmaf(qn[k][e], b[e], acc));
+        for (int e = 0; e < V; ++e) part = fmaf(qp[k][e], a[e], fmaf(qn[k][e], b[e], part));
+        acc += li + k * LPB < nch ? part : 0.f;  // a lane past d read channel 0: drop it
       }
       acc = wave_sum<LPB>(acc);
       if (li == 0 && blk < c1) out[blk] = blk < m ? acc : -INFINITY;
@@ -154,8 +169,7 @@ __global__ __launch_bounds__(1024) void block_topk_kernel(const float* __restric
                                                           int32_t* __restrict__ block_ids) {
   extern __shared__ uint32_t smem[];
   uint32_t* scratch = smem;
-  int32_t* stage = reinterpret_cast<int32_t*>(smem + topk_scratch_words(1024));
-  uint32_t* keys = smem + topk_scratch_words(1024) + align4w(K_b);
+  uint32_t* keys = smem + topk_scratch_words(1024);
   const int unit = blockIdx.x;
   const int s = unit / H_kv;
   int n = ctx_lens[s];
@@ -165,7 +179,7 @@ __global__ __launch_bounds__(1024) void block_topk_kernel(const float* __restric
   for (int i = threadIdx.x; i < m; i += 1024) keys[i] = float_key(sc[i]);
   __syncthreads();
   wg_topk_ascending<1024>(keys, m, K_b, block_ids + size_t(unit) * K_b, K_b, nullptr,
-                         [](int i) { return int32_t(i); }, scratch, stage, nullptr);
+                         [](int i) { return int32_t(i); }, scratch);
 }
 
 template <class E, int LPB, int CPL>
@@ -206,7 +220,7 @@ hipError_t launch_block_score(const Problem& P, const void* q, const void* kmax,
 hipError_t launch_block_topk(const Problem& P, const float* scores, const int32_t* ctx_lens, int K_b,
                              int32_t* block_ids, uint32_t* err, hipStream_t st) {
   (void)err;
-  const size_t lds = (topk_scratch_words(1024) + size_t(align4w(K_b)) + size_t(P.m_max)) * sizeof(uint32_t);
+  const size_t lds = (topk_scratch_words(1024) + size_t(P.m_max)) * sizeof(uint32_t);
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(block_topk_kernel),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));

@@ -404,16 +404,13 @@ __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __rest
   int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(1024));
   const int S = K_b * B;
   uint32_t* s_keys = smem + topk_scratch_words(1024) + align4w(K_b);
-  int32_t* stage = reinterpret_cast<int32_t*>(s_keys + S);
-  float* stage_sc = reinterpret_cast<float*>(stage + K_t);
   const int unit = blockIdx.x;
   for (int i = threadIdx.x; i < K_b; i += 1024) s_bl[i] = block_ids[size_t(unit) * K_b + i];
   for (int i = threadIdx.x; i < S; i += 1024) s_keys[i] = keys[size_t(unit) * S + i];
   __syncthreads();
   wg_topk_ascending<1024>(s_keys, S, K_t, token_ids + size_t(unit) * K_t, K_t,
                           token_scores ? token_scores + size_t(unit) * K_t : nullptr,
-                          [=](int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch, stage,
-                          stage_sc);
+                          [=](int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch);
 }
 
 template <int HT, int NGR>
@@ -468,7 +465,7 @@ hipError_t launch_token_alpha(const Problem& P, const float* logits, const float
 hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32_t* block_ids, int K_b,
                              int K_t, int32_t* token_ids, float* token_scores, hipStream_t st) {
   const size_t lds =
-      (topk_scratch_words(1024) + size_t(align4w(K_b)) + size_t(K_b) * P.B + 2 * size_t(K_t)) * sizeof(uint32_t);
+      (topk_scratch_words(1024) + size_t(align4w(K_b)) + size_t(K_b) * P.B) * sizeof(uint32_t);
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(token_topk_kernel),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));

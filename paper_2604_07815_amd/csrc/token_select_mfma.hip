@@ -47,14 +47,14 @@ constexpr uint32_t kBf16Base = 0x43434343u;  // high byte of bf16(128 + c), c < 
 // (offsets from 8w): the low nibbles of two bytes, then their high nibbles.
 __device__ constexpr int kSliceChan[8] = {0, 2, 1, 3, 4, 6, 5, 7};
 
-// LDS words: top-k scratch | block list | block-list stage | q~ table (4 heads
-// x 32 channels of bf16, in slice order) | per-wave partials | list of keys in
-// play (max(m_max, S)) | top-K_t stage (K_t ids, K_t scores).
+// LDS words: top-k scratch | block list | q~ table (4 heads x 32 channels of
+// bf16, in slice order) | per-wave partials | list of keys in play
+// (max(m_max, S)).
 __host__ __device__ inline size_t list_words(int S, int m_max) { return size_t(S > m_max ? S : m_max); }
 
-size_t mfma_select_lds_bytes(int S, int K_b, int K_t, int m_max) {
-  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(2 * K_b)) + 64 + kSelNW * 8 +
-          align4w(int(list_words(S, m_max))) + 2 * size_t(K_t)) *
+size_t mfma_select_lds_bytes(int S, int K_b, int m_max) {
+  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(K_b)) + 64 + kSelNW * 8 +
+          align4w(int(list_words(S, m_max)))) *
          sizeof(uint32_t);
 }
 
@@ -69,13 +69,10 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   extern __shared__ uint32_t smem[];
   uint32_t* scratch = smem;
   int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(NT));
-  int32_t* s_bstage = s_bl + K_b;
-  uint16_t* s_qt = reinterpret_cast<uint16_t*>(s_bl + align4w(2 * K_b));  // [4][32] (64 words)
+  uint16_t* s_qt = reinterpret_cast<uint16_t*>(s_bl + align4w(K_b));  // [4][32] (64 words)
   float* s_red = reinterpret_cast<float*>(s_qt + 128);                    // [NW][8]
   uint32_t* list = reinterpret_cast<uint32_t*>(s_red + NW * 8);
   const int S = K_b * B;
-  int32_t* stage = reinterpret_cast<int32_t*>(list + align4w(int(list_words(S, m_max))));
-  float* stage_sc = reinterpret_cast<float*>(stage + K_t);
 
   const int unit = blockIdx.x;
   const int s = unit / H_kv, g = unit % H_kv;
@@ -124,8 +121,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
     s_qt[tid] = v;
   }
   if (block_scores) {
-    wg_topk_regs<NT, kSelBPT>(bk, K_b, s_bl, K_b, nullptr, [](int i) { return int32_t(i); }, scratch, list,
-                              s_bstage, nullptr);
+    wg_topk_regs<NT, kSelBPT>(bk, K_b, s_bl, K_b, nullptr, [](int i) { return int32_t(i); }, scratch, list);
   }
   __syncthreads();
 
@@ -255,8 +251,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   wg_topk_regs<NT, kSelSPT>(keys, K_t, token_ids + size_t(unit) * K_t, K_t,
                             token_scores ? token_scores + size_t(unit) * K_t : nullptr,
                             [=](int slot) { return int32_t((s_bl[slot >> lgB] << lgB) | (slot & (B - 1))); },
-                            scratch, list,
-                            stage, stage_sc);
+                            scratch, list);
   if (block_scores && block_ids_out)
     for (int i = tid; i < K_b; i += NT) block_ids_out[size_t(unit) * K_b + i] = s_bl[i];
 }
@@ -264,7 +259,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
 bool fused_token_select_ok(const Problem& P, int K_b, int K_t) {
   const int S = K_b * P.B;
   return P.dtype == 1 && P.G >= 1 && P.G <= kSelMaxG && P.d_c == 32 && (P.B & (P.B - 1)) == 0 && S <= kSelMaxSlots &&
-         P.m_max <= kSelMaxBlocks && mfma_select_lds_bytes(S, K_b, K_t, P.m_max) <= kSelMaxLds;
+         P.m_max <= kSelMaxBlocks && mfma_select_lds_bytes(S, K_b, P.m_max) <= kSelMaxLds;
 }
 
 template <int G>
@@ -272,7 +267,7 @@ static hipError_t launch_g(const Problem& P, const void* q, const uint8_t* codes
                            const int32_t* channels, const float* block_scores, const int32_t* block_ids_in,
                            int32_t* block_ids_out, const int32_t* ctx_lens, int K_b, int K_t, int32_t* token_ids,
                            float* token_scores, uint32_t* err, hipStream_t st) {
-  const size_t lds = mfma_select_lds_bytes(K_b * P.B, K_b, K_t, P.m_max);
+  const size_t lds = mfma_select_lds_bytes(K_b * P.B, K_b, P.m_max);
   auto kern = token_select_mfma_kernel<G>;
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),

@@ -35,10 +35,10 @@ __host__ __device__ constexpr int align4w(int words) { return (words + 3) & ~3; 
 // up to out_cap.  Thread t holds the keys of positions t + j*NT, j < EPT
 // (kInvalidKey marks an empty position, never selected).  out_scores
 // (nullable) receives key_float of each selected key.  `list` (LDS, as many
-// words as there are valid keys) is clobbered; `stage` / `stage_sc` (LDS,
-// out_cap entries) hold the result until one final copy, because a
-// work-group barrier waits for outstanding global stores.  Every thread of
-// the work-group must call it, with k uniform.
+// words as there are valid keys) is clobbered.  Each thread writes its own
+// selected positions straight to `out` (global memory, or LDS that the
+// caller reads after a barrier): no staging and no trailing barrier.  Every
+// thread of the work-group must call it, with k uniform.
 //
 // Method: an MSB-first radix select over the bits where the valid keys
 // differ (8-bit digits, LDS histograms) finds the k'-th largest key T and the
@@ -50,7 +50,7 @@ __host__ __device__ constexpr int align4w(int words) { return (words + 3) & ~3; 
 // barrier, so the output is ordered by position without a sort.
 template <int NT, int EPT, class Map>
 __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int out_cap, float* out_scores,
-                             Map map, uint32_t* scratch, uint32_t* list, int32_t* stage, float* stage_sc) {
+                             Map map, uint32_t* scratch, uint32_t* list) {
   constexpr int NW = NT / 64;
   static_assert(NW >= 1 && NW <= kTopkMaxNW && EPT >= 1 && EPT <= kTopkMaxEPT, "work-group shape");
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -242,21 +242,20 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
       const int eb = __builtin_amdgcn_readlane(int(pe), src) + lanes_below(be);
       if (g || (e && eb < r)) {
         const int pos = gb + min(eb, r);
-        stage[pos] = map(tid + j * NT);
-        if (out_scores) stage_sc[pos] = key_float(key);
+        out[pos] = map(tid + j * NT);
+        if (out_scores) out_scores[pos] = key_float(key);
       }
     }
-    __syncthreads();
   }
-  for (int i = tid; i < out_cap; i += NT) {
-    out[i] = i < kk ? stage[i] : -1;
-    if (out_scores) out_scores[i] = i < kk ? stage_sc[i] : 0.0f;
+  for (int i = kk + tid; i < out_cap; i += NT) {
+    out[i] = -1;
+    if (out_scores) out_scores[i] = 0.0f;
   }
 }
 
 template <int NT, int EPT, class Map>
 __device__ void wg_topk_lds_ept(uint32_t* keys, int n, int k, int32_t* out, int out_cap, float* out_scores, Map map,
-                                uint32_t* scratch, int32_t* stage, float* stage_sc) {
+                                uint32_t* scratch) {
   uint32_t kr[EPT];
 #pragma unroll
   for (int j = 0; j < EPT; ++j) {
@@ -265,19 +264,19 @@ __device__ void wg_topk_lds_ept(uint32_t* keys, int n, int k, int32_t* out, int 
   }
   // the key array becomes the list of keys in play once every thread has
   // read it (the selection's first barrier comes before any list write)
-  wg_topk_regs<NT, EPT>(kr, k, out, out_cap, out_scores, map, scratch, keys, stage, stage_sc);
+  wg_topk_regs<NT, EPT>(kr, k, out, out_cap, out_scores, map, scratch, keys);
 }
 
 // The same selection over keys[0, n) in LDS (clobbered), n <= NT*kTopkMaxEPT.
 template <int NT, class Map>
 __device__ void wg_topk_ascending(uint32_t* keys, int n, int k, int32_t* out, int out_cap, float* out_scores,
-                                  Map map, uint32_t* scratch, int32_t* stage, float* stage_sc) {
+                                  Map map, uint32_t* scratch) {
   const int ept = (n + NT - 1) / NT;
-  if (ept <= 1) wg_topk_lds_ept<NT, 1>(keys, n, k, out, out_cap, out_scores, map, scratch, stage, stage_sc);
-  else if (ept <= 2) wg_topk_lds_ept<NT, 2>(keys, n, k, out, out_cap, out_scores, map, scratch, stage, stage_sc);
-  else if (ept <= 4) wg_topk_lds_ept<NT, 4>(keys, n, k, out, out_cap, out_scores, map, scratch, stage, stage_sc);
-  else if (ept <= 8) wg_topk_lds_ept<NT, 8>(keys, n, k, out, out_cap, out_scores, map, scratch, stage, stage_sc);
-  else wg_topk_lds_ept<NT, 16>(keys, n, k, out, out_cap, out_scores, map, scratch, stage, stage_sc);
+  if (ept <= 1) wg_topk_lds_ept<NT, 1>(keys, n, k, out, out_cap, out_scores, map, scratch);
+  else if (ept <= 2) wg_topk_lds_ept<NT, 2>(keys, n, k, out, out_cap, out_scores, map, scratch);
+  else if (ept <= 4) wg_topk_lds_ept<NT, 4>(keys, n, k, out, out_cap, out_scores, map, scratch);
+  else if (ept <= 8) wg_topk_lds_ept<NT, 8>(keys, n, k, out, out_cap, out_scores, map, scratch);
+  else wg_topk_lds_ept<NT, 16>(keys, n, k, out, out_cap, out_scores, map, scratch);
 }
 
 }  // namespace tls
