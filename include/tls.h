@@ -115,10 +115,29 @@ typedef struct tls_kv_view {
   int64_t n_slots;         /* slots per unit (pooled view only) */
 } tls_kv_view;
 
+/* Operator run by tls_sparse_decode (tls_decode_opts.mode).  The two
+ * single-level operators are the baselines the paper measures its operator
+ * against (Sec. 5, kernel study): block-level selection alone (Quest) and
+ * full attention.
+ *   TLS_MODE_TWO_LEVEL    Sec. 4.1: block selection, token selection, then
+ *                         attention over the K_t selected tokens.
+ *   TLS_MODE_BLOCK_SPARSE block selection only, then attention over every
+ *                         valid token of the K_b selected blocks (up to
+ *                         K_b * B tokens).  K_t, codes, qparams and channels
+ *                         are not used; token_ids_in and token_ids_out must
+ *                         be NULL.  block_ids_in / block_ids_out work as in
+ *                         the two-level operator.
+ *   TLS_MODE_DENSE        no selection: attention over all ctx_len tokens
+ *                         of each sequence (full attention).  K_b, K_t and
+ *                         the index arrays are not used; every id argument
+ *                         must be NULL. */
+enum { TLS_MODE_TWO_LEVEL = 0, TLS_MODE_BLOCK_SPARSE = 1, TLS_MODE_DENSE = 2 };
+
 /* Optional knobs of tls_sparse_decode; pass NULL for defaults. */
 typedef struct tls_decode_opts {
   int32_t attn_splits;       /* token splits per unit in the attention stage; 0 = auto */
-  int32_t reserved[7];       /* must be zero                                            */
+  int32_t mode;              /* TLS_MODE_*; 0 = the two-level operator                  */
+  int32_t reserved[6];       /* must be zero                                            */
   hipEvent_t* stage_events;  /* NULL, or TLS_NUM_STAGE_EVENTS events recorded on the
                                 stream around the stages (skipped stages record
                                 back-to-back events)                                   */

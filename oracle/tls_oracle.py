@@ -271,6 +271,31 @@ def decode_unit(q_group, K, V, n, channels, k_b, k_t, B, sigma, index=None, bloc
     return res
 
 
+# ----------------------------------------------------------------------------
+# The single-level operators the paper measures against (Sec. 5, kernel
+# study): block-level selection alone (Quest) and full attention
+# ----------------------------------------------------------------------------
+
+def block_sparse_unit(q_group, K, V, n, k_b, B, sigma, summaries=None, block_ids=None):
+    """Block-level selection alone: M = the top-k_b blocks (Sec. 4.1 coarse
+    stage), then attention over every valid token of M."""
+    res = {}
+    if block_ids is None:
+        kmax, kmin = block_summaries(K, n, B) if summaries is None else summaries
+        block_ids, bscores = select_blocks(q_group, kmax, kmin, k_b)
+        res["block_scores"] = bscores
+    ids = candidates(block_ids, n, B)
+    o, lse = sparse_attention(q_group, K, V, ids, sigma)
+    res.update(block_ids=np.asarray(block_ids), token_ids=ids, out=o, lse=lse)
+    return res
+
+
+def dense_unit(q_group, K, V, n, sigma):
+    """Full attention over the n cached tokens."""
+    o, lse = sparse_attention(q_group, K, V, np.arange(int(n)), sigma)
+    return dict(out=o, lse=lse)
+
+
 def unit_views(q, K, V, s, g, group, mla, d_v):
     """(q_group, K_unit, V_unit) for sequence s and KV head g (float64 arrays)."""
     qg = q[s, g * group:(g + 1) * group]

@@ -22,12 +22,14 @@ __all__ = [
     "tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
     "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error",
     "make_layout", "alloc_workspace", "DTYPE_F32", "DTYPE_BF16", "EXPORTED_SYMBOLS",
+    "MODE_TWO_LEVEL", "MODE_BLOCK_SPARSE", "MODE_DENSE",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtls.so")
 
 OK, INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP_ERROR = 0, 1, 2, 3, 4
 DTYPE_F32, DTYPE_BF16 = 0, 1
+MODE_TWO_LEVEL, MODE_BLOCK_SPARSE, MODE_DENSE = 0, 1, 2
 NUM_STAGE_EVENTS = 8
 DEVERR_CTX_LEN, DEVERR_BLOCK_ID, DEVERR_TOKEN_ID, DEVERR_SLOT, DEVERR_POOL_FULL, DEVERR_CHANNEL = 1, 2, 4, 8, 16, 32
 
@@ -61,7 +63,7 @@ class KvView(ctypes.Structure):
 
 
 class DecodeOpts(ctypes.Structure):
-    _fields_ = [("attn_splits", ctypes.c_int32), ("reserved", ctypes.c_int32 * 7),
+    _fields_ = [("attn_splits", ctypes.c_int32), ("mode", ctypes.c_int32), ("reserved", ctypes.c_int32 * 6),
                 ("stage_events", ctypes.c_void_p)]
 
 
@@ -213,10 +215,12 @@ class KV:
 def tls_sparse_decode(layout, q, kv: KV, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t,
                       block_ids_in, token_ids_in, out, lse, block_ids_out, token_ids_out, ws,
                       attn_splits: int = 0, stage_events: Optional[Sequence[int]] = None,
-                      stream=None) -> None:
-    """One decode step.  stage_events: NUM_STAGE_EVENTS raw hipEvent_t handles."""
+                      mode: int = MODE_TWO_LEVEL, stream=None) -> None:
+    """One decode step.  stage_events: NUM_STAGE_EVENTS raw hipEvent_t handles;
+    mode: MODE_TWO_LEVEL, or one of the single-level baselines."""
     opts = DecodeOpts()
     opts.attn_splits = int(attn_splits)
+    opts.mode = int(mode)
     ev_arr = None
     if stage_events is not None:
         if len(stage_events) != NUM_STAGE_EVENTS:

@@ -23,7 +23,7 @@ constexpr int kMlaRow = kMlaMaxD + 8;  // padded row (elements) against bank con
 
 __global__ __launch_bounds__(256) void attn_mla_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp, const int32_t* __restrict__ slot_map,
-    int64_t n_slots, const int32_t* __restrict__ token_ids, const int32_t* __restrict__ ctx_lens, int H_q,
+    int64_t n_slots, const TokenList tl, const int32_t* __restrict__ ctx_lens, int H_q,
     int H_kv, int G, int d, int d_v, int T, int B, int m_max, int K_t, int ct, float sigma,
     float* __restrict__ po, float* __restrict__ plse, uint32_t* err) {
   __shared__ uint16_t s_q[kMlaMaxG * kMlaRow];
@@ -31,6 +31,7 @@ __global__ __launch_bounds__(256) void attn_mla_kernel(
   __shared__ float s_p[kMlaMaxG][kMlaCt];
   __shared__ float s_ml[kMlaMaxG][2];
   __shared__ int s_ok[kMlaCt];
+  __shared__ int s_tok[kMlaCt];
   const int unit = blockIdx.y, split = blockIdx.x, nsplit = gridDim.x;
   const int s = unit / H_kv, g = unit % H_kv;
   int n = ctx_lens[s];
@@ -44,21 +45,22 @@ __global__ __launch_bounds__(256) void attn_mla_kernel(
     *reinterpret_cast<uint4*>(s_q + h * kMlaRow + c * 8) = ld16(qg + size_t(h) * d + c * 8);
   }
   if (threadIdx.x < kMlaCt) {
-    int okv = 0;
+    int okv = 0, tok = -1;
     const int p = p0 + threadIdx.x;
     if (threadIdx.x < cnt) {
-      const int tok = token_ids[size_t(unit) * K_t + p];
-      if (tok >= 0) {
-        if (tok >= n) set_error(err, 4u);
-        else {
-          bool good = true;
-          kv_row(Kp, slot_map, n_slots, unit, T, B, m_max, d, tok, &good);
-          if (good) okv = 1;
-          else set_error(err, 8u);
-        }
+      bool bad = false;
+      tok = list_token(tl, unit, p, n, &bad);
+      if (bad) {
+        set_error(err, 4u);
+      } else if (tok >= 0) {
+        bool good = true;
+        kv_row(Kp, slot_map, n_slots, unit, T, B, m_max, d, tok, &good);
+        if (good) okv = 1;
+        else set_error(err, 8u);
       }
     }
     s_ok[threadIdx.x] = okv;
+    s_tok[threadIdx.x] = tok;
   }
   __syncthreads();
   for (int i = threadIdx.x; i < kMlaCt * nch; i += 256) {
@@ -66,7 +68,7 @@ __global__ __launch_bounds__(256) void attn_mla_kernel(
     uint4 v = make_uint4(0, 0, 0, 0);
     if (s_ok[t]) {
       bool good = true;
-      const int tok = token_ids[size_t(unit) * K_t + p0 + t];
+      const int tok = s_tok[t];
       const uint16_t* kr = kv_row(Kp, slot_map, n_slots, unit, T, B, m_max, d, tok, &good);
       v = ld16_stream(kr + c * 8);
     }
@@ -172,12 +174,27 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ po
   const int unit = blockIdx.x / G, h = blockIdx.x % G;
   const int s = unit / H_kv, g = unit % H_kv;
   const float* ls = plse + size_t(unit) * nsplit * G + h;
-  if (threadIdx.x < 64) {  // split weights e^{lse_i - M} / sum_j e^{lse_j - M}, one lane per split
-    const float l = int(threadIdx.x) < nsplit ? ls[size_t(threadIdx.x) * G] : -INFINITY;
-    const float M = wave_max_f32(l);
-    const float e = (M == -INFINITY) ? 0.f : exp_or_zero(l - M);
-    const float W = wave_sum_f32(e);
-    s_w[threadIdx.x] = W > 0.f ? e / W : 0.f;
+  if (threadIdx.x < 64) {  // split weights e^{lse_i - M} / sum_j e^{lse_j - M}; lane l holds splits l, l + 64, ...
+    constexpr int PER = kMaxSplits / 64;
+    static_assert(PER * 64 == kMaxSplits, "splits per lane");
+    float l[PER], e[PER];
+    float lm = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int i = int(threadIdx.x) + 64 * j;
+      l[j] = i < nsplit ? ls[size_t(i) * G] : -INFINITY;
+      lm = fmaxf(lm, l[j]);
+    }
+    const float M = wave_max_f32(lm);
+    float es = 0.f;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      e[j] = (M == -INFINITY) ? 0.f : exp_or_zero(l[j] - M);
+      es += e[j];
+    }
+    const float W = wave_sum_f32(es);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) s_w[threadIdx.x + 64 * j] = W > 0.f ? e[j] / W : 0.f;
     if (threadIdx.x == 0) s_lse = W > 0.f ? M + logf(W) : -INFINITY;
   }
   __syncthreads();
@@ -216,10 +233,10 @@ int gqa_auto_splits(const Problem& P, int K_t);
 bool mla_mfma_ok(const Problem& P);
 int mla_mfma_tokens_per_split();
 int mla_mfma_splits(const Problem& P, int K_t);
-hipError_t launch_attention_mla_mfma(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+hipError_t launch_attention_mla_mfma(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                                      const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
                                      uint32_t* err, hipStream_t st);
-hipError_t launch_attention_gqa(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+hipError_t launch_attention_gqa(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                                 const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
                                 uint32_t* err, hipStream_t st);
 
@@ -246,20 +263,20 @@ int attn_splits_for(const Problem& P, int K_t, int requested) {
   return ns < 1 ? 1 : ns;
 }
 
-hipError_t launch_attention(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+hipError_t launch_attention(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                             const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
                             uint32_t* err, hipStream_t st) {
   if (P.mla && mla_mfma_ok(P))
-    return launch_attention_mla_mfma(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
+    return launch_attention_mla_mfma(P, q, kv, tl, ctx_lens, K_t, nsplit, po, plse, err, st);
   if (P.mla) {
     dim3 grid(nsplit, P.units);
     const int ct = (K_t + nsplit - 1) / nsplit;
     attn_mla_kernel<<<grid, 256, 0, st>>>((const uint16_t*)q, (const uint16_t*)kv.k, kv.slot_map, kv.n_slots,
-                                          token_ids, ctx_lens, P.H_q, P.H_kv, P.G, P.d_qk, P.d_v, P.T, P.B,
+                                          tl, ctx_lens, P.H_q, P.H_kv, P.G, P.d_qk, P.d_v, P.T, P.B,
                                           P.m_max, K_t, ct, P.sigma, po, plse, err);
     return hipGetLastError();
   }
-  return launch_attention_gqa(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
+  return launch_attention_gqa(P, q, kv, tl, ctx_lens, K_t, nsplit, po, plse, err, st);
 }
 
 hipError_t launch_merge(const Problem& P, const float* po, const float* plse, int nsplit, void* out, float* lse,

@@ -59,7 +59,7 @@ template <class E, int D, int G>
 __global__ __launch_bounds__(256) void attn_gqa_kernel(
     const typename E::T* __restrict__ q, const typename E::T* __restrict__ Kp,
     const typename E::T* __restrict__ Vp, const int32_t* __restrict__ slot_map, int64_t n_slots,
-    const int32_t* __restrict__ token_ids, const int32_t* __restrict__ ctx_lens, int H_q, int H_kv, int T,
+    const TokenList tl, const int32_t* __restrict__ ctx_lens, int H_q, int H_kv, int T,
     int B, int m_max, int K_t, int tpw, float sigma, float* __restrict__ po, float* __restrict__ plse,
     uint32_t* err) {
   using S = typename E::T;
@@ -90,7 +90,6 @@ __global__ __launch_bounds__(256) void attn_gqa_kernel(
   const int p0 = split * tpw;
   const int cnt = max(0, min(tpw, K_t - p0));
   const int nch = (cnt + CT - 1) / CT;
-  const int32_t* ids = token_ids + size_t(unit) * K_t + p0;
 
   // this lane's gather rows for every chunk (row index within the unit's K/V
   // base, -1: skip); the lane's row group scores exactly these rows
@@ -103,8 +102,9 @@ __global__ __launch_bounds__(256) void attn_gqa_kernel(
       const int idx = c * CT + wid * RPW + i * RPI + rgi;
       int row = -1;
       if (idx < cnt) {
-        const int tok = ids[idx];
-        if (tok >= n) {
+        bool bad = false;
+        const int tok = list_token(tl, unit, p0 + idx, n, &bad);
+        if (bad) {
           if (li == 0) set_error(err, 4u);
         } else if (tok >= 0) {
           if (!slot_map) {
@@ -320,7 +320,7 @@ __device__ inline short bf16_bits_rne(float f) {
 template <int D, int G, int NW, int TPWV, bool WHOLE>
 __global__ __launch_bounds__(64 * NW) void attn_gqa_mfma_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp, const uint16_t* __restrict__ Vp,
-    const int32_t* __restrict__ slot_map, int64_t n_slots, const int32_t* __restrict__ token_ids,
+    const int32_t* __restrict__ slot_map, int64_t n_slots, const TokenList tl,
     const int32_t* __restrict__ ctx_lens, int H_q, int H_kv, int T, int B, int m_max, int K_t, int tpw,
     float sigma, float* __restrict__ po, float* __restrict__ plse, uint16_t* __restrict__ out,
     float* __restrict__ lse, uint32_t* err) {
@@ -354,12 +354,13 @@ __global__ __launch_bounds__(64 * NW) void attn_gqa_mfma_kernel(
 
   // resolve this wave's entries to rows of the unit's K/V base (-1: skip)
   {
-    const int32_t* ids = token_ids + size_t(unit) * K_t + p0 + size_t(w) * tpwv;
+    const int e0 = p0 + w * tpwv;
     for (int i = lane; i < nch * CT; i += 64) {
       int row = -1;
       if (i < cw) {
-        const int tok = ids[i];
-        if (tok >= n) {
+        bool bad = false;
+        const int tok = list_token(tl, unit, e0 + i, n, &bad);
+        if (bad) {
           set_error(err, 4u);
         } else if (tok >= 0) {
           if (!slot_map) {
@@ -629,7 +630,7 @@ int gqa_auto_splits(const Problem& P, int K_t) {
 }
 
 template <class E, int D, int G>
-static void launch_t(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+static void launch_t(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                      const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse, uint32_t* err,
                      hipStream_t st) {
   using S = typename E::T;
@@ -639,25 +640,25 @@ static void launch_t(const Problem& P, const void* q, const KvView& kv, const in
     constexpr int step = 16 * kAttnNW;  // whole tiles for every wave
     tpw = (tpw + step - 1) / step * step;
     attn_gqa_mfma_kernel<D, G, kAttnNW, kAttnMaxTPWBf16 / kAttnNW, false><<<grid, 64 * kAttnNW, 0, st>>>(
-        (const uint16_t*)q, (const uint16_t*)kv.k, (const uint16_t*)kv.v, kv.slot_map, kv.n_slots, token_ids,
+        (const uint16_t*)q, (const uint16_t*)kv.k, (const uint16_t*)kv.v, kv.slot_map, kv.n_slots, tl,
         ctx_lens, P.H_q, P.H_kv, P.T, P.B, P.m_max, K_t, tpw, P.sigma, po, plse, nullptr, nullptr, err);
   } else {
     tpw = (tpw + kAttnCT - 1) / kAttnCT * kAttnCT;
     attn_gqa_kernel<E, D, G><<<grid, 256, 0, st>>>((const S*)q, (const S*)kv.k, (const S*)kv.v, kv.slot_map,
-                                                   kv.n_slots, token_ids, ctx_lens, P.H_q, P.H_kv, P.T, P.B,
+                                                   kv.n_slots, tl, ctx_lens, P.H_q, P.H_kv, P.T, P.B,
                                                    P.m_max, K_t, tpw, P.sigma, po, plse, err);
   }
 }
 
 template <class E, int D>
-static bool launch_d(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+static bool launch_d(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                      const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse, uint32_t* err,
                      hipStream_t st) {
   switch (P.G) {
-    case 1: launch_t<E, D, 1>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
-    case 2: launch_t<E, D, 2>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
-    case 4: launch_t<E, D, 4>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
-    case 8: launch_t<E, D, 8>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
+    case 1: launch_t<E, D, 1>(P, q, kv, tl, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
+    case 2: launch_t<E, D, 2>(P, q, kv, tl, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
+    case 4: launch_t<E, D, 4>(P, q, kv, tl, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
+    case 8: launch_t<E, D, 8>(P, q, kv, tl, ctx_lens, K_t, nsplit, po, plse, err, st); return true;
     default: return false;
   }
 }
@@ -670,45 +671,45 @@ bool gqa_whole_ok(const Problem& P, int K_t) {
 }
 
 template <int D, int G>
-static void launch_whole_t(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+static void launch_whole_t(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                            const int32_t* ctx_lens, int K_t, void* out, float* lse, uint32_t* err, hipStream_t st) {
   constexpr int step = 16 * kWholeNW;
   const int tpw = (K_t + step - 1) / step * step;
   attn_gqa_mfma_kernel<D, G, kWholeNW, kWholeTPWV, true><<<dim3(1, P.units), 64 * kWholeNW, 0, st>>>(
-      (const uint16_t*)q, (const uint16_t*)kv.k, (const uint16_t*)kv.v, kv.slot_map, kv.n_slots, token_ids,
+      (const uint16_t*)q, (const uint16_t*)kv.k, (const uint16_t*)kv.v, kv.slot_map, kv.n_slots, tl,
       ctx_lens, P.H_q, P.H_kv, P.T, P.B, P.m_max, K_t, tpw, P.sigma, nullptr, nullptr, (uint16_t*)out, lse, err);
 }
 
 template <int D>
-static void launch_whole_d(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+static void launch_whole_d(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                            const int32_t* ctx_lens, int K_t, void* out, float* lse, uint32_t* err, hipStream_t st) {
   switch (P.G) {
-    case 1: launch_whole_t<D, 1>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st); break;
-    case 2: launch_whole_t<D, 2>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st); break;
-    case 4: launch_whole_t<D, 4>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st); break;
-    default: launch_whole_t<D, 8>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st); break;
+    case 1: launch_whole_t<D, 1>(P, q, kv, tl, ctx_lens, K_t, out, lse, err, st); break;
+    case 2: launch_whole_t<D, 2>(P, q, kv, tl, ctx_lens, K_t, out, lse, err, st); break;
+    case 4: launch_whole_t<D, 4>(P, q, kv, tl, ctx_lens, K_t, out, lse, err, st); break;
+    default: launch_whole_t<D, 8>(P, q, kv, tl, ctx_lens, K_t, out, lse, err, st); break;
   }
 }
 
-hipError_t launch_attention_gqa_whole(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+hipError_t launch_attention_gqa_whole(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                                       const int32_t* ctx_lens, int K_t, void* out, float* lse, uint32_t* err,
                                       hipStream_t st) {
   if (!gqa_whole_ok(P, K_t)) return hipErrorInvalidValue;
-  if (P.d_qk == 128) launch_whole_d<128>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st);
-  else launch_whole_d<64>(P, q, kv, token_ids, ctx_lens, K_t, out, lse, err, st);
+  if (P.d_qk == 128) launch_whole_d<128>(P, q, kv, tl, ctx_lens, K_t, out, lse, err, st);
+  else launch_whole_d<64>(P, q, kv, tl, ctx_lens, K_t, out, lse, err, st);
   return hipGetLastError();
 }
 
-hipError_t launch_attention_gqa(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+hipError_t launch_attention_gqa(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                                 const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
                                 uint32_t* err, hipStream_t st) {
   bool ok = false;
   if (P.dtype == 1) {
-    if (P.d_qk == 128) ok = launch_d<BF16, 128>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
-    else if (P.d_qk == 64) ok = launch_d<BF16, 64>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
+    if (P.d_qk == 128) ok = launch_d<BF16, 128>(P, q, kv, tl, ctx_lens, K_t, nsplit, po, plse, err, st);
+    else if (P.d_qk == 64) ok = launch_d<BF16, 64>(P, q, kv, tl, ctx_lens, K_t, nsplit, po, plse, err, st);
   } else {
-    if (P.d_qk == 128) ok = launch_d<F32, 128>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
-    else if (P.d_qk == 64) ok = launch_d<F32, 64>(P, q, kv, token_ids, ctx_lens, K_t, nsplit, po, plse, err, st);
+    if (P.d_qk == 128) ok = launch_d<F32, 128>(P, q, kv, tl, ctx_lens, K_t, nsplit, po, plse, err, st);
+    else if (P.d_qk == 64) ok = launch_d<F32, 64>(P, q, kv, tl, ctx_lens, K_t, nsplit, po, plse, err, st);
   }
   if (!ok) return hipErrorInvalidValue;
   return hipGetLastError();

@@ -76,7 +76,7 @@ __device__ inline short bf16_rne_bits(float f) {
 
 __global__ __launch_bounds__(256) void attn_mla_mfma_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kp, const int32_t* __restrict__ slot_map,
-    int64_t n_slots, const int32_t* __restrict__ token_ids, const int32_t* __restrict__ ctx_lens, int H_q,
+    int64_t n_slots, const TokenList tl, const int32_t* __restrict__ ctx_lens, int H_q,
     int H_kv, int T, int B, int m_max, int K_t, int tpw, float sigma, float* __restrict__ po,
     float* __restrict__ plse, uint32_t* err) {
   constexpr int CT = kMlaChunk;
@@ -101,12 +101,12 @@ __global__ __launch_bounds__(256) void attn_mla_mfma_kernel(
 
   // resolve entries to rows of the unit's K base (-1: skip)
   {
-    const int32_t* ids = token_ids + size_t(unit) * K_t + p0;
     for (int i = tid; i < nch * CT; i += 256) {
       int row = -1;
       if (i < cnt) {
-        const int tok = ids[i];
-        if (tok >= n) {
+        bool bad = false;
+        const int tok = list_token(tl, unit, p0 + i, n, &bad);
+        if (bad) {
           set_error(err, 4u);
         } else if (tok >= 0) {
           if (!slot_map) {
@@ -287,14 +287,14 @@ int mla_mfma_splits(const Problem& P, int K_t) {
   return ns < need ? need : ns;
 }
 
-hipError_t launch_attention_mla_mfma(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+hipError_t launch_attention_mla_mfma(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                                      const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
                                      uint32_t* err, hipStream_t st) {
   int tpw = (K_t + nsplit - 1) / nsplit;
   tpw = (tpw + kMlaChunk - 1) / kMlaChunk * kMlaChunk;
   if (tpw > kMlaMaxTPW) return hipErrorInvalidValue;
   attn_mla_mfma_kernel<<<dim3(nsplit, P.units), 256, 0, st>>>(
-      (const uint16_t*)q, (const uint16_t*)kv.k, kv.slot_map, kv.n_slots, token_ids, ctx_lens, P.H_q, P.H_kv, P.T,
+      (const uint16_t*)q, (const uint16_t*)kv.k, kv.slot_map, kv.n_slots, tl, ctx_lens, P.H_q, P.H_kv, P.T,
       P.B, P.m_max, K_t, tpw, P.sigma, po, plse, err);
   return hipGetLastError();
 }

@@ -20,6 +20,25 @@ __device__ inline const S* kv_row(const S* base, const int32_t* slot_map, int64_
   return base + ((unit * size_t(n_slots) + size_t(slot)) * B + tok % B) * d;
 }
 
+// Token of entry p of a unit's work list (-1: empty).  *bad turns true for
+// an explicit id at or past ctx_len n (the caller flags it and skips it).
+__device__ inline int list_token(const TokenList& L, size_t unit, int p, int n, bool* bad) {
+  if (L.kind == kListIds) {
+    const int t = L.ids[unit * size_t(L.stride) + p];
+    if (t >= n) {
+      *bad = true;
+      return -1;
+    }
+    return t < 0 ? -1 : t;
+  }
+  if (L.kind == kListBlocks) {
+    const int blk = L.ids[unit * size_t(L.stride) + p / L.B];
+    const int t = blk * L.B + p % L.B;
+    return blk < 0 || t >= n ? -1 : t;
+  }
+  return p < n ? p : -1;
+}
+
 __device__ inline float exp_or_zero(float x) { return x == -INFINITY ? 0.f : expf(x); }
 
 // Transposing butterfly all-reduce over the MASK*2 lanes of a lane group:

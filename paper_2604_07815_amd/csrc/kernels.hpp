@@ -20,7 +20,7 @@ struct Problem {
 
 // Capacity limits of this build (host validation rejects larger requests).
 constexpr int kMaxKeys = 12288;     // blocks per sequence, and K_b * B candidate slots
-constexpr int kMaxSplits = 64;      // attention splits per unit
+constexpr int kMaxSplits = 128;     // attention splits per unit
 constexpr int kMaxGroupGqa = 8;     // G for the VALU attention path
 constexpr int kTokenSlotsPerWG = 256;
 
@@ -67,15 +67,33 @@ struct KvView {
   const int32_t* slot_map;
   int64_t n_slots;
 };
+
+// The work list of the attention stage: which tokens each unit attends.
+//   kListIds:    ids = [units][stride] token positions (the two-level
+//                selection, or ids given by the caller), -1 = empty;
+//   kListBlocks: ids = [units][stride] block ids, entry p is token
+//                ids[p / B] * B + p % B (block-sparse attention over every
+//                token of the selected blocks), -1 blocks are empty;
+//   kListAll:    entry p is token p (dense attention), ids unused.
+// Derived positions at or past ctx_len are empty entries, not errors.
+enum : int { kListIds = 0, kListBlocks = 1, kListAll = 2 };
+struct TokenList {
+  const int32_t* ids;
+  int stride;
+  int kind;
+  int B;
+};
 int attn_tokens_per_split(const Problem& P);  // token capacity of one attention work-group
 int attn_splits_for(const Problem& P, int K_t, int requested);
 // Whole-unit attention (one work-group per unit writes the output directly;
 // no partials, no merge).  Valid when gqa_whole_ok().
 bool gqa_whole_ok(const Problem& P, int K_t);
-hipError_t launch_attention_gqa_whole(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+hipError_t launch_attention_gqa_whole(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                                       const int32_t* ctx_lens, int K_t, void* out, float* lse, uint32_t* err,
                                       hipStream_t st);
-hipError_t launch_attention(const Problem& P, const void* q, const KvView& kv, const int32_t* token_ids,
+// K_t here is the number of list entries per unit (the budget for kListIds,
+// stride * B for kListBlocks, max_ctx for kListAll).
+hipError_t launch_attention(const Problem& P, const void* q, const KvView& kv, const TokenList& tl,
                             const int32_t* ctx_lens, int K_t, int nsplit, float* po, float* plse,
                             uint32_t* err, hipStream_t st);
 hipError_t launch_merge(const Problem& P, const float* po, const float* plse, int nsplit, void* out,

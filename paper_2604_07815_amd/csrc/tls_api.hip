@@ -215,25 +215,67 @@ tls_status tls_select_tokens(const tls_layout* layout, const void* q, const uint
                                      token_scores, ws, stream, nullptr));
 }
 
-// Attention over the selected tokens and the split merge (stages 6 and 7).
+// Attention over a work list (stages 6 and 7): K_t entries per unit.
 static tls_status finish_decode(const Problem& P, const tls::Workspace& W, const void* q, const tls_kv_view* kv,
-                                const int32_t* ctx_lens, int K_t, const int32_t* tids, void* out, float* lse,
+                                const int32_t* ctx_lens, int K_t, const tls::TokenList& tl, void* out, float* lse,
                                 void* ws, int requested, hipEvent_t* ev, hipStream_t stream) {
   const int nsplit = tls::attn_splits_for(P, K_t, requested);
   tls::KvView view{kv->k, kv->v, kv->slot_map, kv->n_slots};
   if (nsplit == 1 && tls::gqa_whole_ok(P, K_t)) {
-    const hipError_t e = tls::launch_attention_gqa_whole(P, q, view, tids, ctx_lens, K_t, out, lse, err_word(ws),
+    const hipError_t e = tls::launch_attention_gqa_whole(P, q, view, tl, ctx_lens, K_t, out, lse, err_word(ws),
                                                          stream);
     if (ev) hipEventRecord(ev[6], stream);
     if (ev) hipEventRecord(ev[7], stream);
     return hip_status(e);
   }
-  hipError_t e = tls::launch_attention(P, q, view, tids, ctx_lens, K_t, nsplit, at<float>(ws, W.po),
+  hipError_t e = tls::launch_attention(P, q, view, tl, ctx_lens, K_t, nsplit, at<float>(ws, W.po),
                                        at<float>(ws, W.plse), err_word(ws), stream);
   if (ev) hipEventRecord(ev[6], stream);
   if (e == hipSuccess) e = tls::launch_merge(P, at<float>(ws, W.po), at<float>(ws, W.plse), nsplit, out, lse, stream);
   if (ev) hipEventRecord(ev[7], stream);
   return hip_status(e);
+}
+
+// The single-level baselines (TLS_MODE_BLOCK_SPARSE, TLS_MODE_DENSE): block
+// selection (unless given) and attention over every valid token of the
+// selected blocks, or attention over the whole context.
+static tls_status single_level_decode(const Problem& P, int mode, const void* q, const tls_kv_view* kv,
+                                      const int32_t* ctx_lens, const void* kmax, const void* kmin, int K_b, int K_t,
+                                      const int32_t* block_ids_in, const int32_t* token_ids_in, void* out,
+                                      float* lse, int32_t* block_ids_out, int32_t* token_ids_out, void* ws,
+                                      size_t ws_bytes, int requested, hipEvent_t* ev, hipStream_t stream) {
+  if (token_ids_in || token_ids_out) return TLS_ERR_INVALID_ARGUMENT;
+  const bool dense = mode == TLS_MODE_DENSE;
+  if (dense && (block_ids_in || block_ids_out)) return TLS_ERR_INVALID_ARGUMENT;
+  if (!dense && !block_ids_in && (!kmax || !kmin)) return TLS_ERR_INVALID_ARGUMENT;
+  tls_status st = check_budgets(P, dense ? 1 : K_b, 1);
+  if (st != TLS_OK) return st;
+  const int n_list = dense ? P.T : K_b * P.B;  // work-list entries per unit
+  st = check_attention(P, n_list);
+  if (st != TLS_OK) return st;
+  const tls::Workspace W = tls::plan_workspace(P, dense ? 1 : K_b, K_t > 0 ? K_t : 1);
+  if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  auto mark = [&](int i) {
+    if (ev) hipEventRecord(ev[i], stream);
+  };
+  mark(0);
+  hipError_t e = hipSuccess;
+  const int32_t* bids = block_ids_in;
+  if (!dense && !bids) {
+    int32_t* bo = block_ids_out ? block_ids_out : at<int32_t>(ws, W.bids);
+    e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.qpn), at<float>(ws, W.bscores),
+                                err_word(ws), stream);
+    mark(1);
+    if (e == hipSuccess) e = tls::launch_block_topk(P, at<float>(ws, W.bscores), ctx_lens, K_b, bo, err_word(ws), stream);
+    bids = bo;
+  } else {
+    mark(1);
+  }
+  for (int i = 2; i < 6; ++i) mark(i);
+  if (e != hipSuccess) return TLS_ERR_HIP;
+  const tls::TokenList tl = dense ? tls::TokenList{nullptr, 0, tls::kListAll, P.B}
+                                  : tls::TokenList{bids, K_b, tls::kListBlocks, P.B};
+  return finish_decode(P, W, q, kv, ctx_lens, n_list, tl, out, lse, ws, requested, ev, stream);
 }
 
 tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_kv_view* kv, const int32_t* ctx_lens,
@@ -249,6 +291,23 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
   if (!P.mla && !kv->v) return TLS_ERR_INVALID_ARGUMENT;
   if (P.mla && kv->v) return TLS_ERR_INVALID_ARGUMENT;
   if (kv->slot_map && kv->n_slots < 1) return TLS_ERR_INVALID_ARGUMENT;
+  int requested = 0, mode = TLS_MODE_TWO_LEVEL;
+  hipEvent_t* ev = nullptr;
+  if (opts) {
+    for (int i = 0; i < 6; ++i)
+      if (opts->reserved[i] != 0) return TLS_ERR_INVALID_ARGUMENT;
+    if (opts->attn_splits < 0 || opts->attn_splits > tls::kMaxSplits) return TLS_ERR_INVALID_ARGUMENT;
+    if (opts->mode < TLS_MODE_TWO_LEVEL || opts->mode > TLS_MODE_DENSE) return TLS_ERR_INVALID_ARGUMENT;
+    requested = opts->attn_splits;
+    mode = opts->mode;
+    ev = opts->stage_events;
+    if (ev)
+      for (int i = 0; i < TLS_NUM_STAGE_EVENTS; ++i)
+        if (!ev[i]) return TLS_ERR_INVALID_ARGUMENT;
+  }
+  if (mode != TLS_MODE_TWO_LEVEL)
+    return single_level_decode(P, mode, q, kv, ctx_lens, kmax, kmin, K_b, K_t, block_ids_in, token_ids_in, out,
+                               lse, block_ids_out, token_ids_out, ws, ws_bytes, requested, ev, stream);
   const bool sel_tokens = token_ids_in == nullptr;
   const bool sel_blocks = sel_tokens && block_ids_in == nullptr;
   if (sel_blocks && (!kmax || !kmin)) return TLS_ERR_INVALID_ARGUMENT;
@@ -257,18 +316,6 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
   if (st != TLS_OK) return st;
   st = check_attention(P, K_t);
   if (st != TLS_OK) return st;
-  int requested = 0;
-  hipEvent_t* ev = nullptr;
-  if (opts) {
-    for (int i = 0; i < 7; ++i)
-      if (opts->reserved[i] != 0) return TLS_ERR_INVALID_ARGUMENT;
-    if (opts->attn_splits < 0 || opts->attn_splits > tls::kMaxSplits) return TLS_ERR_INVALID_ARGUMENT;
-    requested = opts->attn_splits;
-    ev = opts->stage_events;
-    if (ev)
-      for (int i = 0; i < TLS_NUM_STAGE_EVENTS; ++i)
-        if (!ev[i]) return TLS_ERR_INVALID_ARGUMENT;
-  }
   const tls::Workspace W = tls::plan_workspace(P, K_b, K_t);
   if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
 
@@ -297,7 +344,8 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
     mark(4);
     mark(5);
     if (e != hipSuccess) return TLS_ERR_HIP;
-    return finish_decode(P, W, q, kv, ctx_lens, K_t, to, out, lse, ws, requested, ev, stream);
+    return finish_decode(P, W, q, kv, ctx_lens, K_t, tls::TokenList{to, K_t, tls::kListIds, P.B}, out, lse, ws,
+                         requested, ev, stream);
   }
   if (sel_blocks) {
     int32_t* bo = block_ids_out ? block_ids_out : at<int32_t>(ws, W.bids);
@@ -322,7 +370,8 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
   }
   mark(5);
   if (e != hipSuccess) return TLS_ERR_HIP;
-  return finish_decode(P, W, q, kv, ctx_lens, K_t, tids, out, lse, ws, requested, ev, stream);
+  return finish_decode(P, W, q, kv, ctx_lens, K_t, tls::TokenList{tids, K_t, tls::kListIds, P.B}, out, lse, ws,
+                       requested, ev, stream);
 }
 
 tls_status tls_prefetch_blocks(const tls_layout* layout, const void* host_k, const void* host_v,

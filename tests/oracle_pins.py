@@ -278,6 +278,40 @@ def pin_invariants_and_planted(n_override=None):
         assert np.all(np.isfinite(r["out"]))
 
 
+def pin_single_level_operators(n_override=None):
+    """The baselines: full attention equals torch's float64 SDPA over the n
+    tokens; block-sparse attention attends exactly the valid tokens of the
+    top-k_b blocks, equals the two-level operator with k_t >= those tokens,
+    equals full attention when k_b covers every block, and keeps the planted
+    blocks."""
+    cfg, d, q, K, V = _toy_f64(n_override)
+    n = int(d["ctx_lens"][0])
+    m = O.num_blocks(n, cfg.block)
+    G = cfg.group
+    for g in range(cfg.h_kv):
+        qg = q[0, g * G:(g + 1) * G]
+        dn = O.dense_unit(qg, K[0, g], V[0, g], n, cfg.sigma)
+        kk = torch.from_numpy(K[0, g, :n])[None, None].expand(1, G, -1, -1)
+        vv = torch.from_numpy(V[0, g, :n])[None, None].expand(1, G, -1, -1)
+        ref = torch.nn.functional.scaled_dot_product_attention(torch.from_numpy(qg)[None, :, None, :], kk, vv,
+                                                               scale=cfg.sigma)[0, :, 0].numpy()
+        np.testing.assert_allclose(dn["out"], ref, rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(dn["lse"], scipy.special.logsumexp(cfg.sigma * qg @ K[0, g, :n].T, axis=1),
+                                   rtol=1e-12)
+        bs = O.block_sparse_unit(qg, K[0, g], V[0, g], n, cfg.k_b, cfg.block, cfg.sigma)
+        M = bs["block_ids"]
+        want = [j for j in range(n) if j // cfg.block in set(M.tolist())]
+        assert bs["token_ids"].tolist() == want
+        two = O.decode_unit(qg, K[0, g], V[0, g], n, d["channels"][g], cfg.k_b, cfg.k_b * cfg.block, cfg.block,
+                            cfg.sigma)
+        assert np.array_equal(two["block_ids"], M) and np.array_equal(two["token_ids"], bs["token_ids"])
+        np.testing.assert_array_equal(two["out"], bs["out"])
+        planted = [st + i for st in d["plant_starts"][0, g] for i in range(cfg.cluster_len)]
+        assert set(p // cfg.block for p in planted) <= set(M.tolist())
+        full = O.block_sparse_unit(qg, K[0, g], V[0, g], n, m, cfg.block, cfg.sigma)
+        np.testing.assert_allclose(full["out"], dn["out"], rtol=1e-12, atol=1e-14)
+
+
 def pin_lagged_schedule():
     """Offloaded schedule (Sec. 4.2): T_t = M_t minus C_t, C_{t+1} = M_t; with a
     frozen query (rho = 1) nothing is transferred after the first step and the
@@ -312,5 +346,5 @@ ALL_PINS = [
     pin_quest_golden, pin_quest_forms_agree, pin_quest_upper_bound, pin_topk_bruteforce,
     pin_candidates, pin_quant_golden, pin_quant_bound, pin_alpha_golden, pin_alpha_distribution,
     pin_attention_library, pin_attention_closed_form, pin_dense_equivalence,
-    pin_invariants_and_planted, pin_lagged_schedule,
+    pin_invariants_and_planted, pin_single_level_operators, pin_lagged_schedule,
 ]

@@ -15,8 +15,8 @@ LIB = os.path.join(ROOT, "paper_2604_07815_amd", "libtls.so")
 @pytest.fixture(scope="module")
 def tls():
     if not os.path.exists(LIB):
-        from paper_2604_07815_amd import build as b
-        b.build()
+        import __graft_entry__
+        __graft_entry__.build()
     import paper_2604_07815_amd as t
     return t
 
@@ -123,3 +123,27 @@ def test_null_pointers_are_rejected_before_launch(tls):
     st = lib.tls_prefetch_blocks(ctypes.byref(L), dummy, dummy, dummy, dummy, dummy, 8, dummy, dummy, 10,
                                  dummy, dummy, null, dummy, 1 << 40, null)
     assert st == 1
+
+
+def test_decode_modes_are_validated_before_launch(tls):
+    """Unknown operator modes and id arguments the single-level operators do
+    not take are rejected on the host."""
+    lib = _raw(tls)
+    L = _layout(tls)
+    dummy = ctypes.c_void_p(0x1000)
+    null = None
+    kv = tls.KvView(dummy.value, dummy.value, None, 0)
+
+    def call(mode, bids_in=None, tids_in=None, bids_out=None, tids_out=None):
+        opts = tls.DecodeOpts()
+        opts.mode = mode
+        return lib.tls_sparse_decode(ctypes.byref(L), dummy, ctypes.byref(kv), dummy, dummy, dummy, dummy, dummy,
+                                     dummy, 8, 128, bids_in, tids_in, dummy, null, bids_out, tids_out, dummy,
+                                     1 << 40, ctypes.byref(opts), null)
+
+    assert call(3) == 1 and call(-1) == 1
+    assert call(tls.MODE_DENSE, tids_in=dummy) == 1
+    assert call(tls.MODE_DENSE, bids_in=dummy) == 1
+    assert call(tls.MODE_DENSE, bids_out=dummy) == 1
+    assert call(tls.MODE_BLOCK_SPARSE, tids_in=dummy) == 1
+    assert call(tls.MODE_BLOCK_SPARSE, tids_out=dummy) == 1

@@ -39,7 +39,7 @@ def test_empty_and_tiny_contexts(splits):
     assert tls.tls_check_device_error(r["ws"]) == 0
 
 
-@pytest.mark.parametrize("splits", [1, 3, 16, 64])
+@pytest.mark.parametrize("splits", [1, 3, 16, 64, 100, 128])
 def test_split_merge_invariance(splits):
     """LSE merge of split partials equals an unsplit computation."""
     cfg = synth.config("toy")
@@ -50,7 +50,7 @@ def test_split_merge_invariance(splits):
     np.testing.assert_allclose(r["lse"].cpu().numpy(), base["lse"].cpu().numpy(), rtol=2e-6, atol=2e-6)
 
 
-@pytest.mark.parametrize("splits", [1, 2, 5, 64])
+@pytest.mark.parametrize("splits", [1, 2, 5, 64, 128])
 def test_split_merge_invariance_bf16(splits):
     """bf16: one work-group per unit (splits=1, output written directly) and
     split partials merged by LSE agree to bf16 rounding, and each matches the
