@@ -44,6 +44,7 @@ def parse():
     ap.add_argument("--workload", default="gqa_b32_ctx96k", choices=sorted(WORKLOADS))
     ap.add_argument("--copies", type=int, default=0, help="layer copies rotated (0: auto)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-modes", action="store_true", help="skip timing the single-level operators")
     ap.add_argument("--cpu-units", type=int, default=48, help="units of the oracle sample")
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + steps of the decode only (for rocprofv3), print nothing else")
@@ -349,6 +350,34 @@ def main():
     torch.cuda.synchronize()
     attn_ms = start.elapsed_time(stop) / args.steps
 
+    # ---- the single-level operators on the same workload (the paper's baselines) ----
+    modes = {}
+    if not args.no_modes:
+        def time_mode(mode, k_b, steps):
+            def f(i):
+                L = layers[i % len(layers)]
+                tls.tls_sparse_decode(layout, L["q"], tls.KV(L["k"], L["v"]), ctx_t, L["kmax"], L["kmin"], None, None,
+                                      None, k_b, cfg.k_t, None, None, attn_out, None, None, None, ws, mode=mode)
+            for i in range(2):
+                f(i)
+            torch.cuda.synchronize()
+            start.record()
+            for i in range(steps):
+                f(i)
+            stop.record()
+            torch.cuda.synchronize()
+            return start.elapsed_time(stop) / steps * 1e3
+        ms = max(4, min(args.steps, 20))
+        modes["two_level_us"] = round(ms_per_step * 1e3, 2)
+        modes["block_sparse_same_blocks_us"] = round(time_mode(tls.MODE_BLOCK_SPARSE, cfg.k_b, ms), 2)
+        kb_eq = max(1, cfg.k_t // cfg.block)
+        modes["block_sparse_same_tokens_us"] = round(time_mode(tls.MODE_BLOCK_SPARSE, kb_eq, ms), 2)
+        modes["dense_us"] = round(time_mode(tls.MODE_DENSE, cfg.k_b, ms), 2)
+        modes["speedup_vs_dense"] = round(modes["dense_us"] / modes["two_level_us"], 2)
+        modes["note"] = (f"same inputs; block-sparse attends every token of the top-{cfg.k_b} blocks "
+                         f"({cfg.k_b * cfg.block} tokens) or of the top-{kb_eq} blocks ({kb_eq * cfg.block} tokens, "
+                         f"the two-level token budget); dense attends all ctx_len tokens")
+
     err = tls.tls_check_device_error(ws)
     nb = algorithmic_bytes(cfg, d["ctx_host"], bids.cpu().numpy(), e)
     us = ms_per_step * 1e3
@@ -384,6 +413,7 @@ def main():
         "stage_marked_step_us": round(marked_ms * 1e3, 2),
         "index_build_ms": round(index_build_ms, 3),
         "device_error_flags": err,
+        "operators": modes or None,
         "roofline": {
             "kernel": "attn_mla_mfma_kernel" if cfg.mla else
                       ("attn_gqa_mfma_kernel" if cfg.dtype == "bf16" else "attn_gqa_kernel"),
