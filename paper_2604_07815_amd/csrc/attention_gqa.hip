@@ -596,19 +596,42 @@ static int mfma_wgs_per_cu_g(int G) {
   }
 }
 
+static int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    cus = 256;
+  return cus;
+}
+
+constexpr int kWideMinTokens = 768;  // tokens per 12-wave split work-group worth its prologue
+
+// Split mode with 12-wave work-groups (the whole-unit kernel writing
+// partials): chosen when the launch fits the compute units in one round and
+// every work-group still has several tiles per wave, so each compute unit
+// keeps twelve waves of gathers in flight instead of four.
+static bool gqa_use_wide(const Problem& P, int K_t, int nsplit, int cus) {
+  if (P.dtype != 1 || nsplit < 2 || long(P.units) * nsplit > cus) return false;
+  const int tpw = (K_t + nsplit - 1) / nsplit;
+  return tpw >= kWideMinTokens && tpw <= kWholeNW * kWholeTPWV - 16 * kWholeNW;
+}
+
 // Split count for the bf16 kernel: the work-groups of one launch are
 // scheduled in rounds of (compute units x resident work-groups); pick the
 // split count that minimises rounds x (tokens per work-group + a fixed
 // per-work-group cost), fewest splits on ties.  0: not this kernel.
 int gqa_auto_splits(const Problem& P, int K_t) {
   if (P.dtype != 1 || K_t < 1) return 0;
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
-    cus = 256;
+  const int cus = device_cus();
   // whole units (one 12-wave work-group each, no partials, no merge) when
   // they fill the compute units in whole rounds
   if (gqa_whole_ok(P, K_t) && P.units % cus == 0) return 1;
+  // fewer units than compute units: as many 12-wave splits as fit in one round
+  if (P.units * 2 <= cus) {
+    const int ns = cus / P.units;
+    for (int w = ns; w >= 2; --w)
+      if (gqa_use_wide(P, K_t, w, cus)) return w;
+  }
   const int occ = P.d_qk == 64 ? mfma_wgs_per_cu_g<64>(P.G) : mfma_wgs_per_cu_g<128>(P.G);
   const long slots = long(cus) * occ;
   constexpr long kFixedTokens = 64;  // prologue and merge cost of one work-group, in tokens
@@ -637,6 +660,14 @@ static void launch_t(const Problem& P, const void* q, const KvView& kv, const To
   dim3 grid(nsplit, P.units);
   int tpw = (K_t + nsplit - 1) / nsplit;
   if constexpr (E::kIsBf16) {
+    if (gqa_use_wide(P, K_t, nsplit, device_cus())) {
+      constexpr int wstep = 16 * kWholeNW;
+      tpw = (tpw + wstep - 1) / wstep * wstep;
+      attn_gqa_mfma_kernel<D, G, kWholeNW, kWholeTPWV, false><<<grid, 64 * kWholeNW, 0, st>>>(
+          (const uint16_t*)q, (const uint16_t*)kv.k, (const uint16_t*)kv.v, kv.slot_map, kv.n_slots, tl, ctx_lens,
+          P.H_q, P.H_kv, P.T, P.B, P.m_max, K_t, tpw, P.sigma, po, plse, nullptr, nullptr, err);
+      return;
+    }
     constexpr int step = 16 * kAttnNW;  // whole tiles for every wave
     tpw = (tpw + step - 1) / step * step;
     attn_gqa_mfma_kernel<D, G, kAttnNW, kAttnMaxTPWBf16 / kAttnNW, false><<<grid, 64 * kAttnNW, 0, st>>>(

@@ -86,3 +86,24 @@ def test_out_of_range_token_id_sets_error_flag():
         ref = c.oracle_unit(0, g, token_ids=np.array([5, 999]))
         G = cfg.group
         H.check_close(r["out"][0, g * G:(g + 1) * G].cpu().numpy(), ref["out"], cfg.dtype, "out")
+
+
+@pytest.mark.parametrize("splits", [2, 3])
+def test_wide_split_attention(splits):
+    """Few units, long token lists: the split attention runs 12-wave
+    work-groups writing partials; it matches the whole-unit result to bf16
+    rounding and the oracle on the same token ids."""
+    cfg = synth.config("qwen3_gqa_48k").replace(batch=2, ctx_lo=20000, ctx_hi=30000, clusters=4, k_b=64, k_t=2048,
+                                               seed=91)
+    c = H.Case(cfg, backend="host").build_index()
+    base = c.decode(attn_splits=1)
+    r = c.decode(attn_splits=splits)
+    assert torch.equal(r["tids"], base["tids"])
+    np.testing.assert_allclose(r["out"].float().cpu().numpy(), base["out"].float().cpu().numpy(), rtol=1e-2,
+                               atol=1e-2)
+    np.testing.assert_allclose(r["lse"].cpu().numpy(), base["lse"].cpu().numpy(), rtol=1e-5, atol=1e-5)
+    G = cfg.group
+    for (s, g) in c.units():
+        ref = c.oracle_unit(s, g, token_ids=r["tids"][s, g].cpu().numpy()[r["tids"][s, g].cpu().numpy() >= 0])
+        H.check_close(r["out"][s, g * G:(g + 1) * G].float().cpu().numpy(), ref["out"], cfg.dtype, f"out {(s, g)}")
+        H.check_close(r["lse"][s, g * G:(g + 1) * G].cpu().numpy(), ref["lse"], cfg.dtype, f"lse {(s, g)}")
