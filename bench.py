@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--copies", type=int, default=0, help="layer copies rotated (0: auto)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-modes", action="store_true", help="skip timing the single-level operators")
+    ap.add_argument("--offload", action="store_true",
+                    help="also run the offloaded-KV schedule of the 96k workload (full K/V in pinned host memory, "
+                         "lagged selection, side-stream prefetch over PCIe) and report it under 'offload'")
     ap.add_argument("--cpu-units", type=int, default=48, help="units of the oracle sample")
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + steps of the decode only (for rocprofv3), print nothing else")
@@ -220,6 +223,98 @@ def traffic_from_profiles(kernel_src_hash):
     if d.get("kernel_src_sha256") != kernel_src_hash:
         return None
     return d.get("traffic_bytes_per_launch")
+
+
+def offload_schedule(tls, synth, torch, np):
+    """The offloaded KV tier of the 96k workload (Sec. 4.2), as a serving loop:
+    K/V of every sequence in pinned host memory, block and token indices and
+    a pool of 2*K_b block slots per unit in HBM.  Per step t of the AR(1)
+    query walk: main stream selects M_t; the side stream brings T_t = M_t
+    minus the resident set into the pool over PCIe; meanwhile the main stream
+    selects tokens from M_{t-1} and attends over the pool; the main stream
+    waits for the transfer before step t+1.  Reported per step (median over
+    the walk): step wall time, decode time, transfer time and bytes."""
+    cfg = synth.config("offload_gqa_96k")
+    dev = torch.device("cuda", 0)
+    walk = synth.draw_query_walk(cfg)
+    d = synth.make_device(cfg, device=dev, pad="zero", q_store=walk[0])
+    dt = torch.bfloat16
+    layout = tls.make_layout(cfg.batch, cfg.h_q, cfg.h_kv, cfg.d_qk, cfg.d_v, cfg.max_ctx, index_channels=cfg.d_c,
+                             block_size=cfg.block, dtype=tls.DTYPE_BF16)
+    m_max = -(-cfg.max_ctx // cfg.block)
+    kmax = torch.empty((cfg.batch, cfg.h_kv, m_max, cfg.d_qk), dtype=dt, device=dev)
+    kmin = torch.empty_like(kmax)
+    codes = torch.empty((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 2), dtype=torch.uint8, device=dev)
+    qparams = torch.empty((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 32, 2), dtype=torch.float32, device=dev)
+    ctx, ch = d["ctx_lens"], d["channels"]
+    tls.tls_build_block_index(layout, d["k"], ctx, 0, cfg.max_ctx, kmax, kmin)
+    tls.tls_build_token_index(layout, d["k"], ctx, ch, 0, cfg.max_ctx, codes, qparams)
+    host_k = torch.empty(d["k"].shape, dtype=dt, pin_memory=True)
+    host_v = torch.empty(d["v"].shape, dtype=dt, pin_memory=True)
+    host_k.copy_(d["k"])
+    host_v.copy_(d["v"])
+    del d
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    B, units, K_b = cfg.block, cfg.batch * cfg.h_kv, cfg.k_b
+    n_slots = 2 * K_b
+    pool_k = torch.zeros((units, n_slots, B, cfg.d_qk), dtype=dt, device=dev)
+    pool_v = torch.zeros((units, n_slots, B, cfg.d_v), dtype=dt, device=dev)
+    slot_map = torch.full((units, m_max), -1, dtype=torch.int32, device=dev)
+    slot_owner = torch.full((units, n_slots), -1, dtype=torch.int32, device=dev)
+    tcount = torch.zeros(units, dtype=torch.int32, device=dev)
+    ws = tls.alloc_workspace(layout, K_b, cfg.k_t, device=dev)
+    kv = tls.KV(pool_k, pool_v, slot_map, n_slots)
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    qs = [synth.host_to_torch(walk[t], cfg.dtype).to(dev) for t in range(walk.shape[0])]
+    out = torch.empty((cfg.batch, cfg.h_q, cfg.d_v), dtype=dt, device=dev)
+    M = [torch.empty((cfg.batch, cfg.h_kv, K_b), dtype=torch.int32, device=dev) for _ in range(2)]
+    tls.tls_select_blocks(layout, qs[0], kmax, kmin, ctx, K_b, M[0], None, ws)
+    tls.tls_prefetch_blocks(layout, host_k, host_v, ctx, M[0], None, K_b, pool_k, pool_v, n_slots, slot_map,
+                            slot_owner, tcount, ws)
+    torch.cuda.synchronize()
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    rec = []
+    for t in range(1, walk.shape[0]):
+        M_prev, M_t = M[(t - 1) % 2], M[t % 2]
+        e0, e_sel, e_dec, e1, p0, p1 = ev(), ev(), ev(), ev(), ev(), ev()
+        e0.record(main)
+        tls.tls_select_blocks(layout, qs[t], kmax, kmin, ctx, K_b, M_t, None, ws)
+        e_sel.record(main)
+        side.wait_event(e_sel)
+        p0.record(side)
+        tls.tls_prefetch_blocks(layout, host_k, host_v, ctx, M_t, M_prev, K_b, pool_k, pool_v, n_slots, slot_map,
+                                slot_owner, tcount, ws, stream=side)
+        p1.record(side)
+        tls.tls_sparse_decode(layout, qs[t], kv, ctx, kmax, kmin, codes, qparams, ch, K_b, cfg.k_t, M_prev, None,
+                              out, None, None, None, ws)
+        e_dec.record(main)
+        main.wait_event(p1)
+        e1.record(main)
+        e1.synchronize()
+        moved = int(tcount.sum().item())
+        rec.append(dict(wall=e0.elapsed_time(e1) * 1e3, select=e0.elapsed_time(e_sel) * 1e3,
+                        decode=e_sel.elapsed_time(e_dec) * 1e3, xfer=p0.elapsed_time(p1) * 1e3, blocks=moved))
+    err = tls.tls_check_device_error(ws)
+    block_bytes = B * (cfg.d_qk + cfg.d_v) * 2
+    med = lambda k: float(np.median([r[k] for r in rec]))  # noqa: E731
+    blocks = float(np.mean([r["blocks"] for r in rec]))
+    xfer_bytes = blocks * block_bytes
+    return {
+        "workload": "offload_gqa_96k: b=32, 32/8 heads, d=128, bf16, n=98304, K_b=128, K_t=2048, "
+                    f"{len(rec)} steps of an AR(1) query walk (rho={cfg.rho}); K/V {2 * host_k.numel() * 2 / 1e9:.1f} GB "
+                    f"in pinned host memory, pool of {n_slots} slots per unit in HBM",
+        "step_wall_us_median": round(med("wall"), 1),
+        "select_blocks_us_median": round(med("select"), 1),
+        "decode_from_pool_us_median": round(med("decode"), 1),
+        "transfer_us_median": round(med("xfer"), 1),
+        "blocks_moved_per_step_mean": round(blocks, 1),
+        "block_repeat_rate": round(1.0 - blocks / (units * K_b), 4),
+        "transfer_MB_per_step_mean": round(xfer_bytes / 1e6, 1),
+        "pcie_GBps": round(xfer_bytes / (med("xfer") * 1e-6) / 1e9, 1),
+        "device_error_flags": err,
+    }
 
 
 def main():
@@ -449,6 +544,11 @@ def main():
             "sample": f"{len(pick)} of {len(units_all)} (sequence, KV head) units, float64 NumPy oracle decode "
                       f"step on prebuilt indices, {cores} worker processes, {wall:.2f} s wall; scaled to all units",
         }
+    if args.offload:
+        del layers, layer, d
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        result["offload"] = offload_schedule(tls, synth, torch, np)
     print(json.dumps(result), flush=True)
 
 

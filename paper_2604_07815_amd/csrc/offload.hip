@@ -9,7 +9,8 @@
 //   3. give the k-th block of T_t (ascending id) the k-th free slot
 //      (ascending), updating slot_map and slot_owner;
 //   4. copy those blocks' rows from pinned host memory into the pool with
-//      device-side loads over PCIe (no host round trip for T_t).
+//      device-side loads over PCIe (no host round trip for T_t), on a few
+//      work-groups that leave the chip to the overlapping decode step.
 // The copy reads rows [iB, min((i+1)B, ctx_len)) of block i.
 #include "kernels.hpp"
 
@@ -103,33 +104,56 @@ __global__ __launch_bounds__(256) void prefetch_plan_kernel(
   }
 }
 
-// One work-group per (transfer entry, unit): copies one block of K (and V).
-template <int D_BYTES_MAX>
-__global__ __launch_bounds__(256) void prefetch_copy_kernel(
-    const uint8_t* __restrict__ host_k, const uint8_t* __restrict__ host_v, const int32_t* __restrict__ ctx_lens,
-    const int32_t* __restrict__ xfer, int K_b, int H_kv, int T, int B, int row_k, int row_v, int64_t n_slots,
-    uint8_t* __restrict__ pool_k, uint8_t* __restrict__ pool_v) {
-  const int k = blockIdx.x, unit = blockIdx.y;
-  const int32_t* list = xfer + size_t(unit) * (2 * K_b + 1);
-  if (k >= list[0]) return;
-  const int b = list[1 + 2 * k], sl = list[2 + 2 * k];
-  const int s = unit / H_kv;
-  int n = ctx_lens[s];
-  n = n < 0 ? 0 : (n > T ? T : n);
-  const int r0 = b * B, r1 = min(r0 + B, n);
-  if (r1 <= r0) return;
-  const size_t rows = size_t(r1 - r0);
-  {
-    const size_t bytes = rows * row_k;
-    const uint8_t* src = host_k + (size_t(unit) * T + r0) * row_k;
-    uint8_t* dst = pool_k + (size_t(unit) * n_slots + sl) * size_t(B) * row_k;
-    for (size_t o = threadIdx.x * 16; o < bytes; o += 256 * 16) *reinterpret_cast<uint4*>(dst + o) = ld16(src + o);
+// The copy runs on a small, fixed number of work-groups so that it never
+// holds more than a few compute units while it waits on PCIe: the decode step
+// it overlaps with keeps the rest of the chip.  Work-group w walks units w,
+// w + gridDim.x, ...; for each entry of a unit's transfer list it copies the
+// block's K and V rows.  Every thread first requests all of its pieces of the
+// block (kCopyPieces 16-byte loads per row array, enough for B rows of up to
+// kCopyPieces * 4 KB / B bytes), then stores them, so each work-group keeps a
+// whole block in flight over the link.
+constexpr int kCopyWGs = 64;
+constexpr int kCopyThreads = 256;
+constexpr int kCopyPieces = 4;  // 16-byte pieces per thread and row array: 256 * 16 * 4 = 16 KB per block
+
+__device__ inline void copy_block_rows(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, size_t bytes) {
+  uint4 v[kCopyPieces];
+#pragma unroll
+  for (int i = 0; i < kCopyPieces; ++i) {
+    const size_t o = (size_t(i) * kCopyThreads + threadIdx.x) * 16;
+    if (o < bytes) v[i] = ld16(src + o);
   }
-  if (host_v) {
-    const size_t bytes = rows * row_v;
-    const uint8_t* src = host_v + (size_t(unit) * T + r0) * row_v;
-    uint8_t* dst = pool_v + (size_t(unit) * n_slots + sl) * size_t(B) * row_v;
-    for (size_t o = threadIdx.x * 16; o < bytes; o += 256 * 16) *reinterpret_cast<uint4*>(dst + o) = ld16(src + o);
+#pragma unroll
+  for (int i = 0; i < kCopyPieces; ++i) {
+    const size_t o = (size_t(i) * kCopyThreads + threadIdx.x) * 16;
+    if (o < bytes) *reinterpret_cast<uint4*>(dst + o) = v[i];
+  }
+  // rows larger than the unrolled span (not used by the shapes of this build)
+  for (size_t o = (size_t(kCopyPieces) * kCopyThreads + threadIdx.x) * 16; o < bytes; o += kCopyThreads * 16)
+    *reinterpret_cast<uint4*>(dst + o) = ld16(src + o);
+}
+
+__global__ __launch_bounds__(kCopyThreads) void prefetch_copy_kernel(
+    const uint8_t* __restrict__ host_k, const uint8_t* __restrict__ host_v, const int32_t* __restrict__ ctx_lens,
+    const int32_t* __restrict__ xfer, int units, int K_b, int H_kv, int T, int B, int row_k, int row_v,
+    int64_t n_slots, uint8_t* __restrict__ pool_k, uint8_t* __restrict__ pool_v) {
+  for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
+    const int32_t* list = xfer + size_t(unit) * (2 * K_b + 1);
+    const int cnt = list[0];
+    const int s = unit / H_kv;
+    int n = ctx_lens[s];
+    n = n < 0 ? 0 : (n > T ? T : n);
+    for (int k = 0; k < cnt; ++k) {
+      const int b = list[1 + 2 * k], sl = list[2 + 2 * k];
+      const int r0 = b * B, r1 = min(r0 + B, n);
+      if (r1 <= r0) continue;
+      const size_t rows = size_t(r1 - r0);
+      copy_block_rows(host_k + (size_t(unit) * T + r0) * row_k,
+                      pool_k + (size_t(unit) * n_slots + sl) * size_t(B) * row_k, rows * row_k);
+      if (host_v)
+        copy_block_rows(host_v + (size_t(unit) * T + r0) * row_v,
+                        pool_v + (size_t(unit) * n_slots + sl) * size_t(B) * row_v, rows * row_v);
+    }
   }
 }
 
@@ -144,10 +168,10 @@ hipError_t launch_prefetch(const Problem& P, const void* host_k, const void* hos
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int es = P.dtype == 1 ? 2 : 4;
-  dim3 grid(K_b, P.units);
-  prefetch_copy_kernel<0><<<grid, 256, 0, st>>>((const uint8_t*)host_k, (const uint8_t*)host_v, ctx_lens,
-                                                transfer_list, K_b, P.H_kv, P.T, P.B, P.d_qk * es, P.d_v * es,
-                                                n_slots, (uint8_t*)pool_k, (uint8_t*)pool_v);
+  const int wgs = P.units < kCopyWGs ? P.units : kCopyWGs;
+  prefetch_copy_kernel<<<wgs, kCopyThreads, 0, st>>>((const uint8_t*)host_k, (const uint8_t*)host_v, ctx_lens,
+                                                     transfer_list, P.units, K_b, P.H_kv, P.T, P.B, P.d_qk * es,
+                                                     P.d_v * es, n_slots, (uint8_t*)pool_k, (uint8_t*)pool_v);
   return hipGetLastError();
 }
 
