@@ -162,24 +162,30 @@ __global__ __launch_bounds__(256) void block_score_kernel(
   }
 }
 
-// One work-group per unit: stage the unit's scores as keys in LDS, select.
+// One work-group per unit: the unit's scores as keys in registers (thread t
+// holds blocks t + 1024 j, requested together), then the work-group top-k.
+template <int EPT>
 __global__ __launch_bounds__(1024) void block_topk_kernel(const float* __restrict__ scores,
                                                           const int32_t* __restrict__ ctx_lens, int H_kv,
                                                           int T, int B, int m_max, int K_b,
                                                           int32_t* __restrict__ block_ids) {
   extern __shared__ uint32_t smem[];
   uint32_t* scratch = smem;
-  uint32_t* keys = smem + topk_scratch_words(1024);
+  uint32_t* list = smem + topk_scratch_words(1024);
   const int unit = blockIdx.x;
   const int s = unit / H_kv;
   int n = ctx_lens[s];
   n = n < 0 ? 0 : (n > T ? T : n);
   const int m = (n + B - 1) / B;
   const float* sc = scores + size_t(unit) * m_max;
-  for (int i = threadIdx.x; i < m; i += 1024) keys[i] = float_key(sc[i]);
-  __syncthreads();
-  wg_topk_ascending<1024>(keys, m, K_b, block_ids + size_t(unit) * K_b, K_b, nullptr,
-                         [](int i) { return int32_t(i); }, scratch);
+  uint32_t kr[EPT];
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const int i = threadIdx.x + j * 1024;
+    kr[j] = i < m ? float_key(sc[i]) : kInvalidKey;
+  }
+  wg_topk_regs<1024, EPT>(kr, K_b, block_ids + size_t(unit) * K_b, K_b, nullptr, [](int i) { return int32_t(i); },
+                          scratch, list);
 }
 
 template <class E, int LPB, int CPL>
@@ -221,13 +227,22 @@ hipError_t launch_block_topk(const Problem& P, const float* scores, const int32_
                              int32_t* block_ids, uint32_t* err, hipStream_t st) {
   (void)err;
   const size_t lds = (topk_scratch_words(1024) + size_t(P.m_max)) * sizeof(uint32_t);
-  if (lds > 65536) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(block_topk_kernel),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-    if (e != hipSuccess) return e;
-  }
-  block_topk_kernel<<<P.units, 1024, lds, st>>>(scores, ctx_lens, P.H_kv, P.T, P.B, P.m_max, K_b, block_ids);
-  return hipGetLastError();
+  const int ept = (P.m_max + 1023) / 1024;
+  auto go = [&](auto kern) {
+    if (lds > 65536) {
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+      if (e != hipSuccess) return e;
+    }
+    kern<<<P.units, 1024, lds, st>>>(scores, ctx_lens, P.H_kv, P.T, P.B, P.m_max, K_b, block_ids);
+    return hipGetLastError();
+  };
+  if (ept <= 1) return go(block_topk_kernel<1>);
+  if (ept <= 2) return go(block_topk_kernel<2>);
+  if (ept <= 4) return go(block_topk_kernel<4>);
+  if (ept <= 8) return go(block_topk_kernel<8>);
+  if (ept <= 12) return go(block_topk_kernel<12>);
+  return go(block_topk_kernel<16>);
 }
 
 }  // namespace tls

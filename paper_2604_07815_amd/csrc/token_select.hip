@@ -359,11 +359,13 @@ __global__ __launch_bounds__(256) void token_alpha_kernel_g(
     const int h = tid / TPH, j = tid % TPH;
     const float* st = stats + size_t(unit) * n_tchunks * G * 2;
     float M = -INFINITY;
+#pragma unroll 8
     for (int c = j; c < n_tchunks; c += TPH) M = fmaxf(M, st[(c * G + h) * 2]);
 #pragma unroll
     for (int o = TPH / 2; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
     float Z = 0.f;
     if (M != -INFINITY)
+#pragma unroll 8
       for (int c = j; c < n_tchunks; c += TPH) {
         const float mc = st[(c * G + h) * 2], zc = st[(c * G + h) * 2 + 1];
         if (mc != -INFINITY) Z += zc * __expf(mc - M);
@@ -395,6 +397,10 @@ __global__ __launch_bounds__(256) void token_alpha_kernel_g(
   }
 }
 
+// Top-K_t of the alpha keys of each unit, one work-group per unit.  Thread t
+// holds the keys of slots t + 1024 j (j < EPT), requested together straight
+// into registers; the list of keys in play lives in LDS.
+template <int EPT>
 __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __restrict__ keys,
                                                            const int32_t* __restrict__ block_ids, int K_b,
                                                            int B, int K_t, int32_t* __restrict__ token_ids,
@@ -403,14 +409,19 @@ __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __rest
   uint32_t* scratch = smem;
   int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(1024));
   const int S = K_b * B;
-  uint32_t* s_keys = smem + topk_scratch_words(1024) + align4w(K_b);
+  uint32_t* list = smem + topk_scratch_words(1024) + align4w(K_b);
   const int unit = blockIdx.x;
+  uint32_t kr[EPT];
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const int p = threadIdx.x + j * 1024;
+    kr[j] = p < S ? keys[size_t(unit) * S + p] : kInvalidKey;
+  }
   for (int i = threadIdx.x; i < K_b; i += 1024) s_bl[i] = block_ids[size_t(unit) * K_b + i];
-  for (int i = threadIdx.x; i < S; i += 1024) s_keys[i] = keys[size_t(unit) * S + i];
   __syncthreads();
-  wg_topk_ascending<1024>(s_keys, S, K_t, token_ids + size_t(unit) * K_t, K_t,
+  wg_topk_regs<1024, EPT>(kr, K_t, token_ids + size_t(unit) * K_t, K_t,
                           token_scores ? token_scores + size_t(unit) * K_t : nullptr,
-                          [=](int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch);
+                          [=](int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch, list);
 }
 
 template <int HT, int NGR>
@@ -464,15 +475,24 @@ hipError_t launch_token_alpha(const Problem& P, const float* logits, const float
 
 hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32_t* block_ids, int K_b,
                              int K_t, int32_t* token_ids, float* token_scores, hipStream_t st) {
-  const size_t lds =
-      (topk_scratch_words(1024) + size_t(align4w(K_b)) + size_t(K_b) * P.B) * sizeof(uint32_t);
-  if (lds > 65536) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(token_topk_kernel),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-    if (e != hipSuccess) return e;
-  }
-  token_topk_kernel<<<P.units, 1024, lds, st>>>(keys, block_ids, K_b, P.B, K_t, token_ids, token_scores);
-  return hipGetLastError();
+  const int S = K_b * P.B;
+  const size_t lds = (topk_scratch_words(1024) + size_t(align4w(K_b)) + size_t(S)) * sizeof(uint32_t);
+  const int ept = (S + 1023) / 1024;
+  auto go = [&](auto kern) {
+    if (lds > 65536) {
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+      if (e != hipSuccess) return e;
+    }
+    kern<<<P.units, 1024, lds, st>>>(keys, block_ids, K_b, P.B, K_t, token_ids, token_scores);
+    return hipGetLastError();
+  };
+  if (ept <= 1) return go(token_topk_kernel<1>);
+  if (ept <= 2) return go(token_topk_kernel<2>);
+  if (ept <= 4) return go(token_topk_kernel<4>);
+  if (ept <= 8) return go(token_topk_kernel<8>);
+  if (ept <= 12) return go(token_topk_kernel<12>);
+  return go(token_topk_kernel<16>);
 }
 
 }  // namespace tls
