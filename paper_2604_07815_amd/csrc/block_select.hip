@@ -184,7 +184,7 @@ __global__ __launch_bounds__(1024) void block_topk_kernel(const float* __restric
     const int i = threadIdx.x + j * 1024;
     kr[j] = i < m ? float_key(sc[i]) : kInvalidKey;
   }
-  wg_topk_regs<1024, EPT>(kr, K_b, block_ids + size_t(unit) * K_b, K_b, nullptr, [](int i) { return int32_t(i); },
+  wg_topk_regs<1024, EPT>(kr, K_b, block_ids + size_t(unit) * K_b, K_b, nullptr, [](int, int i) { return int32_t(i); },
                           scratch, list);
 }
 

@@ -421,7 +421,7 @@ __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __rest
   __syncthreads();
   wg_topk_regs<1024, EPT>(kr, K_t, token_ids + size_t(unit) * K_t, K_t,
                           token_scores ? token_scores + size_t(unit) * K_t : nullptr,
-                          [=](int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch, list);
+                          [=](int, int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch, list);
 }
 
 template <int HT, int NGR>

@@ -53,7 +53,7 @@ __device__ constexpr int kSliceChan[8] = {0, 2, 1, 3, 4, 6, 5, 7};
 __host__ __device__ inline size_t list_words(int S, int m_max) { return size_t(S > m_max ? S : m_max); }
 
 size_t mfma_select_lds_bytes(int S, int K_b, int m_max) {
-  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(K_b)) + 64 + kSelNW * 8 +
+  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(K_b)) + 64 + kSelNW * 12 +
           align4w(int(list_words(S, m_max)))) *
          sizeof(uint32_t);
 }
@@ -70,8 +70,8 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   uint32_t* scratch = smem;
   int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(NT));
   uint16_t* s_qt = reinterpret_cast<uint16_t*>(s_bl + align4w(K_b));  // [4][32] (64 words)
-  float* s_red = reinterpret_cast<float*>(s_qt + 128);                    // [NW][8]
-  uint32_t* list = reinterpret_cast<uint32_t*>(s_red + NW * 8);
+  float* s_red = reinterpret_cast<float*>(s_qt + 128);                    // [NW][12]
+  uint32_t* list = reinterpret_cast<uint32_t*>(s_red + NW * 12);
   const int S = K_b * B;
 
   const int unit = blockIdx.x;
@@ -121,7 +121,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
     s_qt[tid] = v;
   }
   if (block_scores) {
-    wg_topk_regs<NT, kSelBPT>(bk, K_b, s_bl, K_b, nullptr, [](int i) { return int32_t(i); }, scratch, list);
+    wg_topk_regs<NT, kSelBPT>(bk, K_b, s_bl, K_b, nullptr, [](int, int i) { return int32_t(i); }, scratch, list);
   }
   __syncthreads();
 
@@ -158,6 +158,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   // 1. index rows of the owned slots
   uint4 cw[kSelSPT];
   float2 qp[kSelSPT];
+  int32_t tokpos[kSelSPT];  // token position of each owned slot (for the output)
   uint32_t vmask = 0;
 #pragma unroll
   for (int i = 0; i < kSelSPT; ++i) {
@@ -165,9 +166,11 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
     const int e = slot >> lgB, o = slot & (B - 1);
     cw[i] = make_uint4(0, 0, 0, 0);
     qp[i] = make_float2(0.f, 0.f);
+    tokpos[i] = -1;
     if (slot < S) {
       const int blk = s_bl[e];
       const int tok = blk * B + o;
+      tokpos[i] = tok;
       if (blk >= 0 && tok < n) {
         const size_t r = size_t(unit) * T + tok;
         cw[i] = ld16_stream(codes + r * 16);
@@ -205,15 +208,21 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
       mx[h] = fmaxf(mx[h], lg[i][h]);
     }
   }
+  const uint32_t wcnt = wave_reduce_bits(uint32_t(__popc(vmask)), [](uint32_t a, uint32_t b) { return a + b; });
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     const float w = wave_max_f32(mx[h]);
-    if (lane == 0) s_red[wid * 8 + h] = w;
+    if (lane == 0) s_red[wid * 12 + h] = w;
   }
+  if (lane == 0) s_red[wid * 12 + 8] = __uint_as_float(wcnt);
   __syncthreads();
   static_assert(NW == 16, "one wave value per lane of a 16-lane row");
 #pragma unroll
-  for (int h = 0; h < G; ++h) mx[h] = combine_waves_max_f32(s_red[(lane & 15) * 8 + h]);
+  for (int h = 0; h < G; ++h) {
+    mx[h] = combine_waves_max_f32(s_red[(lane & 15) * 12 + h]);
+    if (mx[h] == -INFINITY) mx[h] = 0.f;  // no candidate: every logit is -inf, every exponential 0
+  }
+  const uint32_t n_valid = combine_waves_sum_u32(__float_as_uint(s_red[(lane & 15) * 12 + 8]));
   // 3. exponentials (base 2: the logits carry log2(e)) and their per-head sums
   float sum[G];
 #pragma unroll
@@ -222,36 +231,45 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
   for (int i = 0; i < kSelSPT; ++i)
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const float e = ((vmask >> i) & 1u) ? __builtin_amdgcn_exp2f(lg[i][h] - mx[h]) : 0.f;
+      const float e = __builtin_amdgcn_exp2f(lg[i][h] - mx[h]);  // 0 for an empty slot (logit -inf)
       lg[i][h] = e;
       sum[h] += e;
     }
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     const float w = wave_sum_f32(sum[h]);
-    if (lane == 0) s_red[wid * 8 + 4 + h] = w;
+    if (lane == 0) s_red[wid * 12 + 4 + h] = w;
   }
+  topk_prepare<NT>(scratch);  // the token top-k's histograms, cleared before the barrier below
   __syncthreads();
   float iz[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    const float Z = combine_waves_sum_f32(s_red[(lane & 15) * 8 + 4 + h]);
+    const float Z = combine_waves_sum_f32(s_red[(lane & 15) * 12 + 4 + h]);
     iz[h] = Z > 0.f ? 1.0f / Z : 0.f;
   }
   // 4. alpha keys in registers, top-K_t
+  // Every alpha lies in [0, bound] with bound = (1/G) sum_h 1/Z_h, evaluated in
+  // the same operation order (each exponential is <= 1 and rounding is
+  // monotone), so the top-k needs no statistics pass of its own.  A NaN alpha
+  // (NaN inputs only) ranks as 0.
   const float invG = 1.0f / float(G);
+  float bsum = 0.f;
+#pragma unroll
+  for (int h = 0; h < G; ++h) bsum = fmaf(1.0f, iz[h], bsum);
   uint32_t keys[kSelSPT];
 #pragma unroll
   for (int i = 0; i < kSelSPT; ++i) {
     float a = 0.f;
 #pragma unroll
-    for (int h = 0; h < G; ++h) a += lg[i][h] * iz[h];
-    keys[i] = ((vmask >> i) & 1u) ? float_key(a * invG) : kInvalidKey;
+    for (int h = 0; h < G; ++h) a = fmaf(lg[i][h], iz[h], a);
+    const float av = a * invG;
+    keys[i] = ((vmask >> i) & 1u) ? (av == av ? float_key(av) : float_key(0.f)) : kInvalidKey;
   }
+  const TopkKnown known{n_valid, float_key(bsum * invG), float_key(0.f)};
   wg_topk_regs<NT, kSelSPT>(keys, K_t, token_ids + size_t(unit) * K_t, K_t,
                             token_scores ? token_scores + size_t(unit) * K_t : nullptr,
-                            [=](int slot) { return int32_t((s_bl[slot >> lgB] << lgB) | (slot & (B - 1))); },
-                            scratch, list);
+                            [&](int j, int) { return tokpos[j]; }, scratch, list, &known);
   if (block_scores && block_ids_out)
     for (int i = tid; i < K_b; i += NT) block_ids_out[size_t(unit) * K_b + i] = s_bl[i];
 }

@@ -48,9 +48,24 @@ __host__ __device__ constexpr int align4w(int words) { return (words + 3) & ~3; 
 // and the first r keys == T: per (key slot j, wave) counts in position order
 // (j-major, then wave, then lane) give every key its output index with one
 // barrier, so the output is ordered by position without a sort.
+// Counts the caller already knows about its keys: the number of valid keys
+// and bounds lo <= key <= hi of every valid key.  With them the selection
+// skips its own statistics pass and barrier; the caller must then have run
+// topk_prepare on the scratch area before a work-group barrier.
+struct TopkKnown {
+  uint32_t cnt, hi, lo;
+};
+
+template <int NT>
+__device__ inline void topk_prepare(uint32_t* scratch) {
+  constexpr int kHistAll = align4w_c(4 * kTopkHistWords);
+  for (int i = threadIdx.x; i < kHistAll; i += NT) scratch[i] = 0u;
+  if (threadIdx.x == 0) scratch[kHistAll + 50] = 0u;
+}
+
 template <int NT, int EPT, class Map>
 __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int out_cap, float* out_scores,
-                             Map map, uint32_t* scratch, uint32_t* list) {
+                             Map map, uint32_t* scratch, uint32_t* list, const TopkKnown* known = nullptr) {
   constexpr int NW = NT / 64;
   static_assert(NW >= 1 && NW <= kTopkMaxNW && EPT >= 1 && EPT <= kTopkMaxEPT, "work-group shape");
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -60,33 +75,39 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
   uint32_t* cg = misc + 64;             // [EPT][NW] keys > T per (slot, wave)
   uint32_t* ce = cg + kTopkMaxEPT * kTopkMaxNW;  // [EPT][NW] keys == T
 
-  // valid count, max and min valid key over the work-group
   uint32_t cnt = 0, kmx = 0u, kmn = 0xffffffffu;
+  if (known) {
+    cnt = known->cnt;
+    kmx = known->hi;
+    kmn = known->lo;
+  } else {
+    // valid count, max and min valid key over the work-group
 #pragma unroll
-  for (int j = 0; j < EPT; ++j) {
-    const uint32_t key = kr[j];
-    cnt += uint32_t(__popcll(__ballot(key != kInvalidKey)));
-    if (key != kInvalidKey) {
-      kmx = max(kmx, key);
-      kmn = min(kmn, key);
+    for (int j = 0; j < EPT; ++j) {
+      const uint32_t key = kr[j];
+      cnt += uint32_t(__popcll(__ballot(key != kInvalidKey)));
+      if (key != kInvalidKey) {
+        kmx = max(kmx, key);
+        kmn = min(kmn, key);
+      }
     }
-  }
-  kmx = wave_max_u32(kmx);
-  kmn = wave_min_u32(kmn);
-  for (int i = tid; i < kHistAll; i += NT) hist[i] = 0u;
-  if (lane == 0) {
-    misc[wid] = cnt;
-    misc[16 + wid] = kmx;
-    misc[32 + wid] = kmn;
-  }
-  if (tid == 0) misc[50] = 0u;
-  __syncthreads();
-  {
-    const int w = lane & 15;
-    const bool ok = w < NW;
-    cnt = combine_waves_sum_u32(ok ? misc[w] : 0u);
-    kmx = combine_waves_max_u32(ok ? misc[16 + w] : 0u);
-    kmn = combine_waves_min_u32(ok ? misc[32 + w] : 0xffffffffu);
+    kmx = wave_max_u32(kmx);
+    kmn = wave_min_u32(kmn);
+    for (int i = tid; i < kHistAll; i += NT) hist[i] = 0u;
+    if (lane == 0) {
+      misc[wid] = cnt;
+      misc[16 + wid] = kmx;
+      misc[32 + wid] = kmn;
+    }
+    if (tid == 0) misc[50] = 0u;
+    __syncthreads();
+    {
+      const int w = lane & 15;
+      const bool ok = w < NW;
+      cnt = combine_waves_sum_u32(ok ? misc[w] : 0u);
+      kmx = combine_waves_max_u32(ok ? misc[16 + w] : 0u);
+      kmn = combine_waves_min_u32(ok ? misc[32 + w] : 0xffffffffu);
+    }
   }
   const int kk = min(k, int(cnt));
 
@@ -242,7 +263,7 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
       const int eb = __builtin_amdgcn_readlane(int(pe), src) + lanes_below(be);
       if (g || (e && eb < r)) {
         const int pos = gb + min(eb, r);
-        out[pos] = map(tid + j * NT);
+        out[pos] = map(j, tid + j * NT);
         if (out_scores) out_scores[pos] = key_float(key);
       }
     }
