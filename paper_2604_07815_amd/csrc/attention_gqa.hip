@@ -626,11 +626,13 @@ int gqa_auto_splits(const Problem& P, int K_t) {
   // whole units (one 12-wave work-group each, no partials, no merge) when
   // they fill the compute units in whole rounds
   if (gqa_whole_ok(P, K_t) && P.units % cus == 0) return 1;
-  // fewer units than compute units: as many 12-wave splits as fit in one round
+  // fewer units than compute units: as many 12-wave splits as fit in one
+  // round, when they still occupy at least half of the compute units (with
+  // fewer, many short 4-wave splits spread the gathers over more of the chip)
   if (P.units * 2 <= cus) {
     const int ns = cus / P.units;
     for (int w = ns; w >= 2; --w)
-      if (gqa_use_wide(P, K_t, w, cus)) return w;
+      if (gqa_use_wide(P, K_t, w, cus) && long(P.units) * w * 2 >= cus) return w;
   }
   const int occ = P.d_qk == 64 ? mfma_wgs_per_cu_g<64>(P.G) : mfma_wgs_per_cu_g<128>(P.G);
   const long slots = long(cus) * occ;
