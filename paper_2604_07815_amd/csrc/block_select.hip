@@ -241,7 +241,6 @@ hipError_t launch_block_topk(const Problem& P, const float* scores, const int32_
   if (ept <= 2) return go(block_topk_kernel<2>);
   if (ept <= 4) return go(block_topk_kernel<4>);
   if (ept <= 8) return go(block_topk_kernel<8>);
-  if (ept <= 12) return go(block_topk_kernel<12>);
   return go(block_topk_kernel<16>);
 }
 

@@ -491,7 +491,6 @@ hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32
   if (ept <= 2) return go(token_topk_kernel<2>);
   if (ept <= 4) return go(token_topk_kernel<4>);
   if (ept <= 8) return go(token_topk_kernel<8>);
-  if (ept <= 12) return go(token_topk_kernel<12>);
   return go(token_topk_kernel<16>);
 }
 

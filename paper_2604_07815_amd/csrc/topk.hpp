@@ -68,6 +68,10 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
                              Map map, uint32_t* scratch, uint32_t* list, const TopkKnown* known = nullptr) {
   constexpr int NW = NT / 64;
   static_assert(NW >= 1 && NW <= kTopkMaxNW && EPT >= 1 && EPT <= kTopkMaxEPT, "work-group shape");
+  // the ordered compaction gives lane L the (slot, wave) entries L*PER ..
+  // L*PER + PER - 1 and finds wave w's entry of every slot at index w % PER,
+  // which needs NW to be a multiple of PER
+  static_assert(NW % ((EPT * NW + 63) / 64) == 0, "keys per thread must keep NW a multiple of PER");
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   constexpr int kHistAll = align4w_c(4 * kTopkHistWords);
   uint32_t* hist = scratch;             // [4 passes][copies][stride]

@@ -107,3 +107,21 @@ def test_wide_split_attention(splits):
         ref = c.oracle_unit(s, g, token_ids=r["tids"][s, g].cpu().numpy()[r["tids"][s, g].cpu().numpy() >= 0])
         H.check_close(r["out"][s, g * G:(g + 1) * G].float().cpu().numpy(), ref["out"], cfg.dtype, f"out {(s, g)}")
         H.check_close(r["lse"][s, g * G:(g + 1) * G].cpu().numpy(), ref["lse"], cfg.dtype, f"lse {(s, g)}")
+
+
+@pytest.mark.parametrize("k_b,k_t", [(128, 2048), (192, 4096)])
+def test_capacity_limits(k_b, k_t):
+    """The largest shapes this build accepts: 131072 tokens (2048 blocks, the
+    fused selection's block capacity) with 8192 candidates, and 12288
+    candidates (K_b = 192, the general selection path's key capacity) with
+    K_t = 4096; sampled units against the oracle."""
+    import paper_2604_07815_amd as tls
+    cfg = synth.config("qwen3_gqa_48k").replace(ctx_lo=131072, ctx_hi=131072, k_b=k_b, k_t=k_t, seed=97)
+    c = H.Case(cfg, backend="device", pad="nan").build_index()
+    r = c.decode()
+    for (s, g) in c.units(3):
+        H.compare_unit(c, r, s, g)
+    assert tls.tls_check_device_error(r["ws"]) == 0
+    with pytest.raises(tls.TlsError) as e:
+        tls.tls_workspace_size(c.layout, k_b + 1 if k_b == 192 else 193, k_t)
+    assert e.value.status == 2
