@@ -451,8 +451,9 @@ def main():
         def time_mode(mode, k_b, steps):
             def f(i):
                 L = layers[i % len(layers)]
-                tls.tls_sparse_decode(layout, L["q"], tls.KV(L["k"], L["v"]), ctx_t, L["kmax"], L["kmin"], None, None,
-                                      None, k_b, cfg.k_t, None, None, attn_out, None, None, None, ws, mode=mode)
+                tls.tls_sparse_decode(layout, L["q"], tls.KV(L["k"], L["v"]), ctx_t, L["kmax"], L["kmin"], L["codes"],
+                                      L["qparams"], ch_t, k_b, cfg.k_t, None, None, attn_out, None, None, None, ws,
+                                      mode=mode)
             for i in range(2):
                 f(i)
             torch.cuda.synchronize()
@@ -467,11 +468,14 @@ def main():
         modes["block_sparse_same_blocks_us"] = round(time_mode(tls.MODE_BLOCK_SPARSE, cfg.k_b, ms), 2)
         kb_eq = max(1, cfg.k_t // cfg.block)
         modes["block_sparse_same_tokens_us"] = round(time_mode(tls.MODE_BLOCK_SPARSE, kb_eq, ms), 2)
+        modes["token_sparse_us"] = round(time_mode(tls.MODE_TOKEN_SPARSE, cfg.k_b, ms), 2)
         modes["dense_us"] = round(time_mode(tls.MODE_DENSE, cfg.k_b, ms), 2)
         modes["speedup_vs_dense"] = round(modes["dense_us"] / modes["two_level_us"], 2)
+        modes["speedup_vs_token_sparse"] = round(modes["token_sparse_us"] / modes["two_level_us"], 2)
         modes["note"] = (f"same inputs; block-sparse attends every token of the top-{cfg.k_b} blocks "
                          f"({cfg.k_b * cfg.block} tokens) or of the top-{kb_eq} blocks ({kb_eq * cfg.block} tokens, "
-                         f"the two-level token budget); dense attends all ctx_len tokens")
+                         f"the two-level token budget); token-sparse selects the top-{cfg.k_t} tokens of the "
+                         f"whole context by the same approximate score; dense attends all ctx_len tokens")
 
     err = tls.tls_check_device_error(ws)
     nb = algorithmic_bytes(cfg, d["ctx_host"], bids.cpu().numpy(), e)

@@ -115,10 +115,10 @@ typedef struct tls_kv_view {
   int64_t n_slots;         /* slots per unit (pooled view only) */
 } tls_kv_view;
 
-/* Operator run by tls_sparse_decode (tls_decode_opts.mode).  The two
+/* Operator run by tls_sparse_decode (tls_decode_opts.mode).  The
  * single-level operators are the baselines the paper measures its operator
- * against (Sec. 5, kernel study): block-level selection alone (Quest) and
- * full attention.
+ * against (Sec. 5, kernel study): block-level selection alone (Quest),
+ * token-level selection alone (Double Sparsity) and full attention.
  *   TLS_MODE_TWO_LEVEL    Sec. 4.1: block selection, token selection, then
  *                         attention over the K_t selected tokens.
  *   TLS_MODE_BLOCK_SPARSE block selection only, then attention over every
@@ -130,8 +130,15 @@ typedef struct tls_kv_view {
  *   TLS_MODE_DENSE        no selection: attention over all ctx_len tokens
  *                         of each sequence (full attention).  K_b, K_t and
  *                         the index arrays are not used; every id argument
- *                         must be NULL. */
-enum { TLS_MODE_TWO_LEVEL = 0, TLS_MODE_BLOCK_SPARSE = 1, TLS_MODE_DENSE = 2 };
+ *                         must be NULL.
+ *   TLS_MODE_TOKEN_SPARSE token selection alone: the approximate score of
+ *                         Sec. 4.1 over every valid token of the unit (the
+ *                         per-head softmax runs over all of them), the K_t
+ *                         largest, then attention over those tokens.  kmax
+ *                         and kmin are not used; the block-id arguments and
+ *                         token_ids_in must be NULL; token_ids_out receives
+ *                         the selection.  G must be 1, 2, 4, 8, 16 or 32. */
+enum { TLS_MODE_TWO_LEVEL = 0, TLS_MODE_BLOCK_SPARSE = 1, TLS_MODE_DENSE = 2, TLS_MODE_TOKEN_SPARSE = 3 };
 
 /* Optional knobs of tls_sparse_decode; pass NULL for defaults. */
 typedef struct tls_decode_opts {

@@ -290,6 +290,18 @@ def block_sparse_unit(q_group, K, V, n, k_b, B, sigma, summaries=None, block_ids
     return res
 
 
+def token_sparse_unit(q_group, K, V, n, channels, k_t, B, sigma, index=None):
+    """Token-level selection alone (the Double Sparsity baseline): the
+    approximate score of Sec. 4.1 over every valid token (the candidate set is
+    every block), the top-k_t, then attention over them."""
+    if index is None:
+        index = token_index(K, n, channels)
+    every_block = np.arange(num_blocks(n, B))
+    ids, alpha, cand = select_tokens(q_group, channels, index[0], index[1], every_block, n, B, k_t, sigma)
+    o, lse = sparse_attention(q_group, K, V, ids, sigma)
+    return dict(token_ids=np.asarray(ids), alpha=alpha, cand=cand, out=o, lse=lse)
+
+
 def dense_unit(q_group, K, V, n, sigma):
     """Full attention over the n cached tokens."""
     o, lse = sparse_attention(q_group, K, V, np.arange(int(n)), sigma)

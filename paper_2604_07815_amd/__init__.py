@@ -22,14 +22,14 @@ __all__ = [
     "tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
     "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error",
     "make_layout", "alloc_workspace", "DTYPE_F32", "DTYPE_BF16", "EXPORTED_SYMBOLS",
-    "MODE_TWO_LEVEL", "MODE_BLOCK_SPARSE", "MODE_DENSE",
+    "MODE_TWO_LEVEL", "MODE_BLOCK_SPARSE", "MODE_DENSE", "MODE_TOKEN_SPARSE",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtls.so")
 
 OK, INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP_ERROR = 0, 1, 2, 3, 4
 DTYPE_F32, DTYPE_BF16 = 0, 1
-MODE_TWO_LEVEL, MODE_BLOCK_SPARSE, MODE_DENSE = 0, 1, 2
+MODE_TWO_LEVEL, MODE_BLOCK_SPARSE, MODE_DENSE, MODE_TOKEN_SPARSE = 0, 1, 2, 3
 NUM_STAGE_EVENTS = 8
 DEVERR_CTX_LEN, DEVERR_BLOCK_ID, DEVERR_TOKEN_ID, DEVERR_SLOT, DEVERR_POOL_FULL, DEVERR_CHANNEL = 1, 2, 4, 8, 16, 32
 

@@ -26,7 +26,7 @@ constexpr int kTokenSlotsPerWG = 256;
 
 // Workspace carving (byte offsets from the workspace base, 256-aligned).
 struct Workspace {
-  size_t err, xfer, qpn, bscores, bids, logits, stats, keys, tids, po, plse, total;
+  size_t err, xfer, qpn, bscores, bids, logits, stats, keys, tids, po, plse, dkeys, dstats, total;
   int n_tchunks;  // token-score work-groups per unit
 };
 Workspace plan_workspace(const Problem& P, int K_b, int K_t);
@@ -60,6 +60,14 @@ hipError_t launch_token_select_fused(const Problem& P, const void* q, const uint
                                      const int32_t* block_ids_in, int32_t* block_ids_out, const int32_t* ctx_lens,
                                      int K_b, int K_t, int32_t* token_ids, float* token_scores, uint32_t* err,
                                      hipStream_t st);
+
+// Token-level selection over every valid token of each unit (the token-only
+// operator): alpha keys [units][T] and per-chunk statistics in the workspace.
+bool ds_supported(const Problem& P);
+size_t ds_stats_floats(const Problem& P);
+hipError_t launch_token_select_dense(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,
+                                     const int32_t* channels, const int32_t* ctx_lens, int K_t, float* stats,
+                                     uint32_t* keys, int32_t* token_ids, uint32_t* err, hipStream_t st);
 
 struct KvView {
   const void* k;

@@ -100,6 +100,8 @@ Workspace plan_workspace(const Problem& P, int K_b, int K_t) {
   w.tids = off;     off = align_up(off + U * size_t(K_t) * sizeof(int32_t));
   w.po = off;       off = align_up(off + U * kMaxSplits * P.G * size_t(P.d_v) * sizeof(float));
   w.plse = off;     off = align_up(off + U * kMaxSplits * P.G * sizeof(float));
+  w.dkeys = off;    off = align_up(off + U * size_t(P.T) * sizeof(uint32_t));  // token-only operator
+  w.dstats = off;   off = align_up(off + ds_stats_floats(P) * sizeof(float));
   w.total = off;
   return w;
 }
@@ -236,14 +238,53 @@ static tls_status finish_decode(const Problem& P, const tls::Workspace& W, const
   return hip_status(e);
 }
 
+// Token-level selection alone (TLS_MODE_TOKEN_SPARSE): alpha over every valid
+// token of each unit, its top-K_t, then attention over those tokens.
+static tls_status token_level_decode(const Problem& P, const void* q, const tls_kv_view* kv,
+                                     const int32_t* ctx_lens, const uint8_t* codes, const float* qparams,
+                                     const int32_t* channels, int K_b, int K_t, const int32_t* block_ids_in,
+                                     const int32_t* token_ids_in, void* out, float* lse, int32_t* block_ids_out,
+                                     int32_t* token_ids_out, void* ws, size_t ws_bytes, int requested,
+                                     hipEvent_t* ev, hipStream_t stream) {
+  if (block_ids_in || token_ids_in || block_ids_out) return TLS_ERR_INVALID_ARGUMENT;
+  if (!codes || !qparams || !channels) return TLS_ERR_INVALID_ARGUMENT;
+  if (K_t < 1) return TLS_ERR_INVALID_ARGUMENT;
+  if (!tls::ds_supported(P)) return TLS_ERR_UNSUPPORTED;
+  tls_status st = check_attention(P, K_t);
+  if (st != TLS_OK) return st;
+  const tls::Workspace W = tls::plan_workspace(P, K_b > 0 ? K_b : 1, K_t);
+  if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  auto mark = [&](int i) {
+    if (ev) hipEventRecord(ev[i], stream);
+  };
+  mark(0);
+  mark(1);
+  mark(2);
+  int32_t* to = token_ids_out ? token_ids_out : at<int32_t>(ws, W.tids);
+  const hipError_t e = tls::launch_token_select_dense(P, q, codes, qparams, channels, ctx_lens, K_t,
+                                                      at<float>(ws, W.dstats), at<uint32_t>(ws, W.dkeys), to,
+                                                      err_word(ws), stream);
+  mark(3);
+  mark(4);
+  mark(5);
+  if (e != hipSuccess) return TLS_ERR_HIP;
+  return finish_decode(P, W, q, kv, ctx_lens, K_t, tls::TokenList{to, K_t, tls::kListIds, P.B}, out, lse, ws,
+                       requested, ev, stream);
+}
+
 // The single-level baselines (TLS_MODE_BLOCK_SPARSE, TLS_MODE_DENSE): block
 // selection (unless given) and attention over every valid token of the
 // selected blocks, or attention over the whole context.
 static tls_status single_level_decode(const Problem& P, int mode, const void* q, const tls_kv_view* kv,
-                                      const int32_t* ctx_lens, const void* kmax, const void* kmin, int K_b, int K_t,
+                                      const int32_t* ctx_lens, const void* kmax, const void* kmin,
+                                      const uint8_t* codes, const float* qparams, const int32_t* channels, int K_b,
+                                      int K_t,
                                       const int32_t* block_ids_in, const int32_t* token_ids_in, void* out,
                                       float* lse, int32_t* block_ids_out, int32_t* token_ids_out, void* ws,
                                       size_t ws_bytes, int requested, hipEvent_t* ev, hipStream_t stream) {
+  if (mode == TLS_MODE_TOKEN_SPARSE)
+    return token_level_decode(P, q, kv, ctx_lens, codes, qparams, channels, K_b, K_t, block_ids_in, token_ids_in,
+                              out, lse, block_ids_out, token_ids_out, ws, ws_bytes, requested, ev, stream);
   if (token_ids_in || token_ids_out) return TLS_ERR_INVALID_ARGUMENT;
   const bool dense = mode == TLS_MODE_DENSE;
   if (dense && (block_ids_in || block_ids_out)) return TLS_ERR_INVALID_ARGUMENT;
@@ -297,7 +338,7 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
     for (int i = 0; i < 6; ++i)
       if (opts->reserved[i] != 0) return TLS_ERR_INVALID_ARGUMENT;
     if (opts->attn_splits < 0 || opts->attn_splits > tls::kMaxSplits) return TLS_ERR_INVALID_ARGUMENT;
-    if (opts->mode < TLS_MODE_TWO_LEVEL || opts->mode > TLS_MODE_DENSE) return TLS_ERR_INVALID_ARGUMENT;
+    if (opts->mode < TLS_MODE_TWO_LEVEL || opts->mode > TLS_MODE_TOKEN_SPARSE) return TLS_ERR_INVALID_ARGUMENT;
     requested = opts->attn_splits;
     mode = opts->mode;
     ev = opts->stage_events;
@@ -306,7 +347,8 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
         if (!ev[i]) return TLS_ERR_INVALID_ARGUMENT;
   }
   if (mode != TLS_MODE_TWO_LEVEL)
-    return single_level_decode(P, mode, q, kv, ctx_lens, kmax, kmin, K_b, K_t, block_ids_in, token_ids_in, out,
+    return single_level_decode(P, mode, q, kv, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t,
+                               block_ids_in, token_ids_in, out,
                                lse, block_ids_out, token_ids_out, ws, ws_bytes, requested, ev, stream);
   const bool sel_tokens = token_ids_in == nullptr;
   const bool sel_blocks = sel_tokens && block_ids_in == nullptr;

@@ -48,6 +48,120 @@ __host__ __device__ constexpr int align4w(int words) { return (words + 3) & ~3; 
 // and the first r keys == T: per (key slot j, wave) counts in position order
 // (j-major, then wave, then lane) give every key its output index with one
 // barrier, so the output is ordered by position without a sort.
+// Run by one whole wave after a pass's histogram is complete: finds the
+// digit holding the remaining-th largest key in play (digits scanned from
+// the top; lane L owns digits 255-4L .. 252-4L, summed over the histogram
+// copies) and publishes misc[48] = digit, misc[49] = keys in higher digits,
+// misc[51] = 1 when the digit's keys are all taken, misc[52] = its key count.
+__device__ inline void topk_scan_pass(const uint32_t* h, int remaining, uint32_t* misc) {
+  const int lane = __lane_id();
+  uint32_t c[4];
+  uint32_t local = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    c[j] = 0;
+#pragma unroll
+    for (int cp = 0; cp < kTopkHistCopies; ++cp) c[j] += h[cp * kTopkHistStride + 255 - 4 * lane - j];
+    local += c[j];
+  }
+  const uint32_t incl = wave_incl_scan_u32(local);
+  uint32_t run = incl - local;
+  int found = -1;
+  uint32_t found_above = 0, found_cnt = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (found < 0 && run + c[j] >= uint32_t(remaining)) {
+      found = 255 - 4 * lane - j;
+      found_above = run;
+      found_cnt = c[j];
+    }
+    run += c[j];
+  }
+  const uint64_t hit = __ballot(found >= 0);
+  const int src = __ffsll((unsigned long long)hit) - 1;
+  if (lane == src) {
+    misc[48] = uint32_t(found);
+    misc[49] = found_above;
+    misc[51] = found_cnt == uint32_t(remaining) - found_above ? 1u : 0u;
+    misc[52] = found_cnt;
+  }
+}
+
+// Ordered compaction of one tile of keys held in registers (slot j of thread
+// t at tile position t + j*NT, position order = j-major, then wave, then
+// lane): writes every key > T and, in position order, the keys == T while
+// fewer than r ties have been taken, at out[#earlier keys > T + min(#earlier
+// ties, r)] (map(j, tile position) gives the value written).  gbase / ebase
+// count the keys > T and == T of earlier tiles (uniform) and are advanced by
+// this tile's counts.  One work-group barrier inside; cg / ce (LDS) must not
+// be rewritten before every thread has returned.
+template <int NT, int EPT, class Map>
+__device__ void topk_compact_tile(const uint32_t (&kr)[EPT], uint32_t T, int r, int& gbase, int& ebase, int32_t* out,
+                                  float* out_scores, Map map, uint32_t* cg, uint32_t* ce) {
+  constexpr int NW = NT / 64;
+  static_assert(NW % ((EPT * NW + 63) / 64) == 0, "keys per thread must keep NW a multiple of PER");
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const uint32_t key = kr[j];
+    const uint64_t bg = __ballot(key != kInvalidKey && key > T);
+    const uint64_t be = __ballot(key != kInvalidKey && key == T);
+    if (lane == 0) {
+      cg[j * NW + wid] = uint32_t(__popcll(bg));
+      ce[j * NW + wid] = uint32_t(__popcll(be));
+    }
+  }
+  __syncthreads();
+  // exclusive prefix of the (slot, wave) counts in position order; lane L
+  // holds entries L*PER .. L*PER+PER-1
+  constexpr int NE = EPT * NW;
+  constexpr int PER = (NE + 63) / 64;
+  uint32_t xg[PER], xe[PER];
+  uint32_t sg = 0, se = 0;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int t = lane * PER + q;
+    xg[q] = sg;
+    xe[q] = se;
+    if (t < NE) {
+      sg += cg[t];
+      se += ce[t];
+    }
+  }
+  const uint32_t ig = wave_incl_scan_u32(sg), ie = wave_incl_scan_u32(se);
+  const uint32_t lg0 = ig - sg, le0 = ie - se;
+  const int tot_g = __builtin_amdgcn_readlane(int(ig), 63), tot_e = __builtin_amdgcn_readlane(int(ie), 63);
+  // entry (j, wid) sits at t = j*NW + wid: lane t / PER, slot t % PER = wid % PER
+  uint32_t pg = xg[0], pe = xe[0];
+#pragma unroll
+  for (int q = 1; q < PER; ++q) {
+    if ((wid % PER) == q) {
+      pg = xg[q];
+      pe = xe[q];
+    }
+  }
+  pg += lg0;
+  pe += le0;
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const int src = (j * NW + wid) / PER;
+    const uint32_t key = kr[j];
+    const bool g = key != kInvalidKey && key > T;
+    const bool e = key != kInvalidKey && key == T;
+    const uint64_t bg = __ballot(g);
+    const uint64_t be = __ballot(e);
+    const int gb = gbase + __builtin_amdgcn_readlane(int(pg), src) + lanes_below(bg);
+    const int eb = ebase + __builtin_amdgcn_readlane(int(pe), src) + lanes_below(be);
+    if (g || (e && eb < r)) {
+      const int pos = gb + min(eb, r);
+      out[pos] = map(j, tid + j * NT);
+      if (out_scores) out_scores[pos] = key_float(key);
+    }
+  }
+  gbase += tot_g;
+  ebase += tot_e;
+}
+
 // Counts the caller already knows about its keys: the number of valid keys
 // and bounds lo <= key <= hi of every valid key.  With them the selection
 // skips its own statistics pass and barrier; the caller must then have run
@@ -75,7 +189,7 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   constexpr int kHistAll = align4w_c(4 * kTopkHistWords);
   uint32_t* hist = scratch;             // [4 passes][copies][stride]
-  uint32_t* misc = scratch + kHistAll;  // [64]: 0..47 wave partials, 48/49/51 pass result, 50 list length
+  uint32_t* misc = scratch + kHistAll;  // [64]: 0..47 wave partials, 48/49/51/52 pass result, 50 list length
   uint32_t* cg = misc + 64;             // [EPT][NW] keys > T per (slot, wave)
   uint32_t* ce = cg + kTopkMaxEPT * kTopkMaxNW;  // [EPT][NW] keys == T
 
@@ -144,38 +258,7 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
       }
     }
     __syncthreads();
-    if (wid == 0) {
-      // lane L owns digits 255-4L .. 252-4L (descending); scan from the top
-      uint32_t c[4];
-      uint32_t local = 0;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        c[j] = 0;
-#pragma unroll
-        for (int cp = 0; cp < kTopkHistCopies; ++cp) c[j] += h[cp * kTopkHistStride + 255 - 4 * lane - j];
-        local += c[j];
-      }
-      const uint32_t incl = wave_incl_scan_u32(local);
-      uint32_t run = incl - local;
-      int found = -1;
-      uint32_t found_above = 0, found_cnt = 0;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (found < 0 && run + c[j] >= uint32_t(remaining)) {
-          found = 255 - 4 * lane - j;
-          found_above = run;
-          found_cnt = c[j];
-        }
-        run += c[j];
-      }
-      const uint64_t hit = __ballot(found >= 0);
-      const int src = __ffsll((unsigned long long)hit) - 1;
-      if (lane == src) {
-        misc[48] = uint32_t(found);
-        misc[49] = found_above;
-        misc[51] = found_cnt == uint32_t(remaining) - found_above ? 1u : 0u;
-      }
-    }
+    if (wid == 0) topk_scan_pass(h, remaining, misc);
     __syncthreads();
     prefix |= misc[48] << shift;
     remaining -= int(misc[49]);
@@ -215,62 +298,8 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
   const int r = remaining;  // keys equal to T still to take, lowest positions first
 
   if (kk > 0) {
-#pragma unroll
-    for (int j = 0; j < EPT; ++j) {
-      const uint32_t key = kr[j];
-      const uint64_t bg = __ballot(key != kInvalidKey && key > T);
-      const uint64_t be = __ballot(key != kInvalidKey && key == T);
-      if (lane == 0) {
-        cg[j * NW + wid] = uint32_t(__popcll(bg));
-        ce[j * NW + wid] = uint32_t(__popcll(be));
-      }
-    }
-    __syncthreads();
-    // exclusive prefix of the (slot, wave) counts in position order; lane L
-    // holds entries L*PER .. L*PER+PER-1
-    constexpr int NE = EPT * NW;
-    constexpr int PER = (NE + 63) / 64;
-    uint32_t xg[PER], xe[PER];
-    uint32_t sg = 0, se = 0;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const int t = lane * PER + q;
-      xg[q] = sg;
-      xe[q] = se;
-      if (t < NE) {
-        sg += cg[t];
-        se += ce[t];
-      }
-    }
-    const uint32_t lg0 = wave_incl_scan_u32(sg) - sg;
-    const uint32_t le0 = wave_incl_scan_u32(se) - se;
-    // entry (j, wid) sits at t = j*NW + wid: lane t / PER, slot t % PER = wid % PER
-    uint32_t pg = xg[0], pe = xe[0];
-#pragma unroll
-    for (int q = 1; q < PER; ++q) {
-      if ((wid % PER) == q) {
-        pg = xg[q];
-        pe = xe[q];
-      }
-    }
-    pg += lg0;
-    pe += le0;
-#pragma unroll
-    for (int j = 0; j < EPT; ++j) {
-      const int src = (j * NW + wid) / PER;
-      const uint32_t key = kr[j];
-      const bool g = key != kInvalidKey && key > T;
-      const bool e = key != kInvalidKey && key == T;
-      const uint64_t bg = __ballot(g);
-      const uint64_t be = __ballot(e);
-      const int gb = __builtin_amdgcn_readlane(int(pg), src) + lanes_below(bg);
-      const int eb = __builtin_amdgcn_readlane(int(pe), src) + lanes_below(be);
-      if (g || (e && eb < r)) {
-        const int pos = gb + min(eb, r);
-        out[pos] = map(j, tid + j * NT);
-        if (out_scores) out_scores[pos] = key_float(key);
-      }
-    }
+    int gbase = 0, ebase = 0;
+    topk_compact_tile<NT, EPT>(kr, T, r, gbase, ebase, out, out_scores, map, cg, ce);
   }
   for (int i = kk + tid; i < out_cap; i += NT) {
     out[i] = -1;
@@ -302,6 +331,151 @@ __device__ void wg_topk_ascending(uint32_t* keys, int n, int k, int32_t* out, in
   else if (ept <= 4) wg_topk_lds_ept<NT, 4>(keys, n, k, out, out_cap, out_scores, map, scratch);
   else if (ept <= 8) wg_topk_lds_ept<NT, 8>(keys, n, k, out, out_cap, out_scores, map, scratch);
   else wg_topk_lds_ept<NT, 16>(keys, n, k, out, out_cap, out_scores, map, scratch);
+}
+
+
+// The same selection over keys[0, n) in global memory, for more keys than
+// the registers hold (token-level selection over a whole context): every
+// pass streams the keys in tiles of NT*16; after the first pass the keys
+// still in play are gathered into `list` (LDS, list_cap words) when they fit,
+// so later passes read only those; the ordered compaction then walks the
+// tiles in position order with running counts.  Writes the selected
+// positions ascending to out[0, k'), then -1 up to out_cap.
+template <int NT>
+__device__ void wg_topk_global(const uint32_t* __restrict__ keys, int n, int k, int32_t* out, int out_cap,
+                               uint32_t* scratch, uint32_t* list, int list_cap) {
+  constexpr int NW = NT / 64;
+  constexpr int EPT = kTopkMaxEPT;
+  constexpr int TILE = NT * EPT;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  constexpr int kHistAll = align4w_c(4 * kTopkHistWords);
+  uint32_t* hist = scratch;
+  uint32_t* misc = scratch + kHistAll;
+  uint32_t* cg = misc + 64;
+  uint32_t* ce = cg + kTopkMaxEPT * kTopkMaxNW;
+  const int ntiles = (n + TILE - 1) / TILE;
+  auto load_tile = [&](int t, uint32_t (&kr)[EPT]) {
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) {
+      const int p = t * TILE + tid + j * NT;
+      kr[j] = p < n ? keys[p] : kInvalidKey;
+    }
+  };
+
+  uint32_t cnt = 0, kmx = 0u, kmn = 0xffffffffu;
+  for (int t = 0; t < ntiles; ++t) {
+    uint32_t kr[EPT];
+    load_tile(t, kr);
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) {
+      const uint32_t key = kr[j];
+      cnt += uint32_t(__popcll(__ballot(key != kInvalidKey)));
+      if (key != kInvalidKey) {
+        kmx = max(kmx, key);
+        kmn = min(kmn, key);
+      }
+    }
+  }
+  kmx = wave_max_u32(kmx);
+  kmn = wave_min_u32(kmn);
+  for (int i = tid; i < kHistAll; i += NT) hist[i] = 0u;
+  if (lane == 0) {
+    misc[wid] = cnt;
+    misc[16 + wid] = kmx;
+    misc[32 + wid] = kmn;
+  }
+  if (tid == 0) misc[50] = 0u;
+  __syncthreads();
+  {
+    const int w = lane & 15;
+    const bool ok = w < NW;
+    cnt = combine_waves_sum_u32(ok ? misc[w] : 0u);
+    kmx = combine_waves_max_u32(ok ? misc[16 + w] : 0u);
+    kmn = combine_waves_min_u32(ok ? misc[32 + w] : 0xffffffffu);
+  }
+  const int kk = min(k, int(cnt));
+  uint32_t prefix = 0u, pmask = 0u;
+  int remaining = kk, bits_left = 0;
+  if (kk > 0) {
+    const uint32_t diff = kmx ^ kmn;
+    bits_left = diff ? 32 - __clz(diff) : 0;
+    pmask = bits_left >= 32 ? 0u : ~((1u << bits_left) - 1u);
+    prefix = kmx & pmask;
+  }
+  int list_n = -1;  // < 0: the keys in play are read from global memory
+  for (int pass = 0; bits_left > 0; ++pass) {
+    const int nb = bits_left < 8 ? bits_left : 8;
+    const int shift = bits_left - nb;
+    const uint32_t dmask = (1u << nb) - 1u;
+    uint32_t* h = hist + kTopkHistWords * pass;
+    uint32_t* hc = h + (lane % kTopkHistCopies) * kTopkHistStride;
+    if (list_n < 0) {
+      for (int t = 0; t < ntiles; ++t) {
+        uint32_t kr[EPT];
+        load_tile(t, kr);
+#pragma unroll
+        for (int j = 0; j < EPT; ++j) {
+          const uint32_t key = kr[j];
+          if (key != kInvalidKey && (key & pmask) == prefix) atomicAdd(&hc[(key >> shift) & dmask], 1u);
+        }
+      }
+    } else {
+      for (int i = tid; i < list_n; i += NT) {
+        const uint32_t key = list[i];
+        if ((key & pmask) == prefix) atomicAdd(&hc[(key >> shift) & dmask], 1u);
+      }
+    }
+    __syncthreads();
+    if (wid == 0) topk_scan_pass(h, remaining, misc);
+    __syncthreads();
+    prefix |= misc[48] << shift;
+    remaining -= int(misc[49]);
+    pmask |= dmask << shift;
+    bits_left -= nb;
+    if (misc[51] && bits_left > 0 && prefix != 0u) {
+      prefix -= 1u;
+      remaining = 0;
+      bits_left = 0;
+    }
+    if (list_n < 0 && bits_left > 0 && int(misc[52]) <= list_cap) {
+      for (int t = 0; t < ntiles; ++t) {
+        uint32_t kr[EPT];
+        load_tile(t, kr);
+        uint32_t wcount = 0;
+#pragma unroll
+        for (int j = 0; j < EPT; ++j) {
+          const uint32_t key = kr[j];
+          wcount += uint32_t(__popcll(__ballot(key != kInvalidKey && (key & pmask) == prefix)));
+        }
+        uint32_t base = 0;
+        if (lane == 0 && wcount) base = atomicAdd(&misc[50], wcount);
+        base = uint32_t(__builtin_amdgcn_readfirstlane(int(base)));
+#pragma unroll
+        for (int j = 0; j < EPT; ++j) {
+          const uint32_t key = kr[j];
+          const bool in = key != kInvalidKey && (key & pmask) == prefix;
+          const uint64_t bal = __ballot(in);
+          if (in) list[base + lanes_below(bal)] = key;
+          base += uint32_t(__popcll(bal));
+        }
+      }
+      __syncthreads();
+      list_n = int(misc[50]);
+    }
+  }
+  const uint32_t T = prefix;
+  const int r = remaining;
+  if (kk > 0) {
+    int gbase = 0, ebase = 0;
+    for (int t = 0; t < ntiles; ++t) {
+      uint32_t kr[EPT];
+      load_tile(t, kr);
+      topk_compact_tile<NT, EPT>(kr, T, r, gbase, ebase, out, nullptr,
+                                 [=](int, int p) { return int32_t(t * TILE + p); }, cg, ce);
+      __syncthreads();  // cg / ce are rewritten by the next tile
+    }
+  }
+  for (int i = kk + tid; i < out_cap; i += NT) out[i] = -1;
 }
 
 }  // namespace tls

@@ -283,7 +283,8 @@ def pin_single_level_operators(n_override=None):
     tokens; block-sparse attention attends exactly the valid tokens of the
     top-k_b blocks, equals the two-level operator with k_t >= those tokens,
     equals full attention when k_b covers every block, and keeps the planted
-    blocks."""
+    blocks; token-level selection alone scores every token, equals the
+    two-level operator with k_b = every block and keeps the planted tokens."""
     cfg, d, q, K, V = _toy_f64(n_override)
     n = int(d["ctx_lens"][0])
     m = O.num_blocks(n, cfg.block)
@@ -310,6 +311,16 @@ def pin_single_level_operators(n_override=None):
         assert set(p // cfg.block for p in planted) <= set(M.tolist())
         full = O.block_sparse_unit(qg, K[0, g], V[0, g], n, m, cfg.block, cfg.sigma)
         np.testing.assert_allclose(full["out"], dn["out"], rtol=1e-12, atol=1e-14)
+        # token-level selection alone: its candidates are every valid token,
+        # it equals the two-level operator with k_b = every block, keeps the
+        # planted tokens, and with k_t = n it is full attention
+        ts = O.token_sparse_unit(qg, K[0, g], V[0, g], n, d["channels"][g], cfg.k_t, cfg.block, cfg.sigma)
+        assert ts["cand"].tolist() == list(range(n)) and len(ts["token_ids"]) == min(cfg.k_t, n)
+        two_all = O.decode_unit(qg, K[0, g], V[0, g], n, d["channels"][g], m, cfg.k_t, cfg.block, cfg.sigma)
+        assert np.array_equal(two_all["token_ids"], ts["token_ids"])
+        assert set(planted) <= set(ts["token_ids"].tolist())
+        ts_all = O.token_sparse_unit(qg, K[0, g], V[0, g], n, d["channels"][g], n, cfg.block, cfg.sigma)
+        np.testing.assert_allclose(ts_all["out"], dn["out"], rtol=1e-12, atol=1e-14)
 
 
 def pin_lagged_schedule():

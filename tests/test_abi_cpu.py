@@ -141,7 +141,10 @@ def test_decode_modes_are_validated_before_launch(tls):
                                      dummy, 8, 128, bids_in, tids_in, dummy, null, bids_out, tids_out, dummy,
                                      1 << 40, ctypes.byref(opts), null)
 
-    assert call(3) == 1 and call(-1) == 1
+    assert call(4) == 1 and call(-1) == 1
+    assert call(tls.MODE_TOKEN_SPARSE, bids_in=dummy) == 1
+    assert call(tls.MODE_TOKEN_SPARSE, tids_in=dummy) == 1
+    assert call(tls.MODE_TOKEN_SPARSE, bids_out=dummy) == 1
     assert call(tls.MODE_DENSE, tids_in=dummy) == 1
     assert call(tls.MODE_DENSE, bids_in=dummy) == 1
     assert call(tls.MODE_DENSE, bids_out=dummy) == 1

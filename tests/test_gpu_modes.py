@@ -52,15 +52,17 @@ def run_mode(c, mode, block_ids_in=None):
     cfg = c.cfg
     out = torch.empty((cfg.batch, cfg.h_q, cfg.d_v), dtype=H.torch_dtype(cfg), device="cuda")
     lse = torch.empty((cfg.batch, cfg.h_q), dtype=torch.float32, device="cuda")
-    bids = None
+    bids = tids = None
     if mode == tls.MODE_BLOCK_SPARSE and block_ids_in is None:
         bids = torch.empty((cfg.batch, cfg.h_kv, cfg.k_b), dtype=torch.int32, device="cuda")
+    if mode == tls.MODE_TOKEN_SPARSE:
+        tids = torch.empty((cfg.batch, cfg.h_kv, cfg.k_t), dtype=torch.int32, device="cuda")
     ws = c.workspace()
-    tls.tls_sparse_decode(c.layout, c.q, c.kv(), c.ctx, c.kmax, c.kmin, None, None, None, cfg.k_b, cfg.k_t,
-                          block_ids_in, None, out, lse, bids, None, ws, mode=mode)
+    tls.tls_sparse_decode(c.layout, c.q, c.kv(), c.ctx, c.kmax, c.kmin, c.codes, c.qparams, c.ch, cfg.k_b, cfg.k_t,
+                          block_ids_in, None, out, lse, bids, tids, ws, mode=mode)
     torch.cuda.synchronize()
     assert tls.tls_check_device_error(ws) == 0
-    return out, lse, bids
+    return out, lse, bids if tids is None else tids
 
 
 def _unit(c, s, g):
@@ -107,3 +109,25 @@ def test_block_sparse_mode(name):
         H.check_close(lse[s, g * G:(g + 1) * G].cpu().numpy(), ref2["lse"], cfg.dtype, f"lse {(s, g)}")
     out2, lse2, _ = run_mode(c, tls.MODE_BLOCK_SPARSE, block_ids_in=bids)
     assert torch.equal(out2, out) and torch.equal(lse2.nan_to_num(0.0), lse.nan_to_num(0.0))
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_token_sparse_mode(name):
+    """Token-level selection alone: the top-K_t of the approximate score over
+    every valid token (near-tie rule), then attention over the GPU's tokens
+    equals the oracle's."""
+    import paper_2604_07815_amd as tls
+    c = get_case(name)
+    cfg = c.cfg
+    G = cfg.group
+    out, lse, tids = run_mode(c, tls.MODE_TOKEN_SPARSE)
+    for (s, g) in c.sample:
+        qg, Ku, Vu, n = _unit(c, s, g)
+        ref = O.token_sparse_unit(qg, Ku, Vu, n, c.ch_host[g], cfg.k_t, cfg.block, cfg.sigma)
+        H.check_selection(tids[s, g].cpu().numpy(), ref["token_ids"], H.alpha_lookup(ref), f"tokens {(s, g)}")
+        mine = H.valid_ids(tids[s, g].cpu().numpy())
+        o, l = O.sparse_attention(qg, Ku, Vu, mine, cfg.sigma)
+        H.check_close(out[s, g * G:(g + 1) * G].float().cpu().numpy(), o, cfg.dtype, f"out {(s, g)}")
+        H.check_close(lse[s, g * G:(g + 1) * G].cpu().numpy(), l, cfg.dtype, f"lse {(s, g)}")
+        planted = [int(p) + i for p in c.plant_starts[s, g] if p >= 0 for i in range(cfg.cluster_len)]
+        assert set(planted) <= set(mine.tolist()), f"planted tokens missed in unit {(s, g)}"
