@@ -225,6 +225,60 @@ def traffic_from_profiles(kernel_src_hash):
     return d.get("traffic_bytes_per_launch")
 
 
+def prefill_timing(tls, torch, cfg, layout, d, L, e, reps=3):
+    """Prefill-side calls on the full workload, HIP events on the launch
+    stream, median of `reps` after one warm call: the two index builders over
+    the resident K, and the fused prefill (K/V rows from the token-major
+    prefill output into the cache, both indices from the same read).  The
+    fused call rewrites the cache with the bytes it already holds."""
+    import numpy as np
+    ctx, ch, T = d["ctx_lens"], d["channels"], cfg.max_ctx
+    n_tok = int(d["ctx_host"].astype(np.int64).sum()) * cfg.h_kv
+    m_tok = int(sum(-(-int(n) // cfg.block) for n in d["ctx_host"])) * cfg.h_kv
+    idx_out = m_tok * 2 * cfg.d_qk * e + n_tok * (cfg.d_c // 2 + 8 * (cfg.d_c // 32))
+    row_kv = cfg.d_qk * e + (0 if cfg.mla else cfg.d_v * e)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(f):
+        f()
+        ts = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            start.record()
+            f()
+            stop.record()
+            torch.cuda.synchronize()
+            ts.append(start.elapsed_time(stop))
+        return float(np.median(ts))
+
+    def build():
+        tls.tls_build_block_index(layout, L["k"], ctx, 0, T, L["kmax"], L["kmin"])
+        tls.tls_build_token_index(layout, L["k"], ctx, ch, 0, T, L["codes"], L["qparams"])
+
+    build_ms = timed(build)
+    k_src = L["k"].transpose(1, 2).contiguous()
+    v_src = None if cfg.mla else L["v"].transpose(1, 2).contiguous()
+
+    def fused():
+        tls.tls_prefill_kv(layout, k_src, v_src, ctx, ch, 0, T, L["k"], L["v"], L["kmax"], L["kmin"], L["codes"],
+                           L["qparams"])
+
+    fused_ms = timed(fused)
+    del k_src, v_src
+    torch.cuda.empty_cache()
+    build_bytes = 2 * n_tok * cfg.d_qk * e + idx_out       # each builder reads K once
+    fused_bytes = 2 * n_tok * row_kv + idx_out             # prefill rows in, cache rows out, indices out
+    return {
+        "index_build_ms": round(build_ms, 3),
+        "index_build_GBps": round(build_bytes / (build_ms * 1e-3) / 1e9, 1),
+        "prefill_kv_ms": round(fused_ms, 3),
+        "prefill_kv_GBps": round(fused_bytes / (fused_ms * 1e-3) / 1e9, 1),
+        "note": "index_build = tls_build_block_index + tls_build_token_index over the whole context (K read by "
+                "each); prefill_kv = tls_prefill_kv: K/V rows from the token-major prefill output written to the "
+                "cache and both indices built from the same read; bytes = reads + writes of valid rows",
+    }
+
+
 def offload_schedule(tls, synth, torch, np):
     """The offloaded KV tier of the 96k workload (Sec. 4.2), as a serving loop:
     K/V of every sequence in pinned host memory, block and token indices and
@@ -247,34 +301,52 @@ def offload_schedule(tls, synth, torch, np):
     codes = torch.empty((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 2), dtype=torch.uint8, device=dev)
     qparams = torch.empty((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 32, 2), dtype=torch.float32, device=dev)
     ctx, ch = d["ctx_lens"], d["channels"]
-    tls.tls_build_block_index(layout, d["k"], ctx, 0, cfg.max_ctx, kmax, kmin)
-    tls.tls_build_token_index(layout, d["k"], ctx, ch, 0, cfg.max_ctx, codes, qparams)
-    host_k = torch.empty(d["k"].shape, dtype=dt, pin_memory=True)
-    host_v = torch.empty(d["v"].shape, dtype=dt, pin_memory=True)
-    host_k.copy_(d["k"])
-    host_v.copy_(d["v"])
-    del d
-    torch.cuda.synchronize()
-    torch.cuda.empty_cache()
     B, units, K_b = cfg.block, cfg.batch * cfg.h_kv, cfg.k_b
     n_slots = 2 * K_b
-    pool_k = torch.zeros((units, n_slots, B, cfg.d_qk), dtype=dt, device=dev)
-    pool_v = torch.zeros((units, n_slots, B, cfg.d_v), dtype=dt, device=dev)
-    slot_map = torch.full((units, m_max), -1, dtype=torch.int32, device=dev)
-    slot_owner = torch.full((units, n_slots), -1, dtype=torch.int32, device=dev)
-    tcount = torch.zeros(units, dtype=torch.int32, device=dev)
-    ws = tls.alloc_workspace(layout, K_b, cfg.k_t, device=dev)
-    kv = tls.KV(pool_k, pool_v, slot_map, n_slots)
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     main = torch.cuda.current_stream()
     side = torch.cuda.Stream()
+    ws = tls.alloc_workspace(layout, K_b, cfg.k_t, device=dev)
     qs = [synth.host_to_torch(walk[t], cfg.dtype).to(dev) for t in range(walk.shape[0])]
-    out = torch.empty((cfg.batch, cfg.h_q, cfg.d_v), dtype=dt, device=dev)
     M = [torch.empty((cfg.batch, cfg.h_kv, K_b), dtype=torch.int32, device=dev) for _ in range(2)]
+    # prefill flow (Fig. 2): the prompt's K/V rows (token-major) go to the HBM
+    # cache with both indices built on the way; the final prompt query selects
+    # the initial residency; the cache is offloaded to pinned host memory on a
+    # side stream, and the HBM cache is then released
+    k_src = d["k"].transpose(1, 2).contiguous()
+    v_src = d["v"].transpose(1, 2).contiguous()
+    K, V = d.pop("k"), d.pop("v")
+    p0, p1 = ev(), ev()
+    p0.record(main)
+    tls.tls_prefill_kv(layout, k_src, v_src, ctx, ch, 0, cfg.max_ctx, K, V, kmax, kmin, codes, qparams)
+    p1.record(main)
+    del k_src, v_src
+    host_k = torch.empty(K.shape, dtype=dt, pin_memory=True)
+    host_v = torch.empty(V.shape, dtype=dt, pin_memory=True)
+    pool_k = torch.zeros((units, n_slots, B, cfg.d_qk), dtype=dt, device=dev)
+    pool_v = torch.zeros((units, n_slots, B, cfg.d_v), dtype=dt, device=dev)
+    slot_map = torch.empty((units, m_max), dtype=torch.int32, device=dev)
+    slot_owner = torch.empty((units, n_slots), dtype=torch.int32, device=dev)
+    tcount = torch.zeros(units, dtype=torch.int32, device=dev)
+    o0, o1, r0, r1 = ev(), ev(), ev(), ev()
     tls.tls_select_blocks(layout, qs[0], kmax, kmin, ctx, K_b, M[0], None, ws)
-    tls.tls_prefetch_blocks(layout, host_k, host_v, ctx, M[0], None, K_b, pool_k, pool_v, n_slots, slot_map,
-                            slot_owner, tcount, ws)
+    r0.record(main)
+    tls.tls_init_residency(layout, K, V, ctx, M[0], K_b, pool_k, pool_v, n_slots, slot_map, slot_owner, ws)
+    r1.record(main)
+    # the offload starts once the residency copy is done: copy work-groups that
+    # share a compute unit with work-groups stalled on PCIe stores slow down
+    side.wait_stream(main)
+    o0.record(side)
+    tls.tls_offload_kv(layout, K, V, ctx, 0, cfg.max_ctx, host_k, host_v, stream=side)
+    o1.record(side)
     torch.cuda.synchronize()
-    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    kv_bytes = 2 * K.numel() * K.element_size()
+    prefill_rec = dict(prefill_kv_ms=p0.elapsed_time(p1), offload_ms=o0.elapsed_time(o1),
+                       residency_ms=r0.elapsed_time(r1))
+    del K, V, d
+    torch.cuda.empty_cache()
+    kv = tls.KV(pool_k, pool_v, slot_map, n_slots)
+    out = torch.empty((cfg.batch, cfg.h_q, cfg.d_v), dtype=dt, device=dev)
     rec = []
     for t in range(1, walk.shape[0]):
         M_prev, M_t = M[(t - 1) % 2], M[t % 2]
@@ -313,6 +385,15 @@ def offload_schedule(tls, synth, torch, np):
         "block_repeat_rate": round(1.0 - blocks / (units * K_b), 4),
         "transfer_MB_per_step_mean": round(xfer_bytes / 1e6, 1),
         "pcie_GBps": round(xfer_bytes / (med("xfer") * 1e-6) / 1e9, 1),
+        "prefill_flow": {
+            "prefill_kv_ms": round(prefill_rec["prefill_kv_ms"], 2),
+            "offload_ms": round(prefill_rec["offload_ms"], 1),
+            "offload_GBps": round(kv_bytes / (prefill_rec["offload_ms"] * 1e-3) / 1e9, 1),
+            "initial_residency_ms": round(prefill_rec["residency_ms"], 3),
+            "note": "tls_prefill_kv (write-back + both indices), then the final prompt query's blocks made "
+                    "resident from HBM (tls_init_residency), then tls_offload_kv copies the whole cache to pinned "
+                    "host memory on a side stream",
+        },
         "device_error_flags": err,
     }
 
@@ -352,12 +433,9 @@ def main():
     kmin = torch.empty_like(kmax)
     codes = torch.empty((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 2), dtype=torch.uint8, device=dev)
     qparams = torch.empty((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 32, 2), dtype=torch.float32, device=dev)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
     tls.tls_build_block_index(layout, d["k"], d["ctx_lens"], 0, cfg.max_ctx, kmax, kmin)
     tls.tls_build_token_index(layout, d["k"], d["ctx_lens"], d["channels"], 0, cfg.max_ctx, codes, qparams)
     torch.cuda.synchronize()
-    index_build_ms = (time.perf_counter() - t0) * 1e3
 
     layer = dict(q=d["q"], k=d["k"], v=d["v"], kmax=kmax, kmin=kmin, codes=codes, qparams=qparams)
     per_layer = sum(t.numel() * t.element_size() for t in layer.values() if t is not None)
@@ -477,6 +555,9 @@ def main():
                          f"the two-level token budget); token-sparse selects the top-{cfg.k_t} tokens of the "
                          f"whole context by the same approximate score; dense attends all ctx_len tokens")
 
+    # ---- prefill side (off the per-step clock): index build, fused write-back ----
+    prefill = None if args.profile_only else prefill_timing(tls, torch, cfg, layout, d, layers[0], e)
+
     err = tls.tls_check_device_error(ws)
     nb = algorithmic_bytes(cfg, d["ctx_host"], bids.cpu().numpy(), e)
     us = ms_per_step * 1e3
@@ -510,7 +591,7 @@ def main():
         "algorithmic_bytes_per_step": nb,
         "stage_us": {k: round(float(v) * 1e3, 2) for k, v in zip(STAGES, stage_ms)},
         "stage_marked_step_us": round(marked_ms * 1e3, 2),
-        "index_build_ms": round(index_build_ms, 3),
+        "prefill": prefill,
         "device_error_flags": err,
         "operators": modes or None,
         "roofline": {

@@ -189,6 +189,27 @@ tls_status tls_build_token_index(const tls_layout* layout, const void* K, const 
                                  const int32_t* channels, int32_t tok_begin, int32_t tok_end,
                                  uint8_t* codes, float* qparams, hipStream_t stream);
 
+/* Prefill write-back fused with both index builds (the prefill flow of
+ * Sec. 4.2 / Fig. 2: the hierarchical indices are built while the prompt's
+ * keys are stored).  For every token t in [tok_begin, tok_end) with
+ * t < ctx_len of its sequence s, copies the prefill output rows
+ *   K[s][h][t][:] = k_src[s][t - tok_begin][h][:]   (and V from v_src),
+ * then builds the block index of every block overlapping the range and the
+ * token index of those tokens, exactly as tls_build_block_index and
+ * tls_build_token_index over [tok_begin, tok_end) would after the copy (bit
+ * for bit), from one read of each touched block.  Rows of those blocks
+ * outside the range (earlier prefill chunks, or later rows already present)
+ * are read from K.  Tokens at or past ctx_len are skipped.
+ *   k_src  [b][tok_end - tok_begin][H_kv][d_qk]  dtype, token-major as a key
+ *                                                projection produces it
+ *   v_src  [b][tok_end - tok_begin][H_kv][d_v]   dtype; NULL iff mla_shared_kv
+ *   K, V   dense cache layouts (V NULL iff mla_shared_kv)
+ * Chunked prefill: call once per chunk with consecutive ranges. */
+tls_status tls_prefill_kv(const tls_layout* layout, const void* k_src, const void* v_src,
+                          const int32_t* ctx_lens, const int32_t* channels, int32_t tok_begin,
+                          int32_t tok_end, void* K, void* V, void* kmax, void* kmin, uint8_t* codes,
+                          float* qparams, hipStream_t stream);
+
 /* Coarse block selection, Sec. 4.1: per unit, the Quest score of each of the
  * ceil(ctx_len/B) blocks, s_i = sum_h (max(q_h,0) . kmax_i + min(q_h,0) . kmin_i)
  * (the paper's GEMM form; fp32 accumulation), then M = the K_b highest
@@ -252,6 +273,33 @@ tls_status tls_prefetch_blocks(const tls_layout* layout, const void* host_k, con
                                void* pool_v, int64_t n_slots, int32_t* slot_map,
                                int32_t* slot_owner, int32_t* transfer_count, void* ws,
                                size_t ws_bytes, hipStream_t stream);
+
+/* Offload of the prefill KV cache to host memory (Sec. 4.2 / Fig. 2: after
+ * prefill the cache lives in host memory and only a resident subset stays in
+ * HBM).  Copies rows [tok_begin, min(tok_end, ctx_len)) of every unit of the
+ * dense device K (and V) into host_k (and host_v), caller-owned pinned host
+ * arrays with the same dense layouts, by device-side stores over PCIe on a
+ * few work-groups (enqueue on a side stream to overlap other work).  V and
+ * host_v are NULL iff mla_shared_kv.  Rows outside the range are untouched. */
+tls_status tls_offload_kv(const tls_layout* layout, const void* K, const void* V, const int32_t* ctx_lens,
+                          int32_t tok_begin, int32_t tok_end, void* host_k, void* host_v,
+                          hipStream_t stream);
+
+/* Initial residency of the offloaded tier (Sec. 4.2 / Fig. 2: the blocks
+ * selected for the final prefill query stay in HBM).  Empties the pool
+ * (slot_map all -1, slot_owner all -1), then gives the blocks of block_ids
+ * ([b][H_kv][K_b], -1 entries ignored; normally tls_select_blocks of the
+ * last prompt token's query) slots 0, 1, ... in ascending block order and
+ * copies their rows from src_k/src_v (dense layouts, device memory or
+ * pinned host memory) into the pool.  The result is the state
+ * tls_prefetch_blocks would reach from an empty pool; the decode loop then
+ * continues with tls_prefetch_blocks.  n_slots >= K_b (2 * K_b for the
+ * lagged schedule).  Block ids past the unit's block count set
+ * TLS_DEVERR_BLOCK_ID and are skipped. */
+tls_status tls_init_residency(const tls_layout* layout, const void* src_k, const void* src_v,
+                              const int32_t* ctx_lens, const int32_t* block_ids, int32_t K_b,
+                              void* pool_k, void* pool_v, int64_t n_slots, int32_t* slot_map,
+                              int32_t* slot_owner, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Reads (and, if clear != 0, resets) the device error word of a workspace.
  * Synchronous: waits for `stream`.  *flags receives TLS_DEVERR_* bits. */

@@ -36,7 +36,8 @@ DEVERR_CTX_LEN, DEVERR_BLOCK_ID, DEVERR_TOKEN_ID, DEVERR_SLOT, DEVERR_POOL_FULL,
 EXPORTED_SYMBOLS = [
     "tls_version", "tls_status_string", "tls_workspace_size", "tls_workspace_init",
     "tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
-    "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error",
+    "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error", "tls_prefill_kv",
+    "tls_offload_kv", "tls_init_residency",
 ]
 
 
@@ -80,11 +81,14 @@ def _load() -> ctypes.CDLL:
         "tls_workspace_init": (I32, [P, SZ, P]),
         "tls_build_block_index": (I32, [LP, P, P, I32, I32, P, P, P]),
         "tls_build_token_index": (I32, [LP, P, P, P, I32, I32, P, P, P]),
+        "tls_prefill_kv": (I32, [LP, P, P, P, P, I32, I32, P, P, P, P, P, P, P]),
         "tls_select_blocks": (I32, [LP, P, P, P, P, I32, P, P, P, SZ, P]),
         "tls_select_tokens": (I32, [LP, P, P, P, P, P, I32, P, I32, P, P, P, SZ, P]),
         "tls_sparse_decode": (I32, [LP, P, ctypes.POINTER(KvView), P, P, P, P, P, P, I32, I32, P, P,
                                     P, P, P, P, P, SZ, ctypes.POINTER(DecodeOpts), P]),
         "tls_prefetch_blocks": (I32, [LP, P, P, P, P, P, I32, P, P, I64, P, P, P, P, SZ, P]),
+        "tls_offload_kv": (I32, [LP, P, P, P, I32, I32, P, P, P]),
+        "tls_init_residency": (I32, [LP, P, P, P, P, I32, P, P, I64, P, P, P, SZ, P]),
         "tls_check_device_error": (I32, [P, SZ, I32, ctypes.POINTER(I32), P]),
     }
     for name, (res, args) in sig.items():
@@ -183,6 +187,16 @@ def tls_build_token_index(layout, K, ctx_lens, channels, tok_begin, tok_end, cod
            "tls_build_token_index")
 
 
+def tls_prefill_kv(layout, k_src, v_src, ctx_lens, channels, tok_begin, tok_end, K, V, kmax, kmin, codes,
+                   qparams, stream=None) -> None:
+    """Prefill write-back of rows [tok_begin, tok_end) fused with both index builds."""
+    _check(_lib.tls_prefill_kv(ctypes.byref(layout), _ptr(k_src, "k_src"), _ptr(v_src, "v_src"),
+                               _ptr(ctx_lens, "ctx_lens"), _ptr(channels, "channels"), int(tok_begin),
+                               int(tok_end), _ptr(K, "K"), _ptr(V, "V"), _ptr(kmax, "kmax"), _ptr(kmin, "kmin"),
+                               _ptr(codes, "codes"), _ptr(qparams, "qparams"), _stream(stream)),
+           "tls_prefill_kv")
+
+
 def tls_select_blocks(layout, q, kmax, kmin, ctx_lens, K_b, block_ids, block_scores, ws, stream=None) -> None:
     _check(_lib.tls_select_blocks(ctypes.byref(layout), _ptr(q, "q"), _ptr(kmax, "kmax"), _ptr(kmin, "kmin"),
                                   _ptr(ctx_lens, "ctx_lens"), int(K_b), _ptr(block_ids, "block_ids"),
@@ -250,6 +264,31 @@ def tls_prefetch_blocks(layout, host_k, host_v, ctx_lens, block_ids_new, block_i
         int(n_slots), _ptr(slot_map, "slot_map"), _ptr(slot_owner, "slot_owner"),
         _ptr(transfer_count, "transfer_count"), _ptr(ws, "ws"), _nbytes(ws), _stream(stream)),
         "tls_prefetch_blocks")
+
+
+def _pinned(t, name):
+    if t is not None and (t.is_cuda or not t.is_pinned()):
+        raise ValueError(f"{name}: must be a pinned host tensor")
+    return _ptr(t, name, device=False)
+
+
+def tls_offload_kv(layout, K, V, ctx_lens, tok_begin, tok_end, host_k, host_v, stream=None) -> None:
+    """Device -> pinned host copy of the cache rows [tok_begin, tok_end)."""
+    _check(_lib.tls_offload_kv(ctypes.byref(layout), _ptr(K, "K"), _ptr(V, "V"), _ptr(ctx_lens, "ctx_lens"),
+                               int(tok_begin), int(tok_end), _pinned(host_k, "host_k"), _pinned(host_v, "host_v"),
+                               _stream(stream)), "tls_offload_kv")
+
+
+def tls_init_residency(layout, src_k, src_v, ctx_lens, block_ids, K_b, pool_k, pool_v, n_slots, slot_map,
+                       slot_owner, ws, stream=None) -> None:
+    """Empty the pool and make block_ids resident; src_k/src_v: GPU tensors or pinned host tensors."""
+    def src(t, name):
+        return None if t is None else (_ptr(t, name) if t.is_cuda else _pinned(t, name))
+    _check(_lib.tls_init_residency(
+        ctypes.byref(layout), src(src_k, "src_k"), src(src_v, "src_v"), _ptr(ctx_lens, "ctx_lens"),
+        _ptr(block_ids, "block_ids"), int(K_b), _ptr(pool_k, "pool_k"), _ptr(pool_v, "pool_v"), int(n_slots),
+        _ptr(slot_map, "slot_map"), _ptr(slot_owner, "slot_owner"), _ptr(ws, "ws"), _nbytes(ws),
+        _stream(stream)), "tls_init_residency")
 
 
 def tls_check_device_error(ws, clear: bool = False, stream=None) -> int:

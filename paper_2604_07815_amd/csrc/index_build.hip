@@ -1,152 +1,402 @@
-// Index construction at prefill (AsyncTLS Sec. 4.1):
-//  * block_index_kernel - per-channel max/min key of every block of B tokens
-//    (the Quest block representation), tail block over its valid tokens;
-//  * token_index_kernel - keys projected on the channel set C and quantised
-//    to asymmetric uint4 per group of 32 channels (INT4 per Sec. 5 setup),
-//    computed with an exact float32 op sequence so the codes are
-//    reproducible bit for bit.
+// Index construction (AsyncTLS Sec. 4.1), optionally fused with the K/V
+// write-back of prefill (the prefill flow of Sec. 4.2 / Fig. 2):
+//  * block index - per-channel max/min key of every block of B tokens (the
+//    Quest block representation), the tail block over its valid tokens;
+//  * token index - keys projected on the channel set C and quantised to
+//    asymmetric uint4 per group of 32 channels (INT4 per the Sec. 5 setup),
+//    with an exact float32 op sequence so the codes are reproducible bit for
+//    bit.
+//
+// One work-group per (block, unit).  It stages the block's rows in LDS with
+// coalesced 16-byte loads (taking the rows of the prefill range from the
+// prefill output, and writing them to the cache on the way), then derives
+// both indices from the tile, so K is read once for both.  Rows wider than
+// the LDS budget are processed in passes of fewer rows; the block max/min
+// then accumulate across passes in registers.
+//
+// Token index: one lane per (token, 32-channel group), the group uniform
+// over a wave, so the channel ids are broadcast reads and every lane walks
+// its own row; staged rows are padded by one word so that the 64 lanes of a
+// wave reading one channel of 64 rows hit different banks.  The scale takes
+// one IEEE division per (token, group); each code's quotient comes from a
+// multiply by the reciprocal of the scale unless it lies within kNearHalf of
+// a rounding boundary (or is not finite), where the IEEE quotient is
+// computed instead, so every code equals rint of the correctly rounded
+// quotient.
 #include "kernels.hpp"
 
 namespace tls {
 
-// One thread per (block, 16-byte channel chunk); rows streamed top to bottom.
-template <class E>
-__global__ __launch_bounds__(256) void block_index_kernel(
-    const typename E::T* __restrict__ K, const int32_t* __restrict__ ctx_lens, int H_kv, int T, int d,
-    int B, int m_max, int tok_begin, int tok_end, typename E::T* __restrict__ kmax,
-    typename E::T* __restrict__ kmin, uint32_t* err) {
-  using S = typename E::T;
-  constexpr int V = E::kVec;
-  const int s = blockIdx.z, g = blockIdx.y;
-  int n = ctx_lens[s];
-  if (n < 0 || n > T) {
-    if (threadIdx.x == 0 && blockIdx.x == 0 && g == 0) set_error(err, 1u);
-    n = n < 0 ? 0 : T;
-  }
-  const int hi = min(tok_end, n);
-  if (tok_begin >= hi) return;
-  const int b0 = tok_begin / B, b1 = (hi + B - 1) / B;  // blocks overlapping [tok_begin, hi)
-  const int cpb = d / V;                                 // chunks per block row
-  const size_t unit = size_t(s) * H_kv + g;
-  const S* Ku = K + unit * size_t(T) * d;
-  const int items = (b1 - b0) * cpb;
-  for (int it = blockIdx.x * blockDim.x + threadIdx.x; it < items; it += gridDim.x * blockDim.x) {
-    const int i = b0 + it / cpb, c = it % cpb;
-    const int r0 = i * B, r1 = min(r0 + B, n);
-    float mx[V], mn[V];
-    {
-      float x[V];
-      unpack16<E>(ld16(Ku + size_t(r0) * d + c * V), x);
+constexpr int kIdxThreads = 256;
+constexpr int kIdxTileBytes = 73984;  // LDS for staged rows: 64 padded rows of an MLA (576 x bf16) key
+constexpr int kIdxMaxWords = 4;       // 4-byte words per thread in the block summary (rows <= 4 KB)
+constexpr int kIdxLoadUnroll = 4;     // 16-byte loads in flight per thread
+// A code from the reciprocal product is used when the product lies farther
+// than this from a half-integer; its error (< 2^-17 for quotients below 16,
+// with a 1-ulp reciprocal) then cannot change the rounded code.
+constexpr float kNearHalf = 1.0f / 16384.0f;
+
+enum : int { kIdxBlock = 1, kIdxToken = 2 };
+
+struct IndexArgs {
+  const uint8_t* k_src;  // prefill K rows [b][S][H_kv][d], S = tok_end - tok_begin; NULL: rows already in k
+  const uint8_t* v_src;  // prefill V rows [b][S][H_kv][d_v]; NULL: no V write-back
+  uint8_t* k;            // dense K cache [b][H_kv][T][d]
+  uint8_t* v;            // dense V cache [b][H_kv][T][d_v]
+  const int32_t* ctx_lens;
+  const int32_t* channels;  // [H_kv][d_c]
+  uint8_t* kmax;
+  uint8_t* kmin;
+  uint8_t* codes;
+  float* qparams;
+  int H_kv, T, d, d_v, d_c, B, m_max, tok_begin, tok_end;
+  int rows_per_pass;  // rows staged in LDS at a time (B when a block fits)
+  int flags;          // kIdxBlock | kIdxToken
+  uint32_t* err;
+};
+
+// Copies rows [r_lo, r_hi) of one unit's V from the prefill output to the cache.
+__device__ inline void copy_v_rows(const IndexArgs& a, int s, int g, size_t unit, int r_lo, int r_hi, int es) {
+  const int rbv = a.d_v * es;
+  const size_t S = size_t(a.tok_end - a.tok_begin);
+  if (rbv % 16 == 0) {
+    const int cpr = rbv / 16;
+    const int n = (r_hi - r_lo) * cpr;
+    for (int base = 0; base < n; base += kIdxThreads * kIdxLoadUnroll) {
+      uint4 x[kIdxLoadUnroll];
 #pragma unroll
-      for (int e = 0; e < V; ++e) mx[e] = mn[e] = x[e];
-    }
-    for (int r = r0 + 1; r < r1; ++r) {
-      float x[V];
-      unpack16<E>(ld16(Ku + size_t(r) * d + c * V), x);
+      for (int u = 0; u < kIdxLoadUnroll; ++u) {
+        const int idx = base + u * kIdxThreads + int(threadIdx.x);
+        if (idx < n) {
+          const int r = r_lo + idx / cpr, c = idx % cpr;
+          x[u] = ld16(a.v_src + ((size_t(s) * S + (r - a.tok_begin)) * a.H_kv + g) * rbv + c * 16);
+        }
+      }
 #pragma unroll
-      for (int e = 0; e < V; ++e) {
-        mx[e] = fmaxf(mx[e], x[e]);
-        mn[e] = fminf(mn[e], x[e]);
+      for (int u = 0; u < kIdxLoadUnroll; ++u) {
+        const int idx = base + u * kIdxThreads + int(threadIdx.x);
+        if (idx < n) {
+          const int r = r_lo + idx / cpr, c = idx % cpr;
+          *reinterpret_cast<uint4*>(a.v + (unit * a.T + r) * rbv + c * 16) = x[u];
+        }
       }
     }
-    S* pmax = kmax + (unit * m_max + i) * d + c * V;
-    S* pmin = kmin + (unit * m_max + i) * d + c * V;
-#pragma unroll
-    for (int e = 0; e < V; ++e) {
-      // values are exact copies of inputs; +0.0f turns -0.0 into +0.0
-      store_out<E>(pmax + e, mx[e] + 0.0f);
-      store_out<E>(pmin + e, mn[e] + 0.0f);
+  } else {  // rows that are not a multiple of 16 bytes: element copies
+    const int n = (r_hi - r_lo) * a.d_v;
+    for (int idx = threadIdx.x; idx < n; idx += kIdxThreads) {
+      const int r = r_lo + idx / a.d_v, c = idx % a.d_v;
+      const uint8_t* src = a.v_src + ((size_t(s) * S + (r - a.tok_begin)) * a.H_kv + g) * rbv + c * es;
+      uint8_t* dst = a.v + (unit * a.T + r) * rbv + c * es;
+      if (es == 2) *reinterpret_cast<uint16_t*>(dst) = *reinterpret_cast<const uint16_t*>(src);
+      else *reinterpret_cast<uint32_t*>(dst) = *reinterpret_cast<const uint32_t*>(src);
     }
   }
 }
 
-// 32 lanes per (token, channel group); a wave covers two (token, group) pairs.
 template <class E>
-__global__ __launch_bounds__(256) void token_index_kernel(
-    const typename E::T* __restrict__ K, const int32_t* __restrict__ ctx_lens,
-    const int32_t* __restrict__ channels, int H_kv, int T, int d, int d_c, int tok_begin, int tok_end,
-    uint8_t* __restrict__ codes, float* __restrict__ qparams, uint32_t* err) {
+__global__ __launch_bounds__(kIdxThreads) void index_rows_kernel(const IndexArgs a) {
 #pragma clang fp contract(off)
+  constexpr int es = int(sizeof(typename E::T));
+  constexpr int EPW = 4 / es;  // elements per 4-byte word
+  extern __shared__ uint4 smem4[];
   const int s = blockIdx.z, g = blockIdx.y;
-  int n = ctx_lens[s];
-  if (n < 0 || n > T) {
-    if (threadIdx.x == 0 && blockIdx.x == 0 && g == 0) set_error(err, 1u);
-    n = n < 0 ? 0 : T;
+  const int tid = threadIdx.x;
+  int n = a.ctx_lens[s];
+  if (n < 0 || n > a.T) {
+    if (tid == 0 && blockIdx.x == 0 && g == 0) set_error(a.err, 1u);
+    n = n < 0 ? 0 : a.T;
   }
-  const int hi = min(tok_end, n);
-  if (tok_begin >= hi) return;
-  const int ngroups = d_c / 32;
-  const int lane = threadIdx.x & 63;
-  const int c = lane & 31;
-  const int half = (blockIdx.x * blockDim.x + threadIdx.x) >> 5;  // global half-wave id
-  const int nhalves = (gridDim.x * blockDim.x) >> 5;
-  const size_t unit = size_t(s) * H_kv + g;
-  const typename E::T* Ku = K + unit * size_t(T) * d;
-  const int items = (hi - tok_begin) * ngroups;
-  for (int it = half; it < items; it += nhalves) {
-    const int j = tok_begin + it / ngroups, grp = it % ngroups;
-    int ch = channels[g * d_c + grp * 32 + c];
-    if (ch < 0 || ch >= d) {  // caller-supplied channel id out of range
-      set_error(err, 32u);
-      ch = 0;
+  const int hi = min(a.tok_end, n);
+  const int i = a.tok_begin / a.B + int(blockIdx.x);
+  const int r0 = i * a.B;
+  if (r0 >= hi) return;  // block past the valid end of the range
+  const int r1 = min(r0 + a.B, n);
+  const size_t unit = size_t(s) * a.H_kv + g;
+  const int rb = a.d * es;  // bytes per K row (multiple of 16)
+  const int cpr = rb / 16;
+  const int wpr = rb / 4;
+  const int tsw = wpr + 1;  // words per staged row (one word of padding)
+  const int R = a.rows_per_pass;
+  const size_t S = size_t(a.tok_end - a.tok_begin);
+
+  uint8_t* tile = reinterpret_cast<uint8_t*>(smem4);
+  uint32_t* t32 = reinterpret_cast<uint32_t*>(smem4);
+  float* part = reinterpret_cast<float*>(tile + size_t(R) * tsw * 4);  // [nph][wpr * EPW][2]
+  const int nph = wpr <= kIdxThreads / 2 ? kIdxThreads / wpr : 1;
+  int* s_ch = reinterpret_cast<int*>(part + (nph > 1 ? nph * wpr * EPW * 2 : 0));
+
+  const bool do_block = a.flags & kIdxBlock, do_token = a.flags & kIdxToken;
+  if (do_token) {
+    for (int c = tid; c < a.d_c; c += kIdxThreads) {
+      int ch = a.channels[g * a.d_c + c];
+      if (ch < 0 || ch >= a.d) {  // caller-supplied channel id out of range: read channel 0
+        set_error(a.err, 32u);
+        ch = 0;
+      }
+      s_ch[c] = ch;
     }
-    const float x = E::to_f(Ku[size_t(j) * d + ch]);
-    float mn = x, mx = x;
+  }
+  // V write-back of the prefill rows of this block
+  if (a.v_src) copy_v_rows(a, s, g, unit, max(r0, a.tok_begin), min(r1, a.tok_end), es);
+
+  // running block max/min: thread owns word w = tid % wpr of rows ph, ph + nph, ...
+  // (nph > 1), or words tid, tid + 256, ... of every row (nph == 1)
+  const int ph = tid / wpr, w0 = tid % wpr;
+  float mx[kIdxMaxWords][EPW], mn[kIdxMaxWords][EPW];
 #pragma unroll
-    for (int o = 16; o > 0; o >>= 1) {
-      mn = fminf(mn, __shfl_xor(mn, o, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  for (int k = 0; k < kIdxMaxWords; ++k)
+#pragma unroll
+    for (int e = 0; e < EPW; ++e) {
+      mx[k][e] = -__builtin_inff();
+      mn[k][e] = __builtin_inff();
     }
-    const float scale = (mx - mn) / 15.0f;  // IEEE float32 subtract and divide
-    uint32_t code = 0;
-    if (scale != 0.0f) {
-      float v = __builtin_rintf((x - mn) / scale);  // round half to even
-      v = fminf(fmaxf(v, 0.0f), 15.0f);
-      code = uint32_t(v);
+
+  const int ngroups = a.d_c / 32;
+  for (int pr0 = r0; pr0 < r1; pr0 += R) {
+    const int nrows = min(R, r1 - pr0);
+    if (pr0 != r0) __syncthreads();  // previous pass done with the tile
+    // ---- stage rows [pr0, pr0 + nrows) ----
+    const int nch = nrows * cpr;
+    for (int base = 0; base < nch; base += kIdxThreads * kIdxLoadUnroll) {
+      uint4 x[kIdxLoadUnroll];
+      bool fresh[kIdxLoadUnroll];
+#pragma unroll
+      for (int u = 0; u < kIdxLoadUnroll; ++u) {
+        const int idx = base + u * kIdxThreads + tid;
+        fresh[u] = false;
+        if (idx < nch) {
+          const int r = pr0 + idx / cpr, cc = idx % cpr;
+          fresh[u] = a.k_src && r >= a.tok_begin && r < a.tok_end;
+          const uint8_t* src = fresh[u] ? a.k_src + ((size_t(s) * S + (r - a.tok_begin)) * a.H_kv + g) * rb
+                                        : a.k + (unit * a.T + r) * rb;
+          x[u] = ld16(src + cc * 16);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kIdxLoadUnroll; ++u) {
+        const int idx = base + u * kIdxThreads + tid;
+        if (idx < nch) {
+          const int rr = idx / cpr, cc = idx % cpr;
+          uint32_t* dst = t32 + rr * tsw + cc * 4;
+          dst[0] = x[u].x;
+          dst[1] = x[u].y;
+          dst[2] = x[u].z;
+          dst[3] = x[u].w;
+          if (fresh[u]) *reinterpret_cast<uint4*>(a.k + (unit * a.T + pr0 + rr) * rb + cc * 16) = x[u];
+        }
+      }
     }
-    const uint32_t nxt = __shfl_down(code, 1, 64);
-    const size_t row = unit * size_t(T) + j;
-    if ((c & 1) == 0) codes[row * (d_c / 2) + grp * 16 + (c >> 1)] = uint8_t(code | (nxt << 4));
-    if (c == 0) {
-      qparams[(row * ngroups + grp) * 2 + 0] = scale;
-      qparams[(row * ngroups + grp) * 2 + 1] = mn + 0.0f;
+    __syncthreads();
+
+    // ---- block summary: fold the staged rows into the running max/min ----
+    if (do_block) {
+      if (nph > 1) {
+        if (ph < nph) {
+          for (int rr = ph; rr < nrows; rr += nph) {
+            const uint32_t word = t32[rr * tsw + w0];
+#pragma unroll
+            for (int e = 0; e < EPW; ++e) {
+              const float x = EPW == 2 ? (e == 0 ? bf16_lo(word) : bf16_hi(word)) : __uint_as_float(word);
+              mx[0][e] = fmaxf(mx[0][e], x);
+              mn[0][e] = fminf(mn[0][e], x);
+            }
+          }
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < kIdxMaxWords; ++k) {
+          const int w = tid + k * kIdxThreads;
+          if (w < wpr) {
+            for (int rr = 0; rr < nrows; ++rr) {
+              const uint32_t word = t32[rr * tsw + w];
+#pragma unroll
+              for (int e = 0; e < EPW; ++e) {
+                const float x = EPW == 2 ? (e == 0 ? bf16_lo(word) : bf16_hi(word)) : __uint_as_float(word);
+                mx[k][e] = fmaxf(mx[k][e], x);
+                mn[k][e] = fminf(mn[k][e], x);
+              }
+            }
+          }
+        }
+      }
+    }
+
+    // ---- token index of the staged rows inside [tok_begin, hi) ----
+    if (do_token) {
+      const int lo = max(pr0, a.tok_begin) - pr0, up = min(pr0 + nrows, hi) - pr0;
+      for (int k = tid; k < 64 * ngroups; k += kIdxThreads) {
+        const int rr = k & 63, grp = k >> 6;  // lane = row of the pass, wave-uniform group
+        if (rr < lo || rr >= up) continue;
+        const typename E::T* rowp = reinterpret_cast<const typename E::T*>(t32 + rr * tsw);
+        const int* chs = s_ch + grp * 32;
+        float lo_v = __builtin_inff(), hi_v = -__builtin_inff();
+#pragma unroll 8
+        for (int j = 0; j < 32; ++j) {
+          const float x = E::to_f(rowp[chs[j]]);
+          lo_v = fminf(lo_v, x);
+          hi_v = fmaxf(hi_v, x);
+        }
+        const float scale = (hi_v - lo_v) / 15.0f;  // IEEE float32 subtract and divide
+        uint32_t w[4] = {0u, 0u, 0u, 0u};
+        if (scale != 0.0f) {
+          const float rcp = __builtin_amdgcn_rcpf(scale);
+          uint32_t near = 0;  // channels whose product lies near a rounding boundary
+#pragma unroll 1
+          for (int wi = 0; wi < 4; ++wi) {  // eight channels per 32-bit word of codes
+            uint32_t acc = 0;
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj) {
+              const float q = (E::to_f(rowp[chs[wi * 8 + jj]]) - lo_v) * rcp;
+              near |= uint32_t(!(fabsf(__builtin_amdgcn_fractf(q) - 0.5f) > kNearHalf && q < 16.0f)) << (wi * 8 + jj);
+              // round half to even, clamp; channel 2k in the low nibble of byte k
+              acc |= uint32_t(fminf(fmaxf(__builtin_rintf(q), 0.0f), 15.0f)) << (4 * jj);
+            }
+            w[0] = wi == 0 ? acc : w[0];
+            w[1] = wi == 1 ? acc : w[1];
+            w[2] = wi == 2 ? acc : w[2];
+            w[3] = wi == 3 ? acc : w[3];
+          }
+          // rare: recompute those codes from the IEEE quotient
+          for (; near != 0; near &= near - 1) {
+            const int j = __builtin_ctz(near);
+            const float q = fminf(fmaxf(__builtin_rintf((E::to_f(rowp[chs[j]]) - lo_v) / scale), 0.0f), 15.0f);
+            const int sh = 4 * (j & 7);
+            const uint32_t keep = ~(0xFu << sh), code = uint32_t(q) << sh;
+            switch (j >> 3) {
+              case 0: w[0] = (w[0] & keep) | code; break;
+              case 1: w[1] = (w[1] & keep) | code; break;
+              case 2: w[2] = (w[2] & keep) | code; break;
+              default: w[3] = (w[3] & keep) | code; break;
+            }
+          }
+        }
+        const size_t trow = unit * size_t(a.T) + (pr0 + rr);
+        *reinterpret_cast<uint4*>(a.codes + trow * (a.d_c / 2) + grp * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+        *reinterpret_cast<float2*>(a.qparams + (trow * ngroups + grp) * 2) = make_float2(scale, lo_v + 0.0f);
+      }
     }
   }
+
+  // ---- block summary: combine the row phases and store ----
+  if (do_block) {
+    uint8_t* pmax = a.kmax + (unit * a.m_max + i) * rb;
+    uint8_t* pmin = a.kmin + (unit * a.m_max + i) * rb;
+    if (nph > 1) {
+      if (ph < nph)
+#pragma unroll
+        for (int e = 0; e < EPW; ++e) {
+          part[((ph * wpr + w0) * EPW + e) * 2 + 0] = mx[0][e];
+          part[((ph * wpr + w0) * EPW + e) * 2 + 1] = mn[0][e];
+        }
+      __syncthreads();
+      if (tid < wpr) {
+        float fx[EPW], fn[EPW];
+#pragma unroll
+        for (int e = 0; e < EPW; ++e) {
+          fx[e] = -__builtin_inff();
+          fn[e] = __builtin_inff();
+        }
+        for (int p = 0; p < nph; ++p)
+#pragma unroll
+          for (int e = 0; e < EPW; ++e) {
+            fx[e] = fmaxf(fx[e], part[((p * wpr + tid) * EPW + e) * 2 + 0]);
+            fn[e] = fminf(fn[e], part[((p * wpr + tid) * EPW + e) * 2 + 1]);
+          }
+        // the values are exact copies of inputs; + 0.0f turns -0.0 into +0.0
+        uint32_t wx, wn;
+        if (EPW == 2) {
+          wx = uint32_t(f32_to_bf16(fx[0] + 0.0f)) | (uint32_t(f32_to_bf16(fx[EPW - 1] + 0.0f)) << 16);
+          wn = uint32_t(f32_to_bf16(fn[0] + 0.0f)) | (uint32_t(f32_to_bf16(fn[EPW - 1] + 0.0f)) << 16);
+        } else {
+          wx = __float_as_uint(fx[0] + 0.0f);
+          wn = __float_as_uint(fn[0] + 0.0f);
+        }
+        reinterpret_cast<uint32_t*>(pmax)[tid] = wx;
+        reinterpret_cast<uint32_t*>(pmin)[tid] = wn;
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < kIdxMaxWords; ++k) {
+        const int w = tid + k * kIdxThreads;
+        if (w < wpr) {
+          uint32_t wx, wn;
+          if (EPW == 2) {
+            wx = uint32_t(f32_to_bf16(mx[k][0] + 0.0f)) | (uint32_t(f32_to_bf16(mx[k][EPW - 1] + 0.0f)) << 16);
+            wn = uint32_t(f32_to_bf16(mn[k][0] + 0.0f)) | (uint32_t(f32_to_bf16(mn[k][EPW - 1] + 0.0f)) << 16);
+          } else {
+            wx = __float_as_uint(mx[k][0] + 0.0f);
+            wn = __float_as_uint(mn[k][0] + 0.0f);
+          }
+          reinterpret_cast<uint32_t*>(pmax)[w] = wx;
+          reinterpret_cast<uint32_t*>(pmin)[w] = wn;
+        }
+      }
+    }
+  }
+}
+
+size_t index_rows_lds_bytes(int rb, int rows_per_pass, int d_c, int es) {
+  const int wpr = rb / 4;
+  const int nph = wpr <= kIdxThreads / 2 ? kIdxThreads / wpr : 1;
+  const size_t part = nph > 1 ? size_t(nph) * wpr * (4 / es) * 2 * sizeof(float) : 0;
+  return size_t(rows_per_pass) * (rb + 4) + part + size_t(d_c) * sizeof(int);
+}
+
+static hipError_t launch_index_rows(const Problem& P, const void* k_src, const void* v_src, void* K, void* V,
+                                    const int32_t* ctx_lens, const int32_t* channels, int tok_begin, int tok_end,
+                                    void* kmax, void* kmin, uint8_t* codes, float* qparams, int flags,
+                                    uint32_t* err, hipStream_t st) {
+  const int es = P.dtype == 1 ? 2 : 4;
+  const int rb = P.d_qk * es;
+  IndexArgs a;
+  a.k_src = (const uint8_t*)k_src;
+  a.v_src = (const uint8_t*)v_src;
+  a.k = (uint8_t*)K;
+  a.v = (uint8_t*)V;
+  a.ctx_lens = ctx_lens;
+  a.channels = channels;
+  a.kmax = (uint8_t*)kmax;
+  a.kmin = (uint8_t*)kmin;
+  a.codes = codes;
+  a.qparams = qparams;
+  a.H_kv = P.H_kv;
+  a.T = P.T;
+  a.d = P.d_qk;
+  a.d_v = P.d_v;
+  a.d_c = P.d_c;
+  a.B = P.B;
+  a.m_max = P.m_max;
+  a.tok_begin = tok_begin;
+  a.tok_end = tok_end;
+  a.rows_per_pass = kIdxTileBytes / (rb + 4) < P.B ? kIdxTileBytes / (rb + 4) : P.B;
+  a.flags = flags;
+  a.err = err;
+  const int nblk = (tok_end + P.B - 1) / P.B - tok_begin / P.B;  // blocks overlapping the range
+  dim3 grid(unsigned(nblk), unsigned(P.H_kv), unsigned(P.b));
+  const size_t lds = index_rows_lds_bytes(rb, a.rows_per_pass, (flags & kIdxToken) ? P.d_c : 0, es);
+  if (P.dtype == 1) index_rows_kernel<BF16><<<grid, kIdxThreads, lds, st>>>(a);
+  else index_rows_kernel<F32><<<grid, kIdxThreads, lds, st>>>(a);
+  return hipGetLastError();
 }
 
 hipError_t launch_block_index(const Problem& P, const void* K, const int32_t* ctx_lens, int tok_begin,
                               int tok_end, void* kmax, void* kmin, uint32_t* err, hipStream_t st) {
-  const int B = P.B, d = P.d_qk;
-  const int span_blocks = (tok_end - tok_begin + B - 1) / B + 1;
-  const int cpb = d / (P.dtype == 1 ? 8 : 4);
-  int gx = (span_blocks * cpb + 255) / 256;
-  gx = gx < 1 ? 1 : (gx > 4096 ? 4096 : gx);
-  dim3 grid(gx, P.H_kv, P.b);
-  if (P.dtype == 1)
-    block_index_kernel<BF16><<<grid, 256, 0, st>>>((const uint16_t*)K, ctx_lens, P.H_kv, P.T, d, B,
-                                                   P.m_max, tok_begin, tok_end, (uint16_t*)kmax,
-                                                   (uint16_t*)kmin, err);
-  else
-    block_index_kernel<F32><<<grid, 256, 0, st>>>((const float*)K, ctx_lens, P.H_kv, P.T, d, B, P.m_max,
-                                                  tok_begin, tok_end, (float*)kmax, (float*)kmin, err);
-  return hipGetLastError();
+  return launch_index_rows(P, nullptr, nullptr, const_cast<void*>(K), nullptr, ctx_lens, nullptr, tok_begin,
+                           tok_end, kmax, kmin, nullptr, nullptr, kIdxBlock, err, st);
 }
 
 hipError_t launch_token_index(const Problem& P, const void* K, const int32_t* ctx_lens,
                               const int32_t* channels, int tok_begin, int tok_end, uint8_t* codes,
                               float* qparams, uint32_t* err, hipStream_t st) {
-  const int ngroups = P.d_c / 32;
-  const long items = long(tok_end - tok_begin) * ngroups;  // half-waves of work
-  long gx = (items + 7) / 8;                                // 8 half-waves per 256-thread group
-  gx = gx < 1 ? 1 : (gx > 8192 ? 8192 : gx);
-  dim3 grid(unsigned(gx), P.H_kv, P.b);
-  if (P.dtype == 1)
-    token_index_kernel<BF16><<<grid, 256, 0, st>>>((const uint16_t*)K, ctx_lens, channels, P.H_kv, P.T,
-                                                   P.d_qk, P.d_c, tok_begin, tok_end, codes, qparams, err);
-  else
-    token_index_kernel<F32><<<grid, 256, 0, st>>>((const float*)K, ctx_lens, channels, P.H_kv, P.T,
-                                                  P.d_qk, P.d_c, tok_begin, tok_end, codes, qparams, err);
-  return hipGetLastError();
+  return launch_index_rows(P, nullptr, nullptr, const_cast<void*>(K), nullptr, ctx_lens, channels, tok_begin,
+                           tok_end, nullptr, nullptr, codes, qparams, kIdxToken, err, st);
+}
+
+hipError_t launch_prefill_kv(const Problem& P, const void* k_src, const void* v_src, const int32_t* ctx_lens,
+                             const int32_t* channels, int tok_begin, int tok_end, void* K, void* V, void* kmax,
+                             void* kmin, uint8_t* codes, float* qparams, uint32_t* err, hipStream_t st) {
+  return launch_index_rows(P, k_src, v_src, K, V, ctx_lens, channels, tok_begin, tok_end, kmax, kmin, codes,
+                           qparams, kIdxBlock | kIdxToken, err, st);
 }
 
 }  // namespace tls

@@ -36,6 +36,11 @@ hipError_t launch_block_index(const Problem& P, const void* K, const int32_t* ct
 hipError_t launch_token_index(const Problem& P, const void* K, const int32_t* ctx_lens,
                               const int32_t* channels, int tok_begin, int tok_end, uint8_t* codes,
                               float* qparams, uint32_t* err, hipStream_t st);
+// Prefill write-back of the K/V rows [tok_begin, tok_end) fused with both
+// index builds over the same range (one read of every touched block).
+hipError_t launch_prefill_kv(const Problem& P, const void* k_src, const void* v_src, const int32_t* ctx_lens,
+                             const int32_t* channels, int tok_begin, int tok_end, void* K, void* V, void* kmax,
+                             void* kmin, uint8_t* codes, float* qparams, uint32_t* err, hipStream_t st);
 
 hipError_t launch_block_score(const Problem& P, const void* q, const void* kmax, const void* kmin,
                               const int32_t* ctx_lens, float* qpn, float* scores, uint32_t* err, hipStream_t st);
@@ -114,5 +119,12 @@ hipError_t launch_prefetch(const Problem& P, const void* host_k, const void* hos
                            void* pool_k, void* pool_v, int64_t n_slots, int32_t* slot_map,
                            int32_t* slot_owner, int32_t* transfer_count, int32_t* transfer_list,
                            uint32_t* err, hipStream_t st);
+hipError_t launch_init_residency(const Problem& P, const void* src_k, const void* src_v, const int32_t* ctx_lens,
+                                 const int32_t* block_ids, int K_b, void* pool_k, void* pool_v, int64_t n_slots,
+                                 int32_t* slot_map, int32_t* slot_owner, int32_t* transfer_list, uint32_t* err,
+                                 hipStream_t st);
+hipError_t launch_offload_rows(const Problem& P, const void* K, const void* V, const int32_t* ctx_lens,
+                               int tok_begin, int tok_end, void* host_k, void* host_v, uint32_t* err,
+                               hipStream_t st);
 
 }  // namespace tls

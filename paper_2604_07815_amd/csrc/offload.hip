@@ -12,6 +12,12 @@
 //      device-side loads over PCIe (no host round trip for T_t), on a few
 //      work-groups that leave the chip to the overlapping decode step.
 // The copy reads rows [iB, min((i+1)B, ctx_len)) of block i.
+//
+// The prefill side of the tier (Sec. 4.2, Fig. 2) has two more pieces:
+// offload_rows_kernel copies the K/V rows written at prefill from HBM to the
+// pinned host arrays the prefetch later reads, and the initial residency
+// (the blocks chosen by the final prefill query) is the same plan and copy
+// run on an emptied pool, reading the rows from HBM with a full grid.
 #include "kernels.hpp"
 
 namespace tls {
@@ -157,10 +163,12 @@ __global__ __launch_bounds__(kCopyThreads) void prefetch_copy_kernel(
   }
 }
 
-hipError_t launch_prefetch(const Problem& P, const void* host_k, const void* host_v, const int32_t* ctx_lens,
-                           const int32_t* block_ids_new, const int32_t* block_ids_live, int K_b, void* pool_k,
-                           void* pool_v, int64_t n_slots, int32_t* slot_map, int32_t* slot_owner,
-                           int32_t* transfer_count, int32_t* transfer_list, uint32_t* err, hipStream_t st) {
+static hipError_t launch_plan_and_copy(const Problem& P, const void* src_k, const void* src_v,
+                                       const int32_t* ctx_lens, const int32_t* block_ids_new,
+                                       const int32_t* block_ids_live, int K_b, void* pool_k, void* pool_v,
+                                       int64_t n_slots, int32_t* slot_map, int32_t* slot_owner,
+                                       int32_t* transfer_count, int32_t* transfer_list, uint32_t* err, int copy_wgs,
+                                       hipStream_t st) {
   const size_t lds = ((P.m_max + 31) / 32 + 8) * sizeof(uint32_t);
   prefetch_plan_kernel<<<P.units, 256, lds, st>>>(ctx_lens, block_ids_new, block_ids_live, K_b, P.H_kv, P.T, P.B,
                                                   P.m_max, n_slots, slot_map, slot_owner, transfer_count,
@@ -168,10 +176,86 @@ hipError_t launch_prefetch(const Problem& P, const void* host_k, const void* hos
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int es = P.dtype == 1 ? 2 : 4;
-  const int wgs = P.units < kCopyWGs ? P.units : kCopyWGs;
-  prefetch_copy_kernel<<<wgs, kCopyThreads, 0, st>>>((const uint8_t*)host_k, (const uint8_t*)host_v, ctx_lens,
+  const int wgs = P.units < copy_wgs ? P.units : copy_wgs;
+  prefetch_copy_kernel<<<wgs, kCopyThreads, 0, st>>>((const uint8_t*)src_k, (const uint8_t*)src_v, ctx_lens,
                                                      transfer_list, P.units, K_b, P.H_kv, P.T, P.B, P.d_qk * es,
                                                      P.d_v * es, n_slots, (uint8_t*)pool_k, (uint8_t*)pool_v);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefetch(const Problem& P, const void* host_k, const void* host_v, const int32_t* ctx_lens,
+                           const int32_t* block_ids_new, const int32_t* block_ids_live, int K_b, void* pool_k,
+                           void* pool_v, int64_t n_slots, int32_t* slot_map, int32_t* slot_owner,
+                           int32_t* transfer_count, int32_t* transfer_list, uint32_t* err, hipStream_t st) {
+  return launch_plan_and_copy(P, host_k, host_v, ctx_lens, block_ids_new, block_ids_live, K_b, pool_k, pool_v,
+                              n_slots, slot_map, slot_owner, transfer_count, transfer_list, err, kCopyWGs, st);
+}
+
+hipError_t launch_init_residency(const Problem& P, const void* src_k, const void* src_v, const int32_t* ctx_lens,
+                                 const int32_t* block_ids, int K_b, void* pool_k, void* pool_v, int64_t n_slots,
+                                 int32_t* slot_map, int32_t* slot_owner, int32_t* transfer_list, uint32_t* err,
+                                 hipStream_t st) {
+  // empty pool: every block unmapped, every slot free
+  hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(slot_map), 0xffffffffu, size_t(P.units) * P.m_max, st);
+  if (e == hipSuccess)
+    e = launch_fill_u32(reinterpret_cast<uint32_t*>(slot_owner), 0xffffffffu, size_t(P.units) * n_slots, st);
+  if (e != hipSuccess) return e;
+  // one copy work-group per unit: nothing runs beside it
+  return launch_plan_and_copy(P, src_k, src_v, ctx_lens, block_ids, nullptr, K_b, pool_k, pool_v, n_slots,
+                              slot_map, slot_owner, nullptr, transfer_list, err, P.units, st);
+}
+
+// Device -> pinned host copy of the rows [tok_begin, min(tok_end, ctx_len))
+// of every unit (K, and V unless it aliases K).  In the dense layouts those
+// rows are one contiguous byte range per unit on both sides.  Work-group w
+// copies units w, w + gridDim.x, ...; a few work-groups keep enough stores in
+// flight for the link and leave the rest of the chip to other work.
+constexpr int kOffloadWGs = 64;
+
+__device__ inline void copy_span(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, size_t bytes) {
+  constexpr size_t step = size_t(kCopyPieces) * kCopyThreads * 16;
+  for (size_t base = 0; base < bytes; base += step) {
+    uint4 v[kCopyPieces];
+#pragma unroll
+    for (int i = 0; i < kCopyPieces; ++i) {
+      const size_t o = base + (size_t(i) * kCopyThreads + threadIdx.x) * 16;
+      if (o < bytes) v[i] = ld16_stream(src + o);
+    }
+#pragma unroll
+    for (int i = 0; i < kCopyPieces; ++i) {
+      const size_t o = base + (size_t(i) * kCopyThreads + threadIdx.x) * 16;
+      if (o < bytes) *reinterpret_cast<uint4*>(dst + o) = v[i];
+    }
+  }
+}
+
+__global__ __launch_bounds__(kCopyThreads) void offload_rows_kernel(
+    const uint8_t* __restrict__ k, const uint8_t* __restrict__ v, const int32_t* __restrict__ ctx_lens, int units,
+    int H_kv, int T, int tok_begin, int tok_end, int row_k, int row_v, uint8_t* __restrict__ host_k,
+    uint8_t* __restrict__ host_v, uint32_t* err) {
+  for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
+    int n = ctx_lens[unit / H_kv];
+    if (n < 0 || n > T) {
+      if (threadIdx.x == 0 && unit % H_kv == 0) set_error(err, 1u);
+      n = n < 0 ? 0 : T;
+    }
+    const int hi = min(tok_end, n);
+    if (hi <= tok_begin) continue;
+    const size_t rows = size_t(hi - tok_begin);
+    const size_t first = size_t(unit) * T + tok_begin;
+    copy_span(k + first * row_k, host_k + first * row_k, rows * row_k);
+    if (v) copy_span(v + first * row_v, host_v + first * row_v, rows * row_v);
+  }
+}
+
+hipError_t launch_offload_rows(const Problem& P, const void* K, const void* V, const int32_t* ctx_lens,
+                               int tok_begin, int tok_end, void* host_k, void* host_v, uint32_t* err,
+                               hipStream_t st) {
+  const int es = P.dtype == 1 ? 2 : 4;
+  const int wgs = P.units < kOffloadWGs ? P.units : kOffloadWGs;
+  offload_rows_kernel<<<wgs, kCopyThreads, 0, st>>>((const uint8_t*)K, (const uint8_t*)V, ctx_lens, P.units,
+                                                    P.H_kv, P.T, tok_begin, tok_end, P.d_qk * es, P.d_v * es,
+                                                    (uint8_t*)host_k, (uint8_t*)host_v, err);
   return hipGetLastError();
 }
 

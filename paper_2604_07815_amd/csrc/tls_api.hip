@@ -53,6 +53,32 @@ tls_status make_problem(const tls_layout* L, Problem* P) {
   return TLS_OK;
 }
 
+// Device address of caller-owned pinned host memory (hipHostMalloc or
+// registered); false for pageable host memory or device memory.
+bool pinned_device_ptr(const void* p, const void** out) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess || a.type != hipMemoryTypeHost || !a.devicePointer) {
+    (void)hipGetLastError();
+    return false;
+  }
+  *out = static_cast<const char*>(a.devicePointer) + (static_cast<const char*>(p) - static_cast<const char*>(a.hostPointer));
+  return true;
+}
+
+// Device address of either device memory or pinned host memory.
+bool readable_ptr(const void* p, const void** out) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  if (a.type == hipMemoryTypeDevice) {
+    *out = p;
+    return true;
+  }
+  return pinned_device_ptr(p, out);
+}
+
 tls_status check_budgets(const Problem& P, int K_b, int K_t) {
   if (K_b < 1 || K_t < 1) return TLS_ERR_INVALID_ARGUMENT;
   if (long(K_b) * P.B > tls::kMaxKeys) return TLS_ERR_UNSUPPORTED;
@@ -161,6 +187,56 @@ tls_status tls_build_token_index(const tls_layout* layout, const void* K, const 
   if (tok_end == tok_begin) return TLS_OK;
   return hip_status(
       tls::launch_token_index(P, K, ctx_lens, channels, tok_begin, tok_end, codes, qparams, nullptr, stream));
+}
+
+tls_status tls_prefill_kv(const tls_layout* layout, const void* k_src, const void* v_src, const int32_t* ctx_lens,
+                          const int32_t* channels, int32_t tok_begin, int32_t tok_end, void* K, void* V, void* kmax,
+                          void* kmin, uint8_t* codes, float* qparams, hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!k_src || !ctx_lens || !channels || !K || !kmax || !kmin || !codes || !qparams) return TLS_ERR_INVALID_ARGUMENT;
+  if (P.mla ? (v_src != nullptr || V != nullptr) : (!v_src || !V)) return TLS_ERR_INVALID_ARGUMENT;
+  if (tok_begin < 0 || tok_end < tok_begin || tok_end > P.T) return TLS_ERR_INVALID_ARGUMENT;
+  if (tok_end == tok_begin) return TLS_OK;
+  return hip_status(tls::launch_prefill_kv(P, k_src, v_src, ctx_lens, channels, tok_begin, tok_end, K, V, kmax, kmin,
+                                           codes, qparams, nullptr, stream));
+}
+
+tls_status tls_offload_kv(const tls_layout* layout, const void* K, const void* V, const int32_t* ctx_lens,
+                          int32_t tok_begin, int32_t tok_end, void* host_k, void* host_v, hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!K || !ctx_lens || !host_k) return TLS_ERR_INVALID_ARGUMENT;
+  if (P.mla ? (V != nullptr || host_v != nullptr) : (!V || !host_v)) return TLS_ERR_INVALID_ARGUMENT;
+  if (tok_begin < 0 || tok_end < tok_begin || tok_end > P.T) return TLS_ERR_INVALID_ARGUMENT;
+  const void* dk = nullptr;
+  const void* dv = nullptr;
+  if (!pinned_device_ptr(host_k, &dk) || (host_v && !pinned_device_ptr(host_v, &dv))) return TLS_ERR_INVALID_ARGUMENT;
+  if (tok_end == tok_begin) return TLS_OK;
+  return hip_status(tls::launch_offload_rows(P, K, V, ctx_lens, tok_begin, tok_end, const_cast<void*>(dk),
+                                             const_cast<void*>(dv), nullptr, stream));
+}
+
+tls_status tls_init_residency(const tls_layout* layout, const void* src_k, const void* src_v, const int32_t* ctx_lens,
+                              const int32_t* block_ids, int32_t K_b, void* pool_k, void* pool_v, int64_t n_slots,
+                              int32_t* slot_map, int32_t* slot_owner, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!src_k || !ctx_lens || !block_ids || !pool_k || !slot_map || !slot_owner || !ws) return TLS_ERR_INVALID_ARGUMENT;
+  if (P.mla ? (src_v != nullptr || pool_v != nullptr) : (!src_v || !pool_v)) return TLS_ERR_INVALID_ARGUMENT;
+  st = check_budgets(P, K_b, 1);
+  if (st != TLS_OK) return st;
+  if (n_slots < int64_t(K_b) || n_slots > (int64_t(1) << 30)) return TLS_ERR_INVALID_ARGUMENT;
+  const void* dk = nullptr;
+  const void* dv = nullptr;
+  if (!readable_ptr(src_k, &dk) || (src_v && !readable_ptr(src_v, &dv))) return TLS_ERR_INVALID_ARGUMENT;
+  const tls::Workspace W = tls::plan_workspace(P, K_b, 1);
+  if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  return hip_status(tls::launch_init_residency(P, dk, dv, ctx_lens, block_ids, K_b, pool_k, pool_v, n_slots, slot_map,
+                                               slot_owner, at<int32_t>(ws, W.xfer), err_word(ws), stream));
 }
 
 tls_status tls_select_blocks(const tls_layout* layout, const void* q, const void* kmax, const void* kmin,
@@ -434,21 +510,7 @@ tls_status tls_prefetch_blocks(const tls_layout* layout, const void* host_k, con
   // host K/V must be pinned (device-accessible) host memory
   const void* dk = nullptr;
   const void* dv = nullptr;
-  {
-    hipPointerAttribute_t a;
-    if (hipPointerGetAttributes(&a, host_k) != hipSuccess || a.type != hipMemoryTypeHost || !a.devicePointer) {
-      (void)hipGetLastError();
-      return TLS_ERR_INVALID_ARGUMENT;
-    }
-    dk = static_cast<const char*>(a.devicePointer) + (static_cast<const char*>(host_k) - static_cast<const char*>(a.hostPointer));
-    if (host_v) {
-      if (hipPointerGetAttributes(&a, host_v) != hipSuccess || a.type != hipMemoryTypeHost || !a.devicePointer) {
-        (void)hipGetLastError();
-        return TLS_ERR_INVALID_ARGUMENT;
-      }
-      dv = static_cast<const char*>(a.devicePointer) + (static_cast<const char*>(host_v) - static_cast<const char*>(a.hostPointer));
-    }
-  }
+  if (!pinned_device_ptr(host_k, &dk) || (host_v && !pinned_device_ptr(host_v, &dv))) return TLS_ERR_INVALID_ARGUMENT;
   const tls::Workspace W = tls::plan_workspace(P, K_b, 1);
   if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
   int32_t* xfer = at<int32_t>(ws, W.xfer);

@@ -30,7 +30,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ["tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
-              "tls_sparse_decode", "tls_prefetch_blocks", "tls_workspace_size", "tls_check_device_error"]:
+              "tls_sparse_decode", "tls_prefetch_blocks", "tls_workspace_size", "tls_check_device_error",
+              "tls_prefill_kv", "tls_offload_kv", "tls_init_residency"]:
         assert n in names, n
 
 
@@ -123,6 +124,38 @@ def test_null_pointers_are_rejected_before_launch(tls):
     st = lib.tls_prefetch_blocks(ctypes.byref(L), dummy, dummy, dummy, dummy, dummy, 8, dummy, dummy, 10,
                                  dummy, dummy, null, dummy, 1 << 40, null)
     assert st == 1
+
+
+def test_prefill_calls_are_validated_before_launch(tls):
+    """The prefill-side entry points reject bad arguments on the host (none of
+    these calls reaches the device)."""
+    lib = _raw(tls)
+    L = _layout(tls)
+    Lm = _layout(tls, num_kv_heads=1, head_dim_qk=576, head_dim_v=512, index_channels=128, mla_shared_kv=True)
+    d = ctypes.c_void_p(0x1000)
+    null = None
+    ok_args = [d, d, d, d, 0, 64, d, d, d, d, d, d]
+    assert lib.tls_prefill_kv(ctypes.byref(L), *([null] + ok_args[1:]), null) == 1   # no k_src
+    assert lib.tls_prefill_kv(ctypes.byref(L), *(ok_args[:1] + [null] + ok_args[2:]), null) == 1  # GQA without v_src
+    bad_range = list(ok_args)
+    bad_range[4], bad_range[5] = 100, 50
+    assert lib.tls_prefill_kv(ctypes.byref(L), *bad_range, null) == 1                # tok_end < tok_begin
+    bad_range[4], bad_range[5] = 0, 4097
+    assert lib.tls_prefill_kv(ctypes.byref(L), *bad_range, null) == 1                # past max_ctx
+    assert lib.tls_prefill_kv(ctypes.byref(Lm), *ok_args, null) == 1                 # MLA passes no V
+    # an empty range is a no-op that succeeds without touching anything
+    empty = list(ok_args)
+    empty[4] = empty[5] = 64
+    assert lib.tls_prefill_kv(ctypes.byref(L), *empty, null) == 0
+    # offload: host arrays must be pinned host memory (a device-looking pointer is not)
+    assert lib.tls_offload_kv(ctypes.byref(L), d, d, d, 0, 64, null, d, null) == 1
+    assert lib.tls_offload_kv(ctypes.byref(L), d, null, d, 0, 64, d, d, null) == 1
+    assert lib.tls_offload_kv(ctypes.byref(Lm), d, d, d, 0, 64, d, null, null) == 1
+    # residency: budget, pool size and workspace checks
+    assert lib.tls_init_residency(ctypes.byref(L), d, d, d, d, 0, d, d, 16, d, d, d, 1 << 40, null) == 1
+    assert lib.tls_init_residency(ctypes.byref(L), d, d, d, d, 8, d, d, 4, d, d, d, 1 << 40, null) == 1
+    assert lib.tls_init_residency(ctypes.byref(L), d, d, d, d, 8, d, d, 16, d, d, null, 1 << 40, null) == 1
+    assert lib.tls_init_residency(ctypes.byref(Lm), d, d, d, d, 8, d, d, 16, d, d, d, 1 << 40, null) == 1
 
 
 def test_decode_modes_are_validated_before_launch(tls):
