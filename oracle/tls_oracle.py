@@ -176,6 +176,41 @@ def dequantize(packed: np.ndarray, qparams: np.ndarray) -> np.ndarray:
 
 
 # ----------------------------------------------------------------------------
+# Channel set C (Sec. 4.1, "Fine-grained Token Selection": the importance of
+# each channel over a held-out calibration set, then the top-d_c channels)
+# ----------------------------------------------------------------------------
+
+def channel_absmax(x: np.ndarray) -> np.ndarray:
+    """max over the calibration rows of |x|, per (head, channel).
+
+    x: [N][H][d] (token-major activations).  An empty set gives zeros (the
+    identity of a maximum of absolute values)."""
+    x = np.abs(np.asarray(x, dtype=np.float64))
+    if x.shape[0] == 0:
+        return np.zeros(x.shape[1:], dtype=np.float64)
+    return x.max(axis=0)
+
+
+def channel_importance(q_absmax_group: np.ndarray, k_absmax: np.ndarray) -> np.ndarray:
+    """s_i = (1/G) sum_h max|q_h[i]| * max|k[i]| over the G query heads that
+    share the key (q_absmax_group [G][d], k_absmax [d])."""
+    G = q_absmax_group.shape[0]
+    return (q_absmax_group * k_absmax[None, :]).sum(axis=0) / G
+
+
+def calibrate_channels(q_cal: np.ndarray, k_cal: np.ndarray, G: int, d_c: int):
+    """C per KV head: the d_c channels of highest importance (ties -> lower
+    channel), ascending.  q_cal [N][H_q][d], k_cal [N][H_kv][d].
+
+    Returns (channels [H_kv][d_c], scores [H_kv][d], q_absmax, k_absmax)."""
+    qa, ka = channel_absmax(q_cal), channel_absmax(k_cal)
+    H_kv = ka.shape[0]
+    scores = np.stack([channel_importance(qa[g * G:(g + 1) * G], ka[g]) for g in range(H_kv)])
+    chans = np.stack([topk_ascending(scores[g], d_c) for g in range(H_kv)])
+    return chans, scores, qa, ka
+
+
+# ----------------------------------------------------------------------------
 # Token selection inside the selected blocks (Sec. 4.1)
 # ----------------------------------------------------------------------------
 

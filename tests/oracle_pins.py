@@ -353,9 +353,80 @@ def pin_lagged_schedule():
         assert prev is not None
 
 
+# --- channel calibration (Sec. 4.1) -------------------------------------------
+
+def pin_calibration_golden():
+    """Hand-derived worked example, including a tie at the cut."""
+    g = _golden("calibration_worked.json")
+    q, k = np.asarray(g["q_cal"], float), np.asarray(g["k_cal"], float)
+    for d_c, want in g["channels"].items():
+        ch, sc, qa, ka = O.calibrate_channels(q, k, g["G"], int(d_c))
+        np.testing.assert_array_equal(qa, g["q_absmax"])
+        np.testing.assert_array_equal(ka, g["k_absmax"])
+        np.testing.assert_array_equal(sc, g["scores"])
+        np.testing.assert_array_equal(ch, want)
+
+
+def pin_calibration_properties(seed=17):
+    """Planted outlier channels are found; the result does not depend on the
+    order or signs of the calibration rows and scales with the activations;
+    every score bounds the per-channel logit magnitude of every calibration
+    row; a channel no key uses is never chosen; an empty set gives zeros."""
+    r = np.random.default_rng(seed)
+    N, H_kv, G, d, d_c = 300, 2, 4, 64, 16
+    q = r.standard_normal((N, H_kv * G, d))
+    k = r.standard_normal((N, H_kv, d))
+    planted = [np.sort(r.choice(d, size=8, replace=False)) for _ in range(H_kv)]
+    for g in range(H_kv):
+        q[:, g * G:(g + 1) * G, planted[g]] *= 10.0
+        k[:, g, planted[g]] *= 10.0
+    ch, sc, qa, ka = O.calibrate_channels(q, k, G, d_c)
+    for g in range(H_kv):
+        assert set(planted[g].tolist()) <= set(ch[g].tolist())
+        assert np.all(np.diff(ch[g]) > 0) and len(ch[g]) == d_c
+    # order and signs of the rows do not matter
+    perm = r.permutation(N)
+    flip_q = np.where(r.random(q.shape) < 0.5, -1.0, 1.0)
+    flip_k = np.where(r.random(k.shape) < 0.5, -1.0, 1.0)
+    ch2, sc2, _, _ = O.calibrate_channels((q * flip_q)[perm], (k * flip_k)[perm], G, d_c)
+    np.testing.assert_array_equal(ch2, ch)
+    np.testing.assert_array_equal(sc2, sc)
+    # scaling q by 4 and k by 0.5 (exact in binary) scales the scores by 2
+    ch3, sc3, _, _ = O.calibrate_channels(4.0 * q, 0.5 * k, G, d_c)
+    np.testing.assert_array_equal(ch3, ch)
+    np.testing.assert_array_equal(sc3, 2.0 * sc)
+    # the score bounds every row's per-channel logit mass: G s_i >= sum_h |q_h[i] k[i]|
+    for g in range(H_kv):
+        mass = np.abs(q[:, g * G:(g + 1) * G, :] * k[:, g:g + 1, :]).sum(axis=1)  # [N][d]
+        assert np.all(mass <= G * sc[g][None, :] * (1 + 1e-12))
+    # equality when one row holds every maximum: append that row
+    row_q = np.abs(q).max(axis=0, keepdims=True)
+    row_k = np.abs(k).max(axis=0, keepdims=True)
+    _, sc4, _, _ = O.calibrate_channels(np.concatenate([q, row_q]), np.concatenate([k, row_k]), G, d_c)
+    for g in range(H_kv):
+        mass = (row_q[0, g * G:(g + 1) * G, :] * row_k[0, g][None, :]).sum(axis=0)
+        np.testing.assert_allclose(G * sc4[g], mass, rtol=1e-15)
+    # heads with identical activations: the score is the plain product of the maxima
+    q_same = np.repeat(q[:, ::G, :], G, axis=1)
+    _, sc5, qa5, ka5 = O.calibrate_channels(q_same, k, G, d_c)
+    for g in range(H_kv):
+        np.testing.assert_allclose(sc5[g], np.abs(q[:, g * G, :]).max(axis=0) * np.abs(k[:, g, :]).max(axis=0),
+                                   rtol=1e-15)
+    # a channel that no key uses scores 0 and is never chosen
+    k0 = k.copy()
+    k0[:, :, 5] = 0.0
+    ch6, sc6, _, _ = O.calibrate_channels(q, k0, G, d_c)
+    assert np.all(sc6[:, 5] == 0.0) and not np.any(ch6 == 5)
+    # empty calibration set: zero scores, ties to the lowest channels
+    ch7, sc7, _, _ = O.calibrate_channels(q[:0], k[:0], G, d_c)
+    assert np.all(sc7 == 0.0)
+    np.testing.assert_array_equal(ch7, np.tile(np.arange(d_c), (H_kv, 1)))
+
+
 ALL_PINS = [
     pin_quest_golden, pin_quest_forms_agree, pin_quest_upper_bound, pin_topk_bruteforce,
     pin_candidates, pin_quant_golden, pin_quant_bound, pin_alpha_golden, pin_alpha_distribution,
     pin_attention_library, pin_attention_closed_form, pin_dense_equivalence,
-    pin_invariants_and_planted, pin_single_level_operators, pin_lagged_schedule,
+    pin_invariants_and_planted, pin_single_level_operators, pin_lagged_schedule, pin_calibration_golden,
+    pin_calibration_properties,
 ]

@@ -74,6 +74,19 @@ def _wrong_candidates(block_ids, n, B):      # ignores the ragged tail
 
 _REAL_ATTN = O.sparse_attention
 
+def _absmax_signed(x):                       # max of x instead of max of |x|
+    x = np.asarray(x, dtype=np.float64)
+    return np.zeros(x.shape[1:]) if x.shape[0] == 0 else x.max(axis=0)
+
+
+def _importance_sum(qa, ka):                 # drops the 1/G
+    return (qa * ka[None, :]).sum(axis=0)
+
+
+def _importance_max_heads(qa, ka):           # max over the heads instead of their mean
+    return (qa * ka[None, :]).max(axis=0)
+
+
 MUTATIONS = [
     ("quest_scores", _swap_max_min),
     ("block_summaries", _floor_blocks),
@@ -85,6 +98,9 @@ MUTATIONS = [
     ("sparse_attention", _attn_no_scale),
     ("sparse_attention", _attn_transposed_values),
     ("candidates", _wrong_candidates),
+    ("channel_absmax", _absmax_signed),
+    ("channel_importance", _importance_sum),
+    ("channel_importance", _importance_max_heads),
 ]
 
 
