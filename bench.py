@@ -279,6 +279,41 @@ def prefill_timing(tls, torch, cfg, layout, d, L, e, reps=3):
     }
 
 
+def calibration_timing(tls, torch, cfg, layout, dev, n_cal=16384, reps=5):
+    """The channel-calibration pass (Sec. 4.1) over n_cal token rows of the
+    workload's head shapes (random activations generated on the GPU; the
+    paper does not state the size of its calibration set): the per-channel
+    maxima over all query and key heads, then the scores and top-d_c
+    channels.  HIP events on the launch stream, median of `reps`."""
+    import numpy as np
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    g = torch.Generator(device=dev).manual_seed(cfg.seed + 950)
+    q = torch.randn((n_cal, cfg.h_q, cfg.d_qk), generator=g, device=dev).to(dt)
+    k = torch.randn((n_cal, cfg.h_kv, cfg.d_qk), generator=g, device=dev).to(dt)
+    qa = torch.empty((cfg.h_q, cfg.d_qk), dtype=torch.float32, device=dev)
+    ka = torch.empty((cfg.h_kv, cfg.d_qk), dtype=torch.float32, device=dev)
+    ch = torch.empty((cfg.h_kv, cfg.d_c), dtype=torch.int32, device=dev)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(f):
+        f()
+        ts = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            a.record()
+            f()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+
+    absmax_ms = timed(lambda: tls.tls_calibrate_absmax(layout, q, k, qa, ka))
+    select_ms = timed(lambda: tls.tls_calibrate_channels(layout, qa, ka, ch))
+    nbytes = n_cal * (cfg.h_q + cfg.h_kv) * cfg.d_qk * q.element_size()
+    return {"n_cal_rows": n_cal, "absmax_ms": round(absmax_ms, 3),
+            "absmax_GBps": round(nbytes / (absmax_ms * 1e-3) / 1e9, 1), "select_us": round(select_ms * 1e3, 1)}
+
+
 def offload_schedule(tls, synth, torch, np):
     """The offloaded KV tier of the 96k workload (Sec. 4.2), as a serving loop:
     K/V of every sequence in pinned host memory, block and token indices and
@@ -557,6 +592,7 @@ def main():
 
     # ---- prefill side (off the per-step clock): index build, fused write-back ----
     prefill = None if args.profile_only else prefill_timing(tls, torch, cfg, layout, d, layers[0], e)
+    calibration = calibration_timing(tls, torch, cfg, layout, dev)
 
     err = tls.tls_check_device_error(ws)
     nb = algorithmic_bytes(cfg, d["ctx_host"], bids.cpu().numpy(), e)
@@ -592,6 +628,7 @@ def main():
         "stage_us": {k: round(float(v) * 1e3, 2) for k, v in zip(STAGES, stage_ms)},
         "stage_marked_step_us": round(marked_ms * 1e3, 2),
         "prefill": prefill,
+        "calibration": calibration,
         "device_error_flags": err,
         "operators": modes or None,
         "roofline": {

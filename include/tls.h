@@ -189,6 +189,31 @@ tls_status tls_build_token_index(const tls_layout* layout, const void* K, const 
                                  const int32_t* channels, int32_t tok_begin, int32_t tok_end,
                                  uint8_t* codes, float* qparams, hipStream_t stream);
 
+/* Channel calibration for the token index, Sec. 4.1: the channel set C of
+ * each KV group is chosen offline from a held-out calibration set by the
+ * importance s_i = (1/G) sum_h max|q_h[i]| * max|k[i]| of every score
+ * dimension i.  This call computes the running maxima: over the n_cal rows
+ * of q_cal [n_cal][H_q][d_qk] and k_cal [n_cal][H_kv][d_qk] (dtype,
+ * token-major as the projections produce them), q_absmax [H_q][d_qk] and
+ * k_absmax [H_kv][d_qk] (float) receive max |x| per (head, channel).
+ * accumulate = 0 starts from zero; accumulate = 1 folds the rows into the
+ * values already held (a calibration set streamed in batches; the arrays
+ * must hold results of earlier calls).  The maxima are exact and do not
+ * depend on batching or launch order.  n_cal = 0 is allowed (q_cal and k_cal
+ * may then be NULL). */
+tls_status tls_calibrate_absmax(const tls_layout* layout, const void* q_cal, const void* k_cal,
+                                int32_t n_cal, float* q_absmax, float* k_absmax, int32_t accumulate,
+                                hipStream_t stream);
+
+/* Channel selection from the maxima of tls_calibrate_absmax (Sec. 4.1): per
+ * KV head g, s_i = (sum over the G heads h of g, in order, of
+ * q_absmax[h][i] * k_absmax[g][i]) / G in float32, then channels[g][:] =
+ * the d_c channels with the highest s_i (ties to the lower channel),
+ * ascending, ready for tls_build_token_index.  scores (nullable)
+ * [H_kv][d_qk] receives every s_i. */
+tls_status tls_calibrate_channels(const tls_layout* layout, const float* q_absmax, const float* k_absmax,
+                                  int32_t* channels, float* scores, hipStream_t stream);
+
 /* Prefill write-back fused with both index builds (the prefill flow of
  * Sec. 4.2 / Fig. 2: the hierarchical indices are built while the prompt's
  * keys are stored).  For every token t in [tok_begin, tok_end) with

@@ -37,7 +37,7 @@ EXPORTED_SYMBOLS = [
     "tls_version", "tls_status_string", "tls_workspace_size", "tls_workspace_init",
     "tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
     "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error", "tls_prefill_kv",
-    "tls_offload_kv", "tls_init_residency",
+    "tls_offload_kv", "tls_init_residency", "tls_calibrate_absmax", "tls_calibrate_channels",
 ]
 
 
@@ -88,6 +88,8 @@ def _load() -> ctypes.CDLL:
                                     P, P, P, P, P, SZ, ctypes.POINTER(DecodeOpts), P]),
         "tls_prefetch_blocks": (I32, [LP, P, P, P, P, P, I32, P, P, I64, P, P, P, P, SZ, P]),
         "tls_offload_kv": (I32, [LP, P, P, P, I32, I32, P, P, P]),
+        "tls_calibrate_absmax": (I32, [LP, P, P, I32, P, P, I32, P]),
+        "tls_calibrate_channels": (I32, [LP, P, P, P, P, P]),
         "tls_init_residency": (I32, [LP, P, P, P, P, I32, P, P, I64, P, P, P, SZ, P]),
         "tls_check_device_error": (I32, [P, SZ, I32, ctypes.POINTER(I32), P]),
     }
@@ -185,6 +187,24 @@ def tls_build_token_index(layout, K, ctx_lens, channels, tok_begin, tok_end, cod
                                       _ptr(channels, "channels"), int(tok_begin), int(tok_end),
                                       _ptr(codes, "codes"), _ptr(qparams, "qparams"), _stream(stream)),
            "tls_build_token_index")
+
+
+def tls_calibrate_absmax(layout, q_cal, k_cal, q_absmax, k_absmax, accumulate: bool = False, stream=None) -> None:
+    """Running max |x| per (head, channel) over calibration rows q_cal [N][H_q][d], k_cal [N][H_kv][d]."""
+    n = 0 if q_cal is None else int(q_cal.shape[0])
+    if k_cal is not None and int(k_cal.shape[0]) != n:
+        raise ValueError("q_cal and k_cal must hold the same number of rows")
+    _check(_lib.tls_calibrate_absmax(ctypes.byref(layout), _ptr(q_cal, "q_cal") if n else None,
+                                     _ptr(k_cal, "k_cal") if n else None, n, _ptr(q_absmax, "q_absmax"),
+                                     _ptr(k_absmax, "k_absmax"), 1 if accumulate else 0, _stream(stream)),
+           "tls_calibrate_absmax")
+
+
+def tls_calibrate_channels(layout, q_absmax, k_absmax, channels, scores=None, stream=None) -> None:
+    """Channel importance and the top-d_c channels per KV head (ascending)."""
+    _check(_lib.tls_calibrate_channels(ctypes.byref(layout), _ptr(q_absmax, "q_absmax"), _ptr(k_absmax, "k_absmax"),
+                                       _ptr(channels, "channels"), _ptr(scores, "scores"), _stream(stream)),
+           "tls_calibrate_channels")
 
 
 def tls_prefill_kv(layout, k_src, v_src, ctx_lens, channels, tok_begin, tok_end, K, V, kmax, kmin, codes,

@@ -114,6 +114,13 @@ hipError_t launch_merge(const Problem& P, const float* po, const float* plse, in
 
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, size_t n, hipStream_t st);
 
+// Channel calibration (token-index channel set): running max |x| per (head,
+// channel) over n token-major rows [n][H][d_qk], merged into `out` (>= 0);
+// then scores and the top-d_c channels per KV head.
+hipError_t launch_calib_absmax(const Problem& P, const void* x, int n, int H, float* out, hipStream_t st);
+hipError_t launch_calib_select(const Problem& P, const float* q_absmax, const float* k_absmax, int32_t* channels,
+                               float* scores, hipStream_t st);
+
 hipError_t launch_prefetch(const Problem& P, const void* host_k, const void* host_v, const int32_t* ctx_lens,
                            const int32_t* block_ids_new, const int32_t* block_ids_live, int K_b,
                            void* pool_k, void* pool_v, int64_t n_slots, int32_t* slot_map,

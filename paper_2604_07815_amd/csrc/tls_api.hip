@@ -239,6 +239,33 @@ tls_status tls_init_residency(const tls_layout* layout, const void* src_k, const
                                                slot_owner, at<int32_t>(ws, W.xfer), err_word(ws), stream));
 }
 
+tls_status tls_calibrate_absmax(const tls_layout* layout, const void* q_cal, const void* k_cal, int32_t n_cal,
+                                float* q_absmax, float* k_absmax, int32_t accumulate, hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (n_cal < 0 || (accumulate != 0 && accumulate != 1) || !q_absmax || !k_absmax) return TLS_ERR_INVALID_ARGUMENT;
+  if (n_cal > 0 && (!q_cal || !k_cal)) return TLS_ERR_INVALID_ARGUMENT;
+  hipError_t e = hipSuccess;
+  if (!accumulate) {
+    e = tls::launch_fill_u32(reinterpret_cast<uint32_t*>(q_absmax), 0u, size_t(P.H_q) * P.d_qk, stream);
+    if (e == hipSuccess)
+      e = tls::launch_fill_u32(reinterpret_cast<uint32_t*>(k_absmax), 0u, size_t(P.H_kv) * P.d_qk, stream);
+  }
+  if (e == hipSuccess) e = tls::launch_calib_absmax(P, q_cal, n_cal, P.H_q, q_absmax, stream);
+  if (e == hipSuccess) e = tls::launch_calib_absmax(P, k_cal, n_cal, P.H_kv, k_absmax, stream);
+  return hip_status(e);
+}
+
+tls_status tls_calibrate_channels(const tls_layout* layout, const float* q_absmax, const float* k_absmax,
+                                  int32_t* channels, float* scores, hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!q_absmax || !k_absmax || !channels) return TLS_ERR_INVALID_ARGUMENT;
+  return hip_status(tls::launch_calib_select(P, q_absmax, k_absmax, channels, scores, stream));
+}
+
 tls_status tls_select_blocks(const tls_layout* layout, const void* q, const void* kmax, const void* kmin,
                              const int32_t* ctx_lens, int32_t K_b, int32_t* block_ids, float* block_scores, void* ws,
                              size_t ws_bytes, hipStream_t stream) {

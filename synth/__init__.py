@@ -164,6 +164,27 @@ def draw_channels(cfg: DecodeConfig) -> np.ndarray:
     return out
 
 
+def draw_calibration(cfg: DecodeConfig, n_cal: int, seed_offset: int = 950):
+    """Seeded calibration activations for the channel-importance pass, in
+    storage form: q [n_cal][h_q][d_qk], k [n_cal][h_kv][d_qk].
+
+    Unlike the decode workloads, channels differ in scale, as in trained
+    models: every (head, channel) has a log-normal scale exp(0.5 z), and each
+    KV head has d_c/4 outlier channels, scaled by 6 in its keys and in the
+    queries of its group.  Returns (q, k, outliers [h_kv][d_c/4])."""
+    r = _rng(cfg.seed + seed_offset)
+    G, d = cfg.group, cfg.d_qk
+    k_scale = np.exp(0.5 * r.standard_normal((cfg.h_kv, d)))
+    q_scale = np.exp(0.5 * r.standard_normal((cfg.h_q, d))) * cfg.q_std
+    outliers = np.stack([np.sort(r.choice(d, size=cfg.d_c // 4, replace=False)) for _ in range(cfg.h_kv)])
+    for g in range(cfg.h_kv):
+        k_scale[g, outliers[g]] *= 6.0
+        q_scale[g * G:(g + 1) * G, outliers[g]] *= 6.0
+    q = r.standard_normal((n_cal, cfg.h_q, d), dtype=np.float32) * q_scale.astype(np.float32)
+    k = r.standard_normal((n_cal, cfg.h_kv, d), dtype=np.float32) * k_scale.astype(np.float32)
+    return _store(q.astype(np.float32), cfg.dtype), _store(k.astype(np.float32), cfg.dtype), outliers.astype(np.int32)
+
+
 def draw_plant_starts(cfg: DecodeConfig, ctx_lens: np.ndarray) -> np.ndarray:
     """Start positions of non-overlapping planted clusters, [batch][h_kv][clusters].
 

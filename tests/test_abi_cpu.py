@@ -31,7 +31,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ["tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
               "tls_sparse_decode", "tls_prefetch_blocks", "tls_workspace_size", "tls_check_device_error",
-              "tls_prefill_kv", "tls_offload_kv", "tls_init_residency"]:
+              "tls_prefill_kv", "tls_offload_kv", "tls_init_residency", "tls_calibrate_absmax",
+              "tls_calibrate_channels"]:
         assert n in names, n
 
 
@@ -156,6 +157,19 @@ def test_prefill_calls_are_validated_before_launch(tls):
     assert lib.tls_init_residency(ctypes.byref(L), d, d, d, d, 8, d, d, 4, d, d, d, 1 << 40, null) == 1
     assert lib.tls_init_residency(ctypes.byref(L), d, d, d, d, 8, d, d, 16, d, d, null, 1 << 40, null) == 1
     assert lib.tls_init_residency(ctypes.byref(Lm), d, d, d, d, 8, d, d, 16, d, d, d, 1 << 40, null) == 1
+
+
+def test_calibration_calls_are_validated_before_launch(tls):
+    lib = _raw(tls)
+    L = _layout(tls)
+    d = ctypes.c_void_p(0x1000)
+    null = None
+    assert lib.tls_calibrate_absmax(ctypes.byref(L), d, d, -1, d, d, 0, null) == 1     # negative row count
+    assert lib.tls_calibrate_absmax(ctypes.byref(L), null, d, 16, d, d, 0, null) == 1   # rows without q
+    assert lib.tls_calibrate_absmax(ctypes.byref(L), d, d, 16, null, d, 0, null) == 1   # no output
+    assert lib.tls_calibrate_absmax(ctypes.byref(L), d, d, 16, d, d, 2, null) == 1      # accumulate not 0/1
+    assert lib.tls_calibrate_channels(ctypes.byref(L), d, d, null, null, null) == 1     # no channel output
+    assert lib.tls_calibrate_channels(ctypes.byref(_layout(tls, num_q_heads=30)), d, d, d, null, null) == 1
 
 
 def test_decode_modes_are_validated_before_launch(tls):
