@@ -16,8 +16,8 @@
 // The prefill side of the tier (Sec. 4.2, Fig. 2) has two more pieces:
 // offload_rows_kernel copies the K/V rows written at prefill from HBM to the
 // pinned host arrays the prefetch later reads, and the initial residency
-// (the blocks chosen by the final prefill query) is the same plan and copy
-// run on an emptied pool, reading the rows from HBM with a full grid.
+// (the blocks chosen by the final prefill query) is the same plan run on an
+// emptied pool, then a copy with one work-group per transfer entry.
 #include "kernels.hpp"
 
 namespace tls {
@@ -191,6 +191,29 @@ hipError_t launch_prefetch(const Problem& P, const void* host_k, const void* hos
                               n_slots, slot_map, slot_owner, transfer_count, transfer_list, err, kCopyWGs, st);
 }
 
+// Initial residency copy: nothing runs beside it, so every transfer entry
+// gets its own work-group (grid K_b x units; entries past the unit's count
+// exit at once).
+__global__ __launch_bounds__(kCopyThreads) void residency_copy_kernel(
+    const uint8_t* __restrict__ src_k, const uint8_t* __restrict__ src_v, const int32_t* __restrict__ ctx_lens,
+    const int32_t* __restrict__ xfer, int K_b, int H_kv, int T, int B, int row_k, int row_v, int64_t n_slots,
+    uint8_t* __restrict__ pool_k, uint8_t* __restrict__ pool_v) {
+  const int unit = blockIdx.y, k = blockIdx.x;
+  const int32_t* list = xfer + size_t(unit) * (2 * K_b + 1);
+  if (k >= list[0]) return;
+  int n = ctx_lens[unit / H_kv];
+  n = n < 0 ? 0 : (n > T ? T : n);
+  const int b = list[1 + 2 * k], sl = list[2 + 2 * k];
+  const int r0 = b * B, r1 = min(r0 + B, n);
+  if (r1 <= r0) return;
+  const size_t rows = size_t(r1 - r0);
+  copy_block_rows(src_k + (size_t(unit) * T + r0) * row_k, pool_k + (size_t(unit) * n_slots + sl) * size_t(B) * row_k,
+                  rows * row_k);
+  if (src_v)
+    copy_block_rows(src_v + (size_t(unit) * T + r0) * row_v,
+                    pool_v + (size_t(unit) * n_slots + sl) * size_t(B) * row_v, rows * row_v);
+}
+
 hipError_t launch_init_residency(const Problem& P, const void* src_k, const void* src_v, const int32_t* ctx_lens,
                                  const int32_t* block_ids, int K_b, void* pool_k, void* pool_v, int64_t n_slots,
                                  int32_t* slot_map, int32_t* slot_owner, int32_t* transfer_list, uint32_t* err,
@@ -200,9 +223,16 @@ hipError_t launch_init_residency(const Problem& P, const void* src_k, const void
   if (e == hipSuccess)
     e = launch_fill_u32(reinterpret_cast<uint32_t*>(slot_owner), 0xffffffffu, size_t(P.units) * n_slots, st);
   if (e != hipSuccess) return e;
-  // one copy work-group per unit: nothing runs beside it
-  return launch_plan_and_copy(P, src_k, src_v, ctx_lens, block_ids, nullptr, K_b, pool_k, pool_v, n_slots,
-                              slot_map, slot_owner, nullptr, transfer_list, err, P.units, st);
+  const size_t lds = ((P.m_max + 31) / 32 + 8) * sizeof(uint32_t);
+  prefetch_plan_kernel<<<P.units, 256, lds, st>>>(ctx_lens, block_ids, nullptr, K_b, P.H_kv, P.T, P.B, P.m_max,
+                                                  n_slots, slot_map, slot_owner, nullptr, transfer_list, err);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int es = P.dtype == 1 ? 2 : 4;
+  residency_copy_kernel<<<dim3(unsigned(K_b), unsigned(P.units)), kCopyThreads, 0, st>>>(
+      (const uint8_t*)src_k, (const uint8_t*)src_v, ctx_lens, transfer_list, K_b, P.H_kv, P.T, P.B, P.d_qk * es,
+      P.d_v * es, n_slots, (uint8_t*)pool_k, (uint8_t*)pool_v);
+  return hipGetLastError();
 }
 
 // Device -> pinned host copy of the rows [tok_begin, min(tok_end, ctx_len))
