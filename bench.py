@@ -521,6 +521,28 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = start.elapsed_time(stop) / args.steps
 
+    # ---- per-step distribution: 200 steps, each bracketed by events; then the same
+    # with a 1 GiB scratch write between steps (untimed) so no step can find its
+    # data in the 256 MB Infinity Cache -----------------------------------------------
+    def step_distribution(n, flush=None):
+        pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        torch.cuda.synchronize()
+        for i in range(n):
+            if flush is not None:
+                flush.fill_(float(i))
+            pairs[i][0].record()
+            step(i)
+            pairs[i][1].record()
+        torch.cuda.synchronize()
+        ts = np.array([a.elapsed_time(b) * 1e3 for a, b in pairs])
+        return {"n": n, "median_us": round(float(np.median(ts)), 2), "p10_us": round(float(np.percentile(ts, 10)), 2),
+                "p90_us": round(float(np.percentile(ts, 90)), 2)}
+
+    dist = step_distribution(200)
+    flush_buf = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dist_flush = step_distribution(50, flush_buf)
+    del flush_buf
+
     # ---- per-stage timing with HIP events on the launch stream --------------------
     hev = HipEvents()
     evs = [hev.create(tls.NUM_STAGE_EVENTS) for _ in range(args.steps)]
@@ -625,6 +647,8 @@ def main():
         "achieved_GBps": round(gbps, 1),
         "step_frac_of_peak_hbm": round(gbps / PEAK_HBM_GBPS, 4),
         "algorithmic_bytes_per_step": nb,
+        "step_us_distribution": dist,
+        "step_us_after_1GiB_flush": dist_flush,
         "stage_us": {k: round(float(v) * 1e3, 2) for k, v in zip(STAGES, stage_ms)},
         "stage_marked_step_us": round(marked_ms * 1e3, 2),
         "prefill": prefill,
