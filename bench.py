@@ -685,10 +685,30 @@ def main():
             work.append((qg, Ku, Vu, n, d["channels_host"][g], cfg.k_b, cfg.k_t, cfg.block, cfg.sigma, summ, index))
         cores = max(1, min(16, len(os.sched_getaffinity(0))))
         per_step_s, wall = cpu_baseline(work, cfg, len(units_all), pick, cores)
+        # one unit on one core in this process: the decode step, and the index build it used
+        qg, Ku, Vu, n, chg = work[0][:5]
+        t0 = time.perf_counter()
+        _cpu_unit(work[0])
+        one_unit_s = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        O.block_summaries(Ku, n, cfg.block)
+        O.token_index(Ku, n, chg)
+        index_unit_s = time.perf_counter() - t0
+        cpu_model = "unknown"
+        try:
+            for line in open("/proc/cpuinfo"):
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+        except OSError:
+            pass
         result["cpu_baseline"] = {
             "value": round(per_step_s * 1e6, 1), "unit": "µs/layer-step", "cores": cores, "kind": "oracle",
             "sample": f"{len(pick)} of {len(units_all)} (sequence, KV head) units, float64 NumPy oracle decode "
                       f"step on prebuilt indices, {cores} worker processes, {wall:.2f} s wall; scaled to all units",
+            "cpu_model": cpu_model,
+            "single_core_s_per_unit": round(one_unit_s, 3),
+            "index_build_s_per_unit": round(index_unit_s, 3),
         }
     if args.offload:
         del layers, layer, d
