@@ -28,6 +28,9 @@ CASES = {
                                            seed=142),
     "mla_bf16": synth.config("mla").replace(batch=2, ctx_lo=600, ctx_hi=1100, clusters=1, k_b=6, k_t=100,
                                             seed=143),
+    # V rows of 72 bytes (not a multiple of 16): the element-wise V copy
+    "odd_dv_bf16": synth.config("toy").replace(dtype="bf16", batch=2, h_q=4, h_kv=2, d_v=36, ctx_lo=200, ctx_hi=333,
+                                               clusters=1, k_b=2, k_t=32, seed=145),
     # 4 KB key rows: a block is staged in LDS in several passes of fewer rows
     "wide_f32": synth.config("toy").replace(batch=1, h_q=4, h_kv=2, d_qk=1024, d_v=64, d_c=64, ctx_lo=300,
                                             ctx_hi=300, clusters=1, k_b=2, k_t=32, seed=144),
