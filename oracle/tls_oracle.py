@@ -375,20 +375,30 @@ def lagged_decode(q_steps, K, V, n, channels, k_b, k_t, B, sigma, d_v, mla=False
     M_t = BlockSelect(q_t) and S_t = TokenSelect(q_t, M_{t-1}); the resident
     set evolves as T_t = M_t minus C_t, C_{t+1} = M_t, with C_1 = M_0.
 
-    q_steps: [T+1][b][H_q][d] float64.  Attention always reads the full K/V,
-    so offloading must not change any result.  Returns a list over t = 1..T."""
+    q_steps: [T+1][b][H_q][d] float64.  n: the context length, or a sequence
+    of T+1 lengths when the context grows during decoding (n[0] at the
+    prefill's selection of M_0; at step t the tokens below n[t] exist, the
+    block and token indices are those of that length, and the candidates of
+    M_{t-1} are its blocks' tokens below n[t]).  Attention always reads the
+    full K/V, so offloading must not change any result.  Returns a list over
+    t = 1..T."""
     H_kv = K.shape[1]
     G = q_steps.shape[2] // H_kv
+    n_at = [int(n)] * q_steps.shape[0] if np.ndim(n) == 0 else [int(x) for x in n]
     qg0, Ku, Vu = unit_views(q_steps[0], K, V, s, g, G, mla, d_v)
-    kmax, kmin = block_summaries(Ku, n, B)
-    index = token_index(Ku, n, channels)
+    kmax, kmin = block_summaries(Ku, n_at[0], B)
     M_prev, _ = select_blocks(qg0, kmax, kmin, k_b)
     resident = set(int(x) for x in M_prev)
     steps = []
+    index, index_n = None, -1
     for t in range(1, q_steps.shape[0]):
+        nt = n_at[t]
+        if index_n != nt:  # the indices of the context as it stands at step t
+            kmax, kmin = block_summaries(Ku, nt, B)
+            index, index_n = token_index(Ku, nt, channels), nt
         qg = q_steps[t, s, g * G:(g + 1) * G]
         M_t, _ = select_blocks(qg, kmax, kmin, k_b)
-        S_t, _, _ = select_tokens(qg, channels, index[0], index[1], M_prev, n, B, k_t, sigma)
+        S_t, _, _ = select_tokens(qg, channels, index[0], index[1], M_prev, nt, B, k_t, sigma)
         o, lse = sparse_attention(qg, Ku, Vu, S_t, sigma)
         Mset = set(int(x) for x in M_t)
         transfer = sorted(Mset - resident)

@@ -353,6 +353,48 @@ def pin_lagged_schedule():
         assert prev is not None
 
 
+def pin_lagged_schedule_growth(seed=18):
+    """Offloaded schedule with the context growing by one token per step: a
+    constant length reproduces the fixed-length schedule exactly; every step's
+    tokens lie in the candidates of M_{t-1} at that step's length; a token
+    appended with a key along the step's queries, inside a block of M_{t-1},
+    is selected at once."""
+    cfg = synth.config("toy").replace(ctx_lo=1024, ctx_hi=1024, k_b=4, k_t=64, steps=6)
+    d = synth.make_host(cfg)
+    K = synth.to_f64(d["k"], cfg.dtype)
+    V = synth.to_f64(d["v"], cfg.dtype)
+    qs = synth.to_f64(synth.draw_query_walk(cfg.replace(rho=0.8)), cfg.dtype)
+    args = (d["channels"][0], cfg.k_b, cfg.k_t, cfg.block, cfg.sigma, cfg.d_v)
+    fixed = O.lagged_decode(qs, K, V, 1000, *args)
+    same = O.lagged_decode(qs, K, V, [1000] * qs.shape[0], *args)
+    for a, b in zip(fixed, same):
+        assert np.array_equal(a["token_ids"], b["token_ids"]) and np.array_equal(a["out"], b["out"])
+    n_steps = [1000 + t for t in range(qs.shape[0])]
+    steps = O.lagged_decode(qs, K, V, n_steps, *args)
+    for t, st in enumerate(steps, start=1):
+        cand = set(O.candidates(st["lag_block_ids"], n_steps[t], cfg.block).tolist())
+        assert set(st["token_ids"].tolist()) <= cand
+        assert max(st["token_ids"]) < n_steps[t]
+    # plant: the token appended at step t (position n_t - 1) gets a key along
+    # the group's (frozen) query; an earlier planted key in the same block
+    # keeps that block in every M, so the new token is a candidate at once
+    # and must be selected
+    Kp = K.copy()
+    qf = np.repeat(qs[:1], qs.shape[0], axis=0)
+    u = qf[0, 0, 0:cfg.group].mean(axis=0)
+    u /= np.linalg.norm(u)
+    t_plant = 3
+    pos = n_steps[t_plant] - 1
+    Kp[0, 0, pos] = 4.0 * math.sqrt(cfg.d_qk) * u
+    Kp[0, 0, (pos // cfg.block) * cfg.block + 5] = 4.0 * math.sqrt(cfg.d_qk) * u
+    blocks0 = O.select_blocks(qf[0, 0, 0:cfg.group], *O.block_summaries(Kp[0, 0], n_steps[0], cfg.block), cfg.k_b)[0]
+    assert pos // cfg.block in set(blocks0.tolist())
+    st = O.lagged_decode(qf, Kp, V, n_steps, *args)[t_plant - 1]
+    assert pos in set(st["token_ids"].tolist())
+    before = O.lagged_decode(qf, Kp, V, n_steps, *args)[t_plant - 2]   # one step earlier it does not exist yet
+    assert pos not in set(before["token_ids"].tolist())
+
+
 # --- channel calibration (Sec. 4.1) -------------------------------------------
 
 def pin_calibration_golden():
@@ -427,6 +469,7 @@ ALL_PINS = [
     pin_quest_golden, pin_quest_forms_agree, pin_quest_upper_bound, pin_topk_bruteforce,
     pin_candidates, pin_quant_golden, pin_quant_bound, pin_alpha_golden, pin_alpha_distribution,
     pin_attention_library, pin_attention_closed_form, pin_dense_equivalence,
-    pin_invariants_and_planted, pin_single_level_operators, pin_lagged_schedule, pin_calibration_golden,
+    pin_invariants_and_planted, pin_single_level_operators, pin_lagged_schedule, pin_lagged_schedule_growth,
+    pin_calibration_golden,
     pin_calibration_properties,
 ]
