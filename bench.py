@@ -348,12 +348,19 @@ def offload_schedule(tls, synth, torch, np):
     # cache with both indices built on the way; the final prompt query selects
     # the initial residency; the cache is offloaded to pinned host memory on a
     # side stream, and the HBM cache is then released
-    k_src = d["k"].transpose(1, 2).contiguous()
-    v_src = d["v"].transpose(1, 2).contiguous()
+    # the context grows by one token per sequence per step (from n - T to n):
+    # the rows the walk appends are kept aside; the prompt is the rest
+    T_steps = walk.shape[0] - 1
+    n0 = cfg.max_ctx - T_steps
+    k_future = d["k"][:, :, n0:].contiguous()
+    v_future = d["v"][:, :, n0:].contiguous()
+    ctx = torch.full_like(ctx, n0)
+    k_src = d["k"][:, :, :n0].transpose(1, 2).contiguous()
+    v_src = d["v"][:, :, :n0].transpose(1, 2).contiguous()
     K, V = d.pop("k"), d.pop("v")
     p0, p1 = ev(), ev()
     p0.record(main)
-    tls.tls_prefill_kv(layout, k_src, v_src, ctx, ch, 0, cfg.max_ctx, K, V, kmax, kmin, codes, qparams)
+    tls.tls_prefill_kv(layout, k_src, v_src, ctx, ch, 0, n0, K, V, kmax, kmin, codes, qparams)
     p1.record(main)
     del k_src, v_src
     host_k = torch.empty(K.shape, dtype=dt, pin_memory=True)
@@ -375,7 +382,7 @@ def offload_schedule(tls, synth, torch, np):
     tls.tls_offload_kv(layout, K, V, ctx, 0, cfg.max_ctx, host_k, host_v, stream=side)
     o1.record(side)
     torch.cuda.synchronize()
-    kv_bytes = 2 * K.numel() * K.element_size()
+    kv_bytes = 2 * cfg.batch * cfg.h_kv * n0 * cfg.d_qk * K.element_size()  # the rows offloaded
     prefill_rec = dict(prefill_kv_ms=p0.elapsed_time(p1), offload_ms=o0.elapsed_time(o1),
                        residency_ms=r0.elapsed_time(r1))
     del K, V, d
@@ -387,6 +394,9 @@ def offload_schedule(tls, synth, torch, np):
         M_prev, M_t = M[(t - 1) % 2], M[t % 2]
         e0, e_sel, e_dec, e1, p0, p1 = ev(), ev(), ev(), ev(), ev(), ev()
         e0.record(main)
+        ctx += 1  # the token generated by the previous step joins the context
+        tls.tls_append_tokens(layout, k_future[:, :, t - 1].contiguous(), v_future[:, :, t - 1].contiguous(), ctx, ch,
+                              host_k, host_v, kmax, kmin, codes, qparams, pool=kv)
         tls.tls_select_blocks(layout, qs[t], kmax, kmin, ctx, K_b, M_t, None, ws)
         e_sel.record(main)
         side.wait_event(e_sel)
@@ -409,8 +419,10 @@ def offload_schedule(tls, synth, torch, np):
     blocks = float(np.mean([r["blocks"] for r in rec]))
     xfer_bytes = blocks * block_bytes
     return {
-        "workload": "offload_gqa_96k: b=32, 32/8 heads, d=128, bf16, n=98304, K_b=128, K_t=2048, "
-                    f"{len(rec)} steps of an AR(1) query walk (rho={cfg.rho}); K/V {2 * host_k.numel() * 2 / 1e9:.1f} GB "
+        "workload": "offload_gqa_96k: b=32, 32/8 heads, d=128, bf16, K_b=128, K_t=2048, "
+                    f"{len(rec)} steps of an AR(1) query walk (rho={cfg.rho}) with the context growing from {n0} to "
+                    f"{n0 + len(rec)} tokens (one appended per sequence per step: host row, pool row when resident, "
+                    f"block summary, token-index row); K/V {2 * host_k.numel() * 2 / 1e9:.1f} GB "
                     f"in pinned host memory, pool of {n_slots} slots per unit in HBM",
         "step_wall_us_median": round(med("wall"), 1),
         "select_blocks_us_median": round(med("select"), 1),

@@ -299,6 +299,30 @@ tls_status tls_prefetch_blocks(const tls_layout* layout, const void* host_k, con
                                int32_t* slot_owner, int32_t* transfer_count, void* ws,
                                size_t ws_bytes, hipStream_t stream);
 
+/* Decode-time append (the index definitions of Sec. 4.1 kept current as the
+ * context grows; with the offloaded tier of Sec. 4.2).  For every sequence s
+ * with n = ctx_lens[s] >= 1 (the length including the new token), the token
+ * at t = n - 1:
+ *   K[s][h][t][:] = k_new[s][h][:]   (and V from v_new unless mla_shared_kv);
+ *   block summaries of block t/B: the row itself when t opens the block,
+ *     else the elementwise max / min of the stored summaries and the row --
+ *     the exact max / min of the block's rows, equal bit for bit to a
+ *     rebuild (the summaries must describe rows [B*(t/B), t));
+ *   token-index row t, quantised as tls_build_token_index does;
+ *   and, when pool is given (its slot_map non-NULL) and block t/B is resident,
+ *     row t%B of the block's pool slot (K, and V unless mla_shared_kv), so a
+ *     resident block stays a copy of the cache.
+ * k_new [b][H_kv][d_qk], v_new [b][H_kv][d_v] (device; v_new NULL iff
+ * mla_shared_kv).  K and V (dense layouts) may be device memory or pinned
+ * host memory (the offloaded tier's host copy); the row is stored there by
+ * the device.  Call once per decode step, after raising ctx_lens by one and
+ * before the step's selection.  Sequences with ctx_lens 0 are skipped;
+ * ctx_lens outside [0, max_ctx] and slots >= pool->n_slots are skipped. */
+tls_status tls_append_tokens(const tls_layout* layout, const void* k_new, const void* v_new,
+                             const int32_t* ctx_lens, const int32_t* channels, void* K, void* V, void* kmax,
+                             void* kmin, uint8_t* codes, float* qparams, const tls_kv_view* pool,
+                             hipStream_t stream);
+
 /* Offload of the prefill KV cache to host memory (Sec. 4.2 / Fig. 2: after
  * prefill the cache lives in host memory and only a resident subset stays in
  * HBM).  Copies rows [tok_begin, min(tok_end, ctx_len)) of every unit of the

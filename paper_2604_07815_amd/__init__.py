@@ -37,7 +37,7 @@ EXPORTED_SYMBOLS = [
     "tls_version", "tls_status_string", "tls_workspace_size", "tls_workspace_init",
     "tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
     "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error", "tls_prefill_kv",
-    "tls_offload_kv", "tls_init_residency", "tls_calibrate_absmax", "tls_calibrate_channels",
+    "tls_offload_kv", "tls_init_residency", "tls_calibrate_absmax", "tls_calibrate_channels", "tls_append_tokens",
 ]
 
 
@@ -88,6 +88,7 @@ def _load() -> ctypes.CDLL:
                                     P, P, P, P, P, SZ, ctypes.POINTER(DecodeOpts), P]),
         "tls_prefetch_blocks": (I32, [LP, P, P, P, P, P, I32, P, P, I64, P, P, P, P, SZ, P]),
         "tls_offload_kv": (I32, [LP, P, P, P, I32, I32, P, P, P]),
+        "tls_append_tokens": (I32, [LP, P, P, P, P, P, P, P, P, P, P, ctypes.POINTER(KvView), P]),
         "tls_calibrate_absmax": (I32, [LP, P, P, I32, P, P, I32, P]),
         "tls_calibrate_channels": (I32, [LP, P, P, P, P, P]),
         "tls_init_residency": (I32, [LP, P, P, P, P, I32, P, P, I64, P, P, P, SZ, P]),
@@ -284,6 +285,20 @@ def tls_prefetch_blocks(layout, host_k, host_v, ctx_lens, block_ids_new, block_i
         int(n_slots), _ptr(slot_map, "slot_map"), _ptr(slot_owner, "slot_owner"),
         _ptr(transfer_count, "transfer_count"), _ptr(ws, "ws"), _nbytes(ws), _stream(stream)),
         "tls_prefetch_blocks")
+
+
+def tls_append_tokens(layout, k_new, v_new, ctx_lens, channels, K, V, kmax, kmin, codes, qparams,
+                      pool: Optional["KV"] = None, stream=None) -> None:
+    """Append the token at ctx_lens - 1 of every sequence: cache row (K/V on the GPU or pinned host tensors),
+    incremental block summary, token-index row, and the pool row when pool (a pooled KV view) holds its block."""
+    def cache(t, name):
+        return None if t is None else (_ptr(t, name) if t.is_cuda else _pinned(t, name))
+    view = pool.as_struct() if pool is not None else None
+    _check(_lib.tls_append_tokens(ctypes.byref(layout), _ptr(k_new, "k_new"), _ptr(v_new, "v_new"),
+                                  _ptr(ctx_lens, "ctx_lens"), _ptr(channels, "channels"), cache(K, "K"),
+                                  cache(V, "V"), _ptr(kmax, "kmax"), _ptr(kmin, "kmin"), _ptr(codes, "codes"),
+                                  _ptr(qparams, "qparams"), ctypes.byref(view) if view is not None else None,
+                                  _stream(stream)), "tls_append_tokens")
 
 
 def _pinned(t, name):

@@ -55,6 +55,64 @@ struct IndexArgs {
   uint32_t* err;
 };
 
+// INT4 quantisation of one 32-channel group of a key row (the token index):
+// the group's min and scale = (max - min) / 15 in IEEE float32, and the
+// codes rint((x - min) / scale) clamped to [0, 15], two per byte, channel 2k
+// in the low nibble of byte k (all 0 when scale == 0).  chs: the group's 32
+// channel ids (already validated).  Each code's quotient comes from a
+// multiply by the reciprocal of the scale unless it lies within kNearHalf of
+// a rounding boundary (or is not finite), where the IEEE quotient is
+// recomputed, so the codes equal rint of the correctly rounded quotient.
+template <class E>
+__device__ inline void quantise_group32(const typename E::T* rowp, const int* chs, float& scale_out, float& lo_out,
+                                        uint4& codes_out) {
+#pragma clang fp contract(off)
+  float lo_v = __builtin_inff(), hi_v = -__builtin_inff();
+#pragma unroll 8
+  for (int j = 0; j < 32; ++j) {
+    const float x = E::to_f(rowp[chs[j]]);
+    lo_v = fminf(lo_v, x);
+    hi_v = fmaxf(hi_v, x);
+  }
+  const float scale = (hi_v - lo_v) / 15.0f;  // IEEE float32 subtract and divide
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+  if (scale != 0.0f) {
+    const float rcp = __builtin_amdgcn_rcpf(scale);
+    uint32_t near = 0;  // channels whose product lies near a rounding boundary
+#pragma unroll 1
+    for (int wi = 0; wi < 4; ++wi) {  // eight channels per 32-bit word of codes
+      uint32_t acc = 0;
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        const float q = (E::to_f(rowp[chs[wi * 8 + jj]]) - lo_v) * rcp;
+        near |= uint32_t(!(fabsf(__builtin_amdgcn_fractf(q) - 0.5f) > kNearHalf && q < 16.0f)) << (wi * 8 + jj);
+        // round half to even, clamp; channel 2k in the low nibble of byte k
+        acc |= uint32_t(fminf(fmaxf(__builtin_rintf(q), 0.0f), 15.0f)) << (4 * jj);
+      }
+      w[0] = wi == 0 ? acc : w[0];
+      w[1] = wi == 1 ? acc : w[1];
+      w[2] = wi == 2 ? acc : w[2];
+      w[3] = wi == 3 ? acc : w[3];
+    }
+    // rare: recompute those codes from the IEEE quotient
+    for (; near != 0; near &= near - 1) {
+      const int j = __builtin_ctz(near);
+      const float q = fminf(fmaxf(__builtin_rintf((E::to_f(rowp[chs[j]]) - lo_v) / scale), 0.0f), 15.0f);
+      const int sh = 4 * (j & 7);
+      const uint32_t keep = ~(0xFu << sh), code = uint32_t(q) << sh;
+      switch (j >> 3) {
+        case 0: w[0] = (w[0] & keep) | code; break;
+        case 1: w[1] = (w[1] & keep) | code; break;
+        case 2: w[2] = (w[2] & keep) | code; break;
+        default: w[3] = (w[3] & keep) | code; break;
+      }
+    }
+  }
+  scale_out = scale;
+  lo_out = lo_v;
+  codes_out = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 // Copies rows [r_lo, r_hi) of one unit's V from the prefill output to the cache.
 __device__ inline void copy_v_rows(const IndexArgs& a, int s, int g, size_t unit, int r_lo, int r_hi, int es) {
   const int rbv = a.d_v * es;
@@ -228,50 +286,11 @@ __global__ __launch_bounds__(kIdxThreads) void index_rows_kernel(const IndexArgs
         const int rr = k & 63, grp = k >> 6;  // lane = row of the pass, wave-uniform group
         if (rr < lo || rr >= up) continue;
         const typename E::T* rowp = reinterpret_cast<const typename E::T*>(t32 + rr * tsw);
-        const int* chs = s_ch + grp * 32;
-        float lo_v = __builtin_inff(), hi_v = -__builtin_inff();
-#pragma unroll 8
-        for (int j = 0; j < 32; ++j) {
-          const float x = E::to_f(rowp[chs[j]]);
-          lo_v = fminf(lo_v, x);
-          hi_v = fmaxf(hi_v, x);
-        }
-        const float scale = (hi_v - lo_v) / 15.0f;  // IEEE float32 subtract and divide
-        uint32_t w[4] = {0u, 0u, 0u, 0u};
-        if (scale != 0.0f) {
-          const float rcp = __builtin_amdgcn_rcpf(scale);
-          uint32_t near = 0;  // channels whose product lies near a rounding boundary
-#pragma unroll 1
-          for (int wi = 0; wi < 4; ++wi) {  // eight channels per 32-bit word of codes
-            uint32_t acc = 0;
-#pragma unroll
-            for (int jj = 0; jj < 8; ++jj) {
-              const float q = (E::to_f(rowp[chs[wi * 8 + jj]]) - lo_v) * rcp;
-              near |= uint32_t(!(fabsf(__builtin_amdgcn_fractf(q) - 0.5f) > kNearHalf && q < 16.0f)) << (wi * 8 + jj);
-              // round half to even, clamp; channel 2k in the low nibble of byte k
-              acc |= uint32_t(fminf(fmaxf(__builtin_rintf(q), 0.0f), 15.0f)) << (4 * jj);
-            }
-            w[0] = wi == 0 ? acc : w[0];
-            w[1] = wi == 1 ? acc : w[1];
-            w[2] = wi == 2 ? acc : w[2];
-            w[3] = wi == 3 ? acc : w[3];
-          }
-          // rare: recompute those codes from the IEEE quotient
-          for (; near != 0; near &= near - 1) {
-            const int j = __builtin_ctz(near);
-            const float q = fminf(fmaxf(__builtin_rintf((E::to_f(rowp[chs[j]]) - lo_v) / scale), 0.0f), 15.0f);
-            const int sh = 4 * (j & 7);
-            const uint32_t keep = ~(0xFu << sh), code = uint32_t(q) << sh;
-            switch (j >> 3) {
-              case 0: w[0] = (w[0] & keep) | code; break;
-              case 1: w[1] = (w[1] & keep) | code; break;
-              case 2: w[2] = (w[2] & keep) | code; break;
-              default: w[3] = (w[3] & keep) | code; break;
-            }
-          }
-        }
+        float scale, lo_v;
+        uint4 cw;
+        quantise_group32<E>(rowp, s_ch + grp * 32, scale, lo_v, cw);
         const size_t trow = unit * size_t(a.T) + (pr0 + rr);
-        *reinterpret_cast<uint4*>(a.codes + trow * (a.d_c / 2) + grp * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+        *reinterpret_cast<uint4*>(a.codes + trow * (a.d_c / 2) + grp * 16) = cw;
         *reinterpret_cast<float2*>(a.qparams + (trow * ngroups + grp) * 2) = make_float2(scale, lo_v + 0.0f);
       }
     }
@@ -397,6 +416,184 @@ hipError_t launch_prefill_kv(const Problem& P, const void* k_src, const void* v_
                              void* kmin, uint8_t* codes, float* qparams, uint32_t* err, hipStream_t st) {
   return launch_index_rows(P, k_src, v_src, K, V, ctx_lens, channels, tok_begin, tok_end, kmax, kmin, codes,
                            qparams, kIdxBlock | kIdxToken, err, st);
+}
+
+// ---------------------------------------------------------------------------
+// Append during decode: the token at t = ctx_len - 1 of every sequence.  One
+// work-group per unit writes the new K (and V) row to the cache (device or
+// pinned host memory) and, when its block is resident in the pool, to the
+// block's slot; updates the block summary incrementally (the row itself when
+// t opens the block, else the elementwise max / min of the stored summary and
+// the row: the exact max / min of the block's rows, as a rebuild gives); and
+// quantises the row for the token index.
+// ---------------------------------------------------------------------------
+struct AppendArgs {
+  const uint8_t* k_new;  // [b][H_kv][d]
+  const uint8_t* v_new;  // [b][H_kv][d_v]; NULL when V aliases K
+  uint8_t* k;            // dense K [b][H_kv][T][d]
+  uint8_t* v;            // dense V, or NULL
+  const int32_t* ctx_lens;
+  const int32_t* channels;
+  uint8_t* kmax;
+  uint8_t* kmin;
+  uint8_t* codes;
+  float* qparams;
+  uint8_t* pool_k;  // [units][n_slots][B][d], or NULL
+  uint8_t* pool_v;
+  const int32_t* slot_map;  // [units][m_max], or NULL
+  int64_t n_slots;
+  int H_kv, T, d, d_v, d_c, B, m_max;
+  uint32_t* err;
+};
+
+template <class E>
+__device__ inline uint32_t fold_word(uint32_t old, uint32_t x, bool take_max) {
+  if constexpr (E::kIsBf16) {
+    const float lo = take_max ? fmaxf(bf16_lo(old), bf16_lo(x)) : fminf(bf16_lo(old), bf16_lo(x));
+    const float hi = take_max ? fmaxf(bf16_hi(old), bf16_hi(x)) : fminf(bf16_hi(old), bf16_hi(x));
+    return uint32_t(f32_to_bf16(lo + 0.0f)) | (uint32_t(f32_to_bf16(hi + 0.0f)) << 16);
+  } else {
+    const float a = __uint_as_float(old), b = __uint_as_float(x);
+    return __float_as_uint((take_max ? fmaxf(a, b) : fminf(a, b)) + 0.0f);
+  }
+}
+
+template <class E>
+__device__ inline uint32_t plus_zero_word(uint32_t x) {  // -0.0 -> +0.0, element by element
+  if constexpr (E::kIsBf16) {
+    return uint32_t(f32_to_bf16(bf16_lo(x) + 0.0f)) | (uint32_t(f32_to_bf16(bf16_hi(x) + 0.0f)) << 16);
+  } else {
+    return __float_as_uint(__uint_as_float(x) + 0.0f);
+  }
+}
+
+template <class E>
+__global__ __launch_bounds__(kIdxThreads) void append_token_kernel(const AppendArgs a) {
+  constexpr int es = int(sizeof(typename E::T));
+  extern __shared__ uint4 smem4[];
+  uint32_t* s_row = reinterpret_cast<uint32_t*>(smem4);  // the new key row
+  const int unit = blockIdx.x, tid = threadIdx.x;
+  const int s = unit / a.H_kv;
+  const int n = a.ctx_lens[s];
+  if (n < 0 || n > a.T) {
+    if (tid == 0) set_error(a.err, 1u);
+    return;
+  }
+  if (n == 0) return;
+  const int t = n - 1, blk = t / a.B, r = t % a.B;
+  const int rb = a.d * es, wpr = rb / 4;
+  int* s_ch = reinterpret_cast<int*>(s_row + wpr);
+  int slot = -1;
+  if (a.slot_map) {
+    slot = a.slot_map[size_t(unit) * a.m_max + blk];
+    if (slot >= a.n_slots) {
+      if (tid == 0) set_error(a.err, 8u);
+      slot = -1;
+    }
+  }
+  // the row in 16-byte pieces (rows are a multiple of 16 bytes): the stores to
+  // a host-memory cache then leave the chip as whole 16-byte writes
+  const uint8_t* src = a.k_new + size_t(unit) * rb;
+  uint8_t* dk = a.k + (size_t(unit) * a.T + t) * rb;
+  uint8_t* dp = slot >= 0 ? a.pool_k + ((size_t(unit) * a.n_slots + slot) * a.B + r) * rb : nullptr;
+  for (int c = tid; c < rb / 16; c += kIdxThreads) {
+    const uint4 x = ld16(src + c * 16);
+    reinterpret_cast<uint4*>(s_row)[c] = x;
+    *reinterpret_cast<uint4*>(dk + c * 16) = x;
+    if (dp) *reinterpret_cast<uint4*>(dp + c * 16) = x;
+  }
+  __syncthreads();
+  uint32_t* smx = reinterpret_cast<uint32_t*>(a.kmax + (size_t(unit) * a.m_max + blk) * rb);
+  uint32_t* smn = reinterpret_cast<uint32_t*>(a.kmin + (size_t(unit) * a.m_max + blk) * rb);
+  for (int w = tid; w < wpr; w += kIdxThreads) {
+    const uint32_t x = s_row[w];
+    if (r == 0) {  // the row opens its block
+      const uint32_t z = plus_zero_word<E>(x);
+      smx[w] = z;
+      smn[w] = z;
+    } else {
+      smx[w] = fold_word<E>(smx[w], x, true);
+      smn[w] = fold_word<E>(smn[w], x, false);
+    }
+  }
+  if (a.v_new) {
+    const int rbv = a.d_v * es;
+    const uint8_t* vs = a.v_new + size_t(unit) * rbv;
+    uint8_t* dv = a.v + (size_t(unit) * a.T + t) * rbv;
+    uint8_t* pv = slot >= 0 ? a.pool_v + ((size_t(unit) * a.n_slots + slot) * a.B + r) * rbv : nullptr;
+    if (rbv % 16 == 0) {
+      for (int c = tid; c < rbv / 16; c += kIdxThreads) {
+        const uint4 x = ld16(vs + c * 16);
+        *reinterpret_cast<uint4*>(dv + c * 16) = x;
+        if (pv) *reinterpret_cast<uint4*>(pv + c * 16) = x;
+      }
+    } else {
+      for (int e = tid; e < a.d_v; e += kIdxThreads) {  // rows that are not a multiple of 16 bytes
+        if constexpr (E::kIsBf16) {
+          const uint16_t x = reinterpret_cast<const uint16_t*>(vs)[e];
+          reinterpret_cast<uint16_t*>(dv)[e] = x;
+          if (pv) reinterpret_cast<uint16_t*>(pv)[e] = x;
+        } else {
+          const uint32_t x = reinterpret_cast<const uint32_t*>(vs)[e];
+          reinterpret_cast<uint32_t*>(dv)[e] = x;
+          if (pv) reinterpret_cast<uint32_t*>(pv)[e] = x;
+        }
+      }
+    }
+  }
+  const int g = unit % a.H_kv;
+  for (int c = tid; c < a.d_c; c += kIdxThreads) {
+    int ch = a.channels[g * a.d_c + c];
+    if (ch < 0 || ch >= a.d) {  // caller-supplied channel id out of range: read channel 0
+      set_error(a.err, 32u);
+      ch = 0;
+    }
+    s_ch[c] = ch;
+  }
+  __syncthreads();
+  const int ngroups = a.d_c / 32;
+  if (tid < ngroups) {
+    float scale, lo;
+    uint4 cw;
+    quantise_group32<E>(reinterpret_cast<const typename E::T*>(s_row), s_ch + tid * 32, scale, lo, cw);
+    const size_t trow = size_t(unit) * a.T + t;
+    *reinterpret_cast<uint4*>(a.codes + trow * (a.d_c / 2) + tid * 16) = cw;
+    *reinterpret_cast<float2*>(a.qparams + (trow * ngroups + tid) * 2) = make_float2(scale, lo + 0.0f);
+  }
+}
+
+hipError_t launch_append_tokens(const Problem& P, const void* k_new, const void* v_new, const int32_t* ctx_lens,
+                                const int32_t* channels, void* K, void* V, void* kmax, void* kmin, uint8_t* codes,
+                                float* qparams, void* pool_k, void* pool_v, const int32_t* slot_map, int64_t n_slots,
+                                uint32_t* err, hipStream_t st) {
+  AppendArgs a;
+  a.k_new = (const uint8_t*)k_new;
+  a.v_new = (const uint8_t*)v_new;
+  a.k = (uint8_t*)K;
+  a.v = (uint8_t*)V;
+  a.ctx_lens = ctx_lens;
+  a.channels = channels;
+  a.kmax = (uint8_t*)kmax;
+  a.kmin = (uint8_t*)kmin;
+  a.codes = codes;
+  a.qparams = qparams;
+  a.pool_k = (uint8_t*)pool_k;
+  a.pool_v = (uint8_t*)pool_v;
+  a.slot_map = slot_map;
+  a.n_slots = n_slots;
+  a.H_kv = P.H_kv;
+  a.T = P.T;
+  a.d = P.d_qk;
+  a.d_v = P.d_v;
+  a.d_c = P.d_c;
+  a.B = P.B;
+  a.m_max = P.m_max;
+  a.err = err;
+  const int es = P.dtype == 1 ? 2 : 4;
+  const size_t lds = size_t(P.d_qk) * es + size_t(P.d_c) * sizeof(int);
+  if (P.dtype == 1) append_token_kernel<BF16><<<P.units, kIdxThreads, lds, st>>>(a);
+  else append_token_kernel<F32><<<P.units, kIdxThreads, lds, st>>>(a);
+  return hipGetLastError();
 }
 
 }  // namespace tls

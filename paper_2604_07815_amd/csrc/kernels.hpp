@@ -41,6 +41,13 @@ hipError_t launch_token_index(const Problem& P, const void* K, const int32_t* ct
 hipError_t launch_prefill_kv(const Problem& P, const void* k_src, const void* v_src, const int32_t* ctx_lens,
                              const int32_t* channels, int tok_begin, int tok_end, void* K, void* V, void* kmax,
                              void* kmin, uint8_t* codes, float* qparams, uint32_t* err, hipStream_t st);
+// Decode-time append of the token at ctx_len - 1 of every sequence: cache row,
+// pool row when its block is resident (slot_map non-null), incremental block
+// summary, token-index row.
+hipError_t launch_append_tokens(const Problem& P, const void* k_new, const void* v_new, const int32_t* ctx_lens,
+                                const int32_t* channels, void* K, void* V, void* kmax, void* kmin, uint8_t* codes,
+                                float* qparams, void* pool_k, void* pool_v, const int32_t* slot_map, int64_t n_slots,
+                                uint32_t* err, hipStream_t st);
 
 hipError_t launch_block_score(const Problem& P, const void* q, const void* kmax, const void* kmin,
                               const int32_t* ctx_lens, float* qpn, float* scores, uint32_t* err, hipStream_t st);

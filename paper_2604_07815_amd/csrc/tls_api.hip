@@ -203,6 +203,36 @@ tls_status tls_prefill_kv(const tls_layout* layout, const void* k_src, const voi
                                            codes, qparams, nullptr, stream));
 }
 
+tls_status tls_append_tokens(const tls_layout* layout, const void* k_new, const void* v_new, const int32_t* ctx_lens,
+                             const int32_t* channels, void* K, void* V, void* kmax, void* kmin, uint8_t* codes,
+                             float* qparams, const tls_kv_view* pool, hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!k_new || !ctx_lens || !channels || !K || !kmax || !kmin || !codes || !qparams) return TLS_ERR_INVALID_ARGUMENT;
+  if (P.mla ? (v_new != nullptr || V != nullptr) : (!v_new || !V)) return TLS_ERR_INVALID_ARGUMENT;
+  void* pk = nullptr;
+  void* pv = nullptr;
+  const int32_t* smap = nullptr;
+  int64_t n_slots = 0;
+  if (pool) {
+    if (!pool->k || !pool->slot_map || pool->n_slots < 1 || pool->n_slots > (int64_t(1) << 30))
+      return TLS_ERR_INVALID_ARGUMENT;
+    if (P.mla ? pool->v != nullptr : !pool->v) return TLS_ERR_INVALID_ARGUMENT;
+    pk = const_cast<void*>(pool->k);
+    pv = const_cast<void*>(pool->v);
+    smap = pool->slot_map;
+    n_slots = pool->n_slots;
+  }
+  // the cache may be device memory or pinned host memory (the offloaded tier's host copy)
+  const void* dk = nullptr;
+  const void* dv = nullptr;
+  if (!readable_ptr(K, &dk) || (V && !readable_ptr(V, &dv))) return TLS_ERR_INVALID_ARGUMENT;
+  return hip_status(tls::launch_append_tokens(P, k_new, v_new, ctx_lens, channels, const_cast<void*>(dk),
+                                              const_cast<void*>(dv), kmax, kmin, codes, qparams, pk, pv, smap,
+                                              n_slots, nullptr, stream));
+}
+
 tls_status tls_offload_kv(const tls_layout* layout, const void* K, const void* V, const int32_t* ctx_lens,
                           int32_t tok_begin, int32_t tok_end, void* host_k, void* host_v, hipStream_t stream) {
   Problem P;

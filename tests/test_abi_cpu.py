@@ -32,7 +32,7 @@ def test_header_declares_the_boundary():
     for n in ["tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
               "tls_sparse_decode", "tls_prefetch_blocks", "tls_workspace_size", "tls_check_device_error",
               "tls_prefill_kv", "tls_offload_kv", "tls_init_residency", "tls_calibrate_absmax",
-              "tls_calibrate_channels"]:
+              "tls_calibrate_channels", "tls_append_tokens"]:
         assert n in names, n
 
 
@@ -157,6 +157,22 @@ def test_prefill_calls_are_validated_before_launch(tls):
     assert lib.tls_init_residency(ctypes.byref(L), d, d, d, d, 8, d, d, 4, d, d, d, 1 << 40, null) == 1
     assert lib.tls_init_residency(ctypes.byref(L), d, d, d, d, 8, d, d, 16, d, d, null, 1 << 40, null) == 1
     assert lib.tls_init_residency(ctypes.byref(Lm), d, d, d, d, 8, d, d, 16, d, d, d, 1 << 40, null) == 1
+
+
+def test_append_is_validated_before_launch(tls):
+    lib = _raw(tls)
+    L = _layout(tls)
+    Lm = _layout(tls, num_kv_heads=1, head_dim_qk=576, head_dim_v=512, index_channels=128, mla_shared_kv=True)
+    d = ctypes.c_void_p(0x1000)
+    null = None
+    args = [d, d, d, d, d, d, d, d, d, d]
+    assert lib.tls_append_tokens(ctypes.byref(L), *([null] + args[1:]), null, null) == 1      # no k_new
+    assert lib.tls_append_tokens(ctypes.byref(L), *(args[:1] + [null] + args[2:]), null, null) == 1  # GQA, no v_new
+    assert lib.tls_append_tokens(ctypes.byref(Lm), *args, null, null) == 1                    # MLA passes no V
+    bad_pool = tls.KvView(d.value, d.value, None, 16)                                         # pool without slot map
+    assert lib.tls_append_tokens(ctypes.byref(L), *args, ctypes.byref(bad_pool), null) == 1
+    no_slots = tls.KvView(d.value, d.value, d.value, 0)
+    assert lib.tls_append_tokens(ctypes.byref(L), *args, ctypes.byref(no_slots), null) == 1
 
 
 def test_calibration_calls_are_validated_before_launch(tls):

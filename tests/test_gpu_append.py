@@ -1,7 +1,9 @@
 """Incremental index maintenance during decode: appending one token per step
-re-summarises the token's block and quantises its token-index row (the
-builders' token range).  The maintained indices equal a full build bit for
-bit, and a decode step at the grown length matches the oracle."""
+re-summarises the token's block and quantises its token-index row, either
+with the builders' token range or with tls_append_tokens (which also writes
+the cache row, to device or pinned host memory, and the pool row of a
+resident block).  The maintained indices equal a full build bit for bit, and
+a decode step at the grown length matches the oracle."""
 import numpy as np
 import pytest
 import torch
@@ -51,3 +53,124 @@ def test_append_tokens_matches_full_build(name):
     for (s, g) in c.units():
         H.compare_unit(c, r, s, g)
     assert tls.tls_check_device_error(r["ws"]) == 0
+
+
+def _fresh_index(c):
+    cfg = c.cfg
+    dt = H.torch_dtype(cfg)
+    kmax = torch.full((cfg.batch, cfg.h_kv, c.m_max, cfg.d_qk), 7.0, dtype=dt, device="cuda")
+    kmin = torch.full_like(kmax, 7.0)
+    codes = torch.full((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 2), 0xAA, dtype=torch.uint8, device="cuda")
+    qparams = torch.full((cfg.batch, cfg.h_kv, cfg.max_ctx, cfg.d_c // 32, 2), 7.0, dtype=torch.float32, device="cuda")
+    return kmax, kmin, codes, qparams
+
+
+def _bits(t):
+    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_append_tokens_incremental(name):
+    """tls_append_tokens from a 1000-token prefill to 1100 tokens (crossing the
+    block boundaries at 1024 and 1088): cache rows, block summaries (updated
+    incrementally, never re-read) and token index equal a full build at the
+    final length bit for bit."""
+    import paper_2604_07815_amd as tls
+    cfg = CASES[name]()
+    final, start = 1100, 1000
+    c = H.Case(cfg, backend="host", pad="nan", ctx_lens=np.array([final] * cfg.batch, dtype=np.int32))
+    full = H.Case.__new__(H.Case)
+    full.__dict__.update(c.__dict__)
+    full.build_index()
+    K = c.k.clone()
+    K[:, :, start:] = float("nan")
+    V = None
+    if not cfg.mla:
+        V = c.v.clone()
+        V[:, :, start:] = float("nan")
+    kmax, kmin, codes, qparams = _fresh_index(c)
+    ctx = torch.full((cfg.batch,), start, dtype=torch.int32, device="cuda")
+    tls.tls_build_block_index(c.layout, K, ctx, 0, cfg.max_ctx, kmax, kmin)
+    tls.tls_build_token_index(c.layout, K, ctx, c.ch, 0, cfg.max_ctx, codes, qparams)
+    for t in range(start, final):
+        ctx.fill_(t + 1)
+        k_new = c.k[:, :, t].contiguous()
+        v_new = None if cfg.mla else c.v[:, :, t].contiguous()
+        tls.tls_append_tokens(c.layout, k_new, v_new, ctx, c.ch, K, V, kmax, kmin, codes, qparams)
+    torch.cuda.synchronize()
+    m = -(-final // cfg.block)
+    assert torch.equal(_bits(K[:, :, :final]), _bits(c.k[:, :, :final]))
+    if V is not None:
+        assert torch.equal(_bits(V[:, :, :final]), _bits(c.v[:, :, :final]))
+    assert torch.equal(_bits(kmax[:, :, :m]), _bits(full.kmax[:, :, :m]))
+    assert torch.equal(_bits(kmin[:, :, :m]), _bits(full.kmin[:, :, :m]))
+    assert torch.equal(codes[:, :, :final], full.codes[:, :, :final])
+    assert torch.equal(qparams[:, :, :final].view(torch.int32), full.qparams[:, :, :final].view(torch.int32))
+
+
+@pytest.mark.parametrize("name", ["gqa_bf16", "mla_bf16"])
+def test_append_to_host_cache_and_pool(name):
+    """The offloaded tier's append: the cache is pinned host memory and some
+    blocks (including the growing tail block) are resident in the HBM pool;
+    after the appends the host rows are the new tokens, every resident block's
+    pool slot equals its host rows, and the indices equal a full build."""
+    import paper_2604_07815_amd as tls
+    cfg = CASES[name]()
+    final, start = 1100, 1000
+    c = H.Case(cfg, backend="host", pad="nan", ctx_lens=np.array([final] * cfg.batch, dtype=np.int32))
+    full = H.Case.__new__(H.Case)
+    full.__dict__.update(c.__dict__)
+    full.build_index()
+    dt = H.torch_dtype(cfg)
+    hk = torch.empty(c.k.shape, dtype=dt, pin_memory=True)
+    hk.copy_(c.k.cpu())
+    hk[:, :, start:] = float("nan")
+    hv = None
+    if not cfg.mla:
+        hv = torch.empty(c.v.shape, dtype=dt, pin_memory=True)
+        hv.copy_(c.v.cpu())
+        hv[:, :, start:] = float("nan")
+    kmax, kmin, codes, qparams = _fresh_index(c)
+    ctx = torch.full((cfg.batch,), start, dtype=torch.int32, device="cuda")
+    tls.tls_build_block_index(c.layout, c.k, ctx, 0, cfg.max_ctx, kmax, kmin)
+    tls.tls_build_token_index(c.layout, c.k, ctx, c.ch, 0, cfg.max_ctx, codes, qparams)
+    # resident: blocks 3, 10, 15 (tail at 1000 tokens) and 16 (opened by the appends); 2 * 8 slots per unit
+    units, B, K_b, n_slots = cfg.batch * cfg.h_kv, cfg.block, 8, 16
+    bids = torch.full((cfg.batch, cfg.h_kv, K_b), -1, dtype=torch.int32, device="cuda")
+    bids[:, :, :3] = torch.tensor([3, 10, 15], dtype=torch.int32, device="cuda")
+    pool_k = torch.full((units, n_slots, B, cfg.d_qk), float("nan"), dtype=dt, device="cuda")
+    pool_v = None if cfg.mla else torch.full((units, n_slots, B, cfg.d_v), float("nan"), dtype=dt, device="cuda")
+    slot_map = torch.empty((units, c.m_max), dtype=torch.int32, device="cuda")
+    slot_owner = torch.empty((units, n_slots), dtype=torch.int32, device="cuda")
+    ws = c.workspace(k_b=K_b)
+    tls.tls_init_residency(c.layout, hk, hv, ctx, bids, K_b, pool_k, pool_v, n_slots, slot_map, slot_owner, ws)
+    pool = tls.KV(pool_k, pool_v, slot_map, n_slots)
+    for t in range(start, final):
+        ctx.fill_(t + 1)
+        if t == 1024:  # block 16 opens: make it resident too (empty until the appends fill it)
+            bids[:, :, 3] = 16
+            tls.tls_prefetch_blocks(c.layout, hk, hv, ctx, bids, None, K_b, pool_k, pool_v, n_slots, slot_map,
+                                    slot_owner, None, ws)
+        k_new = c.k[:, :, t].contiguous()
+        v_new = None if cfg.mla else c.v[:, :, t].contiguous()
+        tls.tls_append_tokens(c.layout, k_new, v_new, ctx, c.ch, hk, hv, kmax, kmin, codes, qparams, pool=pool)
+    torch.cuda.synchronize()
+    assert tls.tls_check_device_error(ws) == 0
+    assert torch.equal(_bits(hk[:, :, :final]), _bits(c.k[:, :, :final].cpu()))
+    if hv is not None:
+        assert torch.equal(_bits(hv[:, :, :final]), _bits(c.v[:, :, :final].cpu()))
+    m = -(-final // cfg.block)
+    assert torch.equal(_bits(kmax[:, :, :m]), _bits(full.kmax[:, :, :m]))
+    assert torch.equal(codes[:, :, :final], full.codes[:, :, :final])
+    smap, pk = slot_map.cpu().numpy(), pool_k.cpu()
+    pv = None if pool_v is None else pool_v.cpu()
+    for s in range(cfg.batch):
+        for g in range(cfg.h_kv):
+            u = s * cfg.h_kv + g
+            for b in (3, 10, 15, 16):
+                sl = int(smap[u, b])
+                assert sl >= 0, f"block {b} not resident"
+                rows = min(B, final - b * B)
+                assert torch.equal(_bits(pk[u, sl, :rows]), _bits(hk[s, g, b * B:b * B + rows])), (u, b)
+                if pv is not None:
+                    assert torch.equal(_bits(pv[u, sl, :rows]), _bits(hv[s, g, b * B:b * B + rows])), (u, b)
