@@ -201,17 +201,64 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ po
   const size_t orow = size_t(s) * H_q + size_t(g) * G + h;
   const float* base = po + (size_t(unit) * nsplit * G + h) * d_v;
   const size_t stride = size_t(G) * d_v;  // between splits
-  for (int dd = threadIdx.x; dd < d_v; dd += blockDim.x) {
-    float o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;
-    int i = 0;
-    for (; i + 4 <= nsplit; i += 4) {
-      o0 = fmaf(s_w[i], base[size_t(i) * stride + dd], o0);
-      o1 = fmaf(s_w[i + 1], base[size_t(i + 1) * stride + dd], o1);
-      o2 = fmaf(s_w[i + 2], base[size_t(i + 2) * stride + dd], o2);
-      o3 = fmaf(s_w[i + 3], base[size_t(i + 3) * stride + dd], o3);
+  if (d_v % 4 == 0 && nsplit >= 8) {
+    // many splits: thread (r, c) takes float4 column c of splits r, r + rows,
+    // ...; every load is requested before the first use, then the rows are
+    // summed in order
+    __shared__ float4 s_part[256];
+    const int ncol = d_v / 4;  // <= 256 = blockDim.x
+    const int rows = int(blockDim.x) / ncol;
+    const int c = threadIdx.x % ncol, r = threadIdx.x / ncol;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < rows) {
+      constexpr int U = 8;
+      for (int i0 = r; i0 < nsplit; i0 += U * rows) {
+        float4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int i = i0 + u * rows;
+          v[u] = i < nsplit ? reinterpret_cast<const float4*>(base + size_t(i) * stride)[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int i = i0 + u * rows;
+          const float w = i < nsplit ? s_w[i] : 0.f;
+          acc.x = fmaf(w, v[u].x, acc.x);
+          acc.y = fmaf(w, v[u].y, acc.y);
+          acc.z = fmaf(w, v[u].z, acc.z);
+          acc.w = fmaf(w, v[u].w, acc.w);
+        }
+      }
+      s_part[threadIdx.x] = acc;
     }
-    for (; i < nsplit; ++i) o0 = fmaf(s_w[i], base[size_t(i) * stride + dd], o0);
-    store_out<E>(out + orow * d_v + dd, (o0 + o1) + (o2 + o3));
+    __syncthreads();
+    if (r == 0) {
+      for (int q = 1; q < rows; ++q) {
+        const float4 p = s_part[q * ncol + c];
+        acc.x += p.x;
+        acc.y += p.y;
+        acc.z += p.z;
+        acc.w += p.w;
+      }
+      typename E::T* o = out + orow * d_v + 4 * c;
+      store_out<E>(o + 0, acc.x);
+      store_out<E>(o + 1, acc.y);
+      store_out<E>(o + 2, acc.z);
+      store_out<E>(o + 3, acc.w);
+    }
+  } else {
+    for (int dd = threadIdx.x; dd < d_v; dd += blockDim.x) {
+      float o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;
+      int i = 0;
+      for (; i + 4 <= nsplit; i += 4) {
+        o0 = fmaf(s_w[i], base[size_t(i) * stride + dd], o0);
+        o1 = fmaf(s_w[i + 1], base[size_t(i + 1) * stride + dd], o1);
+        o2 = fmaf(s_w[i + 2], base[size_t(i + 2) * stride + dd], o2);
+        o3 = fmaf(s_w[i + 3], base[size_t(i + 3) * stride + dd], o3);
+      }
+      for (; i < nsplit; ++i) o0 = fmaf(s_w[i], base[size_t(i) * stride + dd], o0);
+      store_out<E>(out + orow * d_v + dd, (o0 + o1) + (o2 + o3));
+    }
   }
   if (threadIdx.x == 0 && lse) lse[orow] = s_lse;
 }
@@ -281,7 +328,7 @@ hipError_t launch_attention(const Problem& P, const void* q, const KvView& kv, c
 
 hipError_t launch_merge(const Problem& P, const float* po, const float* plse, int nsplit, void* out, float* lse,
                         hipStream_t st) {
-  const int threads = P.d_v >= 256 ? 256 : 128;
+  const int threads = 256;  // the float4 path assigns splits to rows of 256 / (d_v / 4) threads
   if (P.dtype == 1)
     merge_kernel<BF16><<<P.units * P.G, threads, 0, st>>>(po, plse, nsplit, P.G, P.d_v, P.H_q, P.H_kv,
                                                           (uint16_t*)out, lse);
