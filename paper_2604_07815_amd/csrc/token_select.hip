@@ -167,6 +167,28 @@ __global__ __launch_bounds__(256) void token_score_mfma_kernel(
   const int m = (n + B - 1) / B;
   const int S = K_b * B;
   const uint16_t* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
+  // the index rows of the four tiles' slots do not depend on q~: request them
+  // first, so their latency overlaps the q~ gather below
+  const int32_t* bl = block_ids + size_t(unit) * K_b;
+  bool valid[4];
+  uint32_t cx[4][NGR];
+  float2 pqv[4][NGR];
+#pragma unroll
+  for (int tl = 0; tl < 4; ++tl) {
+    const int slot = chunk * kTokenSlotsPerWG + w * 64 + tl * 16 + t16;
+    int tok = 0;
+    valid[tl] = slot < S && slot_token(bl, K_b, B, m, n, slot, &tok, err);
+    const size_t row = size_t(unit) * T + tok;
+#pragma unroll
+    for (int grp = 0; grp < NGR; ++grp) {
+      cx[tl][grp] = 0u;
+      pqv[tl][grp] = make_float2(0.f, 0.f);
+      if (valid[tl]) {
+        cx[tl][grp] = *reinterpret_cast<const uint32_t*>(codes + row * (DC / 2) + grp * 16 + lg * 4);
+        pqv[tl][grp] = *reinterpret_cast<const float2*>(qparams + (row * NGR + grp) * 2);
+      }
+    }
+  }
   for (int i = tid; i < G * DC; i += 256) {
     const int h = i / DC, x = i % DC;  // x = grp*32 + lg*8 + e (operand position)
     const int e = x & 7;
@@ -201,14 +223,10 @@ __global__ __launch_bounds__(256) void token_score_mfma_kernel(
 #pragma unroll
       for (int grp = 0; grp < NGR; ++grp) qs[ht][r][grp] = s_qs[(ht * 16 + lg * 4 + r) * NGR + grp];
 
-  const int32_t* bl = block_ids + size_t(unit) * K_b;
   float lgt[4][HT][4];  // [tile][ht][r]
 #pragma unroll
   for (int tl = 0; tl < 4; ++tl) {
     const int slot = chunk * kTokenSlotsPerWG + w * 64 + tl * 16 + t16;
-    int tok = 0;
-    const bool valid = slot < S && slot_token(bl, K_b, B, m, n, slot, &tok, err);
-    const size_t row = size_t(unit) * T + tok;
     ts_f32x4_t acc[HT][NGR];
 #pragma unroll
     for (int ht = 0; ht < HT; ++ht)
@@ -217,15 +235,9 @@ __global__ __launch_bounds__(256) void token_score_mfma_kernel(
     float sc[NGR], off[NGR];
 #pragma unroll
     for (int grp = 0; grp < NGR; ++grp) {
-      uint32_t x = 0;
-      sc[grp] = 0.f;
-      off[grp] = 0.f;
-      if (valid) {
-        x = *reinterpret_cast<const uint32_t*>(codes + row * (DC / 2) + grp * 16 + lg * 4);
-        const float2 pq = *reinterpret_cast<const float2*>(qparams + (row * NGR + grp) * 2);
-        sc[grp] = pq.x;
-        off[grp] = pq.y - 128.0f * pq.x;
-      }
+      const uint32_t x = cx[tl][grp];
+      sc[grp] = pqv[tl][grp].x;
+      off[grp] = pqv[tl][grp].y - 128.0f * pqv[tl][grp].x;
       const uint32_t lo = x & 0x0f0f0f0fu, hi = (x >> 4) & 0x0f0f0f0fu;
       const ts_u32x4_t bw = {__builtin_amdgcn_perm(kBase, lo, 0x04010400u), __builtin_amdgcn_perm(kBase, lo, 0x04030402u),
                              __builtin_amdgcn_perm(kBase, hi, 0x04010400u), __builtin_amdgcn_perm(kBase, hi, 0x04030402u)};
@@ -242,7 +254,7 @@ __global__ __launch_bounds__(256) void token_score_mfma_kernel(
         float v = 0.f;
 #pragma unroll
         for (int grp = 0; grp < NGR; ++grp) v += fmaf(sc[grp], acc[ht][grp][r], off[grp] * qs[ht][r][grp]);
-        lgt[tl][ht][r] = valid ? sigma * v : -INFINITY;
+        lgt[tl][ht][r] = valid[tl] ? sigma * v : -INFINITY;
       }
     if (slot < S) {
       float* lg_out = logits + size_t(unit) * G * S + slot;
