@@ -224,7 +224,8 @@ tls_status tls_calibrate_channels(const tls_layout* layout, const float* q_absma
  * tls_build_token_index over [tok_begin, tok_end) would after the copy (bit
  * for bit), from one read of each touched block.  Rows of those blocks
  * outside the range (earlier prefill chunks, or later rows already present)
- * are read from K.  Tokens at or past ctx_len are skipped.
+ * are read from K.  Tokens at or past ctx_len are skipped.  k_src and v_src
+ * must not overlap K or V.
  *   k_src  [b][tok_end - tok_begin][H_kv][d_qk]  dtype, token-major as a key
  *                                                projection produces it
  *   v_src  [b][tok_end - tok_begin][H_kv][d_v]   dtype; NULL iff mla_shared_kv
@@ -317,7 +318,10 @@ tls_status tls_prefetch_blocks(const tls_layout* layout, const void* host_k, con
  * host memory (the offloaded tier's host copy); the row is stored there by
  * the device.  Call once per decode step, after raising ctx_lens by one and
  * before the step's selection.  Sequences with ctx_lens 0 are skipped;
- * ctx_lens outside [0, max_ctx] and slots >= pool->n_slots are skipped. */
+ * ctx_lens outside [0, max_ctx] and slots >= pool->n_slots are skipped.
+ * Must not run concurrently with tls_prefetch_blocks on the same pool (order
+ * them with events: the prefetch of a step then sees the appended rows in
+ * host memory). */
 tls_status tls_append_tokens(const tls_layout* layout, const void* k_new, const void* v_new,
                              const int32_t* ctx_lens, const int32_t* channels, void* K, void* V, void* kmax,
                              void* kmin, uint8_t* codes, float* qparams, const tls_kv_view* pool,
