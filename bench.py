@@ -555,6 +555,32 @@ def main():
     dist_flush = step_distribution(50, flush_buf)
     del flush_buf
 
+    # ---- the same steps replayed from a HIP graph: one capture of a rotation over
+    # the layer copies, as a serving loop that captures its step would run it ------
+    def graph_replay_us():
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for i in range(len(layers)):
+                step(i)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(len(layers)):
+                step(i)
+        reps = max(1, args.steps // len(layers))
+        graph.replay()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(reps):
+            graph.replay()
+        stop.record()
+        torch.cuda.synchronize()
+        return round(start.elapsed_time(stop) * 1e3 / (reps * len(layers)), 2)
+
+    graph_us = graph_replay_us()
+
     # ---- per-stage timing with HIP events on the launch stream --------------------
     hev = HipEvents()
     evs = [hev.create(tls.NUM_STAGE_EVENTS) for _ in range(args.steps)]
@@ -661,6 +687,7 @@ def main():
         "algorithmic_bytes_per_step": nb,
         "step_us_distribution": dist,
         "step_us_after_1GiB_flush": dist_flush,
+        "step_us_graph_replay": graph_us,
         "stage_us": {k: round(float(v) * 1e3, 2) for k, v in zip(STAGES, stage_ms)},
         "stage_marked_step_us": round(marked_ms * 1e3, 2),
         "prefill": prefill,
