@@ -20,9 +20,11 @@ __all__ = [
     "TlsError", "Layout", "KvView", "KV", "DecodeOpts", "NUM_STAGE_EVENTS", "LIB_PATH",
     "tls_version", "tls_status_string", "tls_workspace_size", "tls_workspace_init",
     "tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
-    "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error",
+    "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error", "tls_prefill_kv", "tls_offload_kv",
+    "tls_init_residency", "tls_calibrate_absmax", "tls_calibrate_channels", "tls_append_tokens",
     "make_layout", "alloc_workspace", "DTYPE_F32", "DTYPE_BF16", "EXPORTED_SYMBOLS",
     "MODE_TWO_LEVEL", "MODE_BLOCK_SPARSE", "MODE_DENSE", "MODE_TOKEN_SPARSE",
+    "DEVERR_CTX_LEN", "DEVERR_BLOCK_ID", "DEVERR_TOKEN_ID", "DEVERR_SLOT", "DEVERR_POOL_FULL", "DEVERR_CHANNEL",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtls.so")

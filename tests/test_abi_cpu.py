@@ -41,6 +41,9 @@ def test_library_exports_every_declared_symbol(tls):
     for n in declared_functions():
         assert hasattr(lib, n), f"libtls.so does not export {n}"
     assert set(declared_functions()) == set(tls.EXPORTED_SYMBOLS)
+    # the binding wraps every entry point under its C name and exports it
+    for n in tls.EXPORTED_SYMBOLS:
+        assert callable(getattr(tls, n, None)) and n in tls.__all__, n
 
 
 def test_version_and_status_strings(tls):
