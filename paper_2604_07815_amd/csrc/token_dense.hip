@@ -43,6 +43,7 @@ __global__ __launch_bounds__(kDsThreads) void ds_score_kernel(
   __shared__ float s_red[kDsNW][G][2];
   __shared__ float s_mz[G][2];
   __shared__ float s_tmp[kDsThreads];
+  __shared__ int s_ch[kDsMaxDc];
   const int chunk = blockIdx.x, unit = blockIdx.y;
   const int s = unit / H_kv, g = unit % H_kv;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -54,14 +55,19 @@ __global__ __launch_bounds__(kDsThreads) void ds_score_kernel(
   const int j0 = chunk * CH;
   if (pass == 1 && j0 >= n) return;
   const int ngr = d_c / 32;
-  for (int i = tid; i < G * d_c; i += kDsThreads) {
-    const int h = i / d_c, c = i % d_c;
+  // the group's channel ids once (every head uses the same), then the q~ gather
+  for (int c = tid; c < d_c; c += kDsThreads) {
     int ch = channels[g * d_c + c];
     if (ch < 0 || ch >= d) {
       set_error(err, 32u);
       ch = 0;
     }
-    s_q[c * G + h] = E::to_f(q[(size_t(s) * H_q + size_t(g) * G + h) * d + ch]);
+    s_ch[c] = ch;
+  }
+  __syncthreads();
+  for (int i = tid; i < G * d_c; i += kDsThreads) {
+    const int h = i / d_c, c = i % d_c;
+    s_q[c * G + h] = E::to_f(q[(size_t(s) * H_q + size_t(g) * G + h) * d + s_ch[c]]);
   }
   __syncthreads();
   for (int i = tid; i < G * ngr; i += kDsThreads) {

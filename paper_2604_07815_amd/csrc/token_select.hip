@@ -30,6 +30,7 @@ __global__ __launch_bounds__(256) void token_score_kernel(
   __shared__ float s_qt[kMaxG * 256];
   __shared__ float s_qsum[kMaxG * kMaxGroups];
   __shared__ float s_red[4 * kMaxG];
+  __shared__ int s_ch[kMaxGroups * 32];
   const int unit = blockIdx.y, chunk = blockIdx.x;
   const int s = unit / H_kv, g = unit % H_kv;
   int n = ctx_lens[s];
@@ -38,14 +39,19 @@ __global__ __launch_bounds__(256) void token_score_kernel(
   const int ngr = d_c / 32;
   const int S = K_b * B;
   const typename E::T* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
-  for (int i = threadIdx.x; i < G * d_c; i += 256) {
-    const int h = i / d_c, c = i % d_c;
-    int ch = channels[g * d_c + c];
+  // the group's channel ids once (every head uses the same), then the q~ gather
+  if (threadIdx.x < d_c) {
+    int ch = channels[g * d_c + threadIdx.x];
     if (ch < 0 || ch >= d) {  // caller-supplied channel id out of range
       set_error(err, 32u);
       ch = 0;
     }
-    s_qt[i] = E::to_f(qg[size_t(h) * d + ch]);
+    s_ch[threadIdx.x] = ch;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < G * d_c; i += 256) {
+    const int h = i / d_c, c = i % d_c;
+    s_qt[i] = E::to_f(qg[size_t(h) * d + s_ch[c]]);
   }
   __syncthreads();
   for (int i = threadIdx.x; i < G * ngr; i += 256) {
@@ -158,6 +164,7 @@ __global__ __launch_bounds__(256) void token_score_mfma_kernel(
   __shared__ __attribute__((aligned(16))) uint16_t s_qt[G * DC];
   __shared__ float s_qs[G * NGR];
   __shared__ float s_red[4][G][2];
+  __shared__ int s_ch[DC];
   const int unit = blockIdx.y, chunk = blockIdx.x;
   const int s = unit / H_kv, g = unit % H_kv;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -189,16 +196,31 @@ __global__ __launch_bounds__(256) void token_score_mfma_kernel(
       }
     }
   }
-  for (int i = tid; i < G * DC; i += 256) {
-    const int h = i / DC, x = i % DC;  // x = grp*32 + lg*8 + e (operand position)
-    const int e = x & 7;
-    const int c = (x & ~7) + ((e & 3) << 1) + (e >> 2);  // channel index of that position
-    int ch = channels[g * DC + c];
+  // the group's channel ids once (every head uses the same), then all of the
+  // work-group's q~ values requested together
+  if (tid < DC) {
+    int ch = channels[g * DC + tid];
     if (ch < 0 || ch >= d) {
       set_error(err, 32u);
       ch = 0;
     }
-    s_qt[i] = qg[size_t(h) * d + ch];
+    s_ch[tid] = ch;
+  }
+  __syncthreads();
+  {
+    constexpr int PER = G * DC / 256;
+    static_assert(PER * 256 == G * DC, "q~ entries per thread");
+    uint16_t qv[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int i = tid + j * 256;
+      const int h = i / DC, x = i % DC;  // x = grp*32 + lg*8 + e (operand position)
+      const int e = x & 7;
+      const int c = (x & ~7) + ((e & 3) << 1) + (e >> 2);  // channel index of that position
+      qv[j] = qg[size_t(h) * d + s_ch[c]];
+    }
+#pragma unroll
+    for (int j = 0; j < PER; ++j) s_qt[tid + j * 256] = qv[j];
   }
   __syncthreads();
   for (int i = tid; i < G * NGR; i += 256) {
