@@ -392,11 +392,12 @@ def offload_schedule(tls, synth, torch, np):
     rec = []
     for t in range(1, walk.shape[0]):
         M_prev, M_t = M[(t - 1) % 2], M[t % 2]
-        e0, e_sel, e_dec, e1, p0, p1 = ev(), ev(), ev(), ev(), ev(), ev()
+        e0, e_app, e_sel, e_dec, e1, p0, p1 = ev(), ev(), ev(), ev(), ev(), ev(), ev()
+        k_new, v_new = k_future[:, :, t - 1].contiguous(), v_future[:, :, t - 1].contiguous()
         e0.record(main)
         ctx += 1  # the token generated by the previous step joins the context
-        tls.tls_append_tokens(layout, k_future[:, :, t - 1].contiguous(), v_future[:, :, t - 1].contiguous(), ctx, ch,
-                              host_k, host_v, kmax, kmin, codes, qparams, pool=kv)
+        tls.tls_append_tokens(layout, k_new, v_new, ctx, ch, host_k, host_v, kmax, kmin, codes, qparams, pool=kv)
+        e_app.record(main)
         tls.tls_select_blocks(layout, qs[t], kmax, kmin, ctx, K_b, M_t, None, ws)
         e_sel.record(main)
         side.wait_event(e_sel)
@@ -411,8 +412,26 @@ def offload_schedule(tls, synth, torch, np):
         e1.record(main)
         e1.synchronize()
         moved = int(tcount.sum().item())
-        rec.append(dict(wall=e0.elapsed_time(e1) * 1e3, select=e0.elapsed_time(e_sel) * 1e3,
-                        decode=e_sel.elapsed_time(e_dec) * 1e3, xfer=p0.elapsed_time(p1) * 1e3, blocks=moved))
+        rec.append(dict(wall=e0.elapsed_time(e1) * 1e3, append=e0.elapsed_time(e_app) * 1e3,
+                        select=e_app.elapsed_time(e_sel) * 1e3, decode=e_sel.elapsed_time(e_dec) * 1e3,
+                        xfer=p0.elapsed_time(p1) * 1e3, blocks=moved))
+    # the same decode call (block selection, then token selection from the
+    # resident blocks and attention over the pool) with no transfer running
+    M_last = M[(walk.shape[0] - 1) % 2]
+    M_tmp = torch.empty_like(M_last)
+    n_quiet = 40
+    q0, q1 = ev(), ev()
+    torch.cuda.synchronize()
+    q0.record(main)
+    for _ in range(n_quiet):
+        tls.tls_select_blocks(layout, qs[-1], kmax, kmin, ctx, K_b, M_tmp, None, ws)
+        tls.tls_sparse_decode(layout, qs[-1], kv, ctx, kmax, kmin, codes, qparams, ch, K_b, cfg.k_t, M_last, None,
+                              out, None, None, None, ws)
+    q1.record(main)
+    torch.cuda.synchronize()
+    quiet_us = q0.elapsed_time(q1) * 1e3 / n_quiet
+    ctx_now = ctx.cpu().numpy()
+    step_bytes = algorithmic_bytes(cfg, ctx_now, M_last.cpu().numpy(), 2)["total"]
     err = tls.tls_check_device_error(ws)
     block_bytes = B * (cfg.d_qk + cfg.d_v) * 2
     med = lambda k: float(np.median([r[k] for r in rec]))  # noqa: E731
@@ -425,8 +444,12 @@ def offload_schedule(tls, synth, torch, np):
                     f"block summary, token-index row); K/V {2 * host_k.numel() * 2 / 1e9:.1f} GB "
                     f"in pinned host memory, pool of {n_slots} slots per unit in HBM",
         "step_wall_us_median": round(med("wall"), 1),
+        "append_us_median": round(med("append"), 1),
         "select_blocks_us_median": round(med("select"), 1),
         "decode_from_pool_us_median": round(med("decode"), 1),
+        "decode_call_with_transfer_us_median": round(med("select") + med("decode"), 1),
+        "decode_call_no_transfer_us": round(quiet_us, 1),
+        "decode_call_no_transfer_frac_of_peak_hbm": round(step_bytes / (quiet_us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
         "transfer_us_median": round(med("xfer"), 1),
         "blocks_moved_per_step_mean": round(blocks, 1),
         "block_repeat_rate": round(1.0 - blocks / (units * K_b), 4),
