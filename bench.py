@@ -474,7 +474,7 @@ def main():
         pmc_summary(*args.pmc_summary)
         return
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: the library runs on one GPU only (asked for --gpus {args.gpus}); "
               "the operator shards by (sequence, KV head) without cross-GPU exchange, "
               "so per-GPU throughput is the single-GPU figure", file=sys.stderr)
         sys.exit(2)

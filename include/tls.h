@@ -64,7 +64,7 @@ typedef int32_t tls_status;
 enum {
   TLS_OK = 0,
   TLS_ERR_INVALID_ARGUMENT = 1,   /* null pointer, bad shape, bad budget        */
-  TLS_ERR_UNSUPPORTED = 2,        /* valid request this build does not handle  */
+  TLS_ERR_UNSUPPORTED = 2,        /* valid request the library does not handle */
   TLS_ERR_WORKSPACE_TOO_SMALL = 3,
   TLS_ERR_HIP = 4                 /* a HIP runtime call or launch failed        */
 };

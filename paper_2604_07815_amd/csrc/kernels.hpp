@@ -18,7 +18,7 @@ struct Problem {
   int units;  // b * H_kv
 };
 
-// Capacity limits of this build (host validation rejects larger requests).
+// Capacity limits of the library (host validation rejects larger requests).
 constexpr int kMaxKeys = 12288;     // blocks per sequence, and K_b * B candidate slots
 constexpr int kMaxSplits = 128;     // attention splits per unit
 constexpr int kMaxGroupGqa = 8;     // G for the VALU attention path

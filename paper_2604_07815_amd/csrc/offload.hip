@@ -134,7 +134,7 @@ __device__ inline void copy_block_rows(const uint8_t* __restrict__ src, uint8_t*
     const size_t o = (size_t(i) * kCopyThreads + threadIdx.x) * 16;
     if (o < bytes) *reinterpret_cast<uint4*>(dst + o) = v[i];
   }
-  // rows larger than the unrolled span (not used by the shapes of this build)
+  // rows larger than the unrolled span (not used by the supported shapes)
   for (size_t o = (size_t(kCopyPieces) * kCopyThreads + threadIdx.x) * 16; o < bytes; o += kCopyThreads * 16)
     *reinterpret_cast<uint4*>(dst + o) = ld16(src + o);
 }

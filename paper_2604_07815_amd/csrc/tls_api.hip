@@ -26,7 +26,7 @@ tls_status make_problem(const tls_layout* L, Problem* P) {
   if (L->mla_shared_kv != 0 && L->mla_shared_kv != 1) return TLS_ERR_INVALID_ARGUMENT;
   if (L->mla_shared_kv && L->head_dim_v > L->head_dim_qk) return TLS_ERR_INVALID_ARGUMENT;
   if (!(L->softmax_scale == L->softmax_scale) || isinf(L->softmax_scale)) return TLS_ERR_INVALID_ARGUMENT;
-  // supported subset of this build
+  // supported subset of the library
   if (L->block_size != 64) return TLS_ERR_UNSUPPORTED;
   if (L->head_dim_qk % 8 != 0 || L->head_dim_qk > 1024) return TLS_ERR_UNSUPPORTED;
   if (L->index_channels > 256) return TLS_ERR_UNSUPPORTED;

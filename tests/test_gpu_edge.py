@@ -111,7 +111,7 @@ def test_wide_split_attention(splits):
 
 @pytest.mark.parametrize("k_b,k_t", [(128, 2048), (192, 4096)])
 def test_capacity_limits(k_b, k_t):
-    """The largest shapes this build accepts: 131072 tokens (2048 blocks, the
+    """The largest shapes the library accepts: 131072 tokens (2048 blocks, the
     fused selection's block capacity) with 8192 candidates, and 12288
     candidates (K_b = 192, the general selection path's key capacity) with
     K_t = 4096; sampled units against the oracle."""
