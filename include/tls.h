@@ -31,9 +31,10 @@
  * - Results are deterministic run to run: fixed reduction orders and no
  *   floating-point atomics.
  * - Every call except tls_check_device_error enqueues kernels only (no
- *   memset or copy nodes, no host round trip), so a serving step (append +
- *   decode, or prefetch + decode) can be captured into a HIP graph and
- *   replayed.  Calls that share a workspace must not run concurrently.
+ *   memset or copy nodes, no host round trip), so a serving step can be
+ *   captured into a HIP graph and replayed (the tests replay decode steps
+ *   and append + decode steps).  Calls that share a workspace must not run
+ *   concurrently.
  * - Unit = one (sequence, KV head) pair; "units" = batch * num_kv_heads.
  *   Query head h belongs to KV head floor(h / G), G = num_q_heads / num_kv_heads.
  *
