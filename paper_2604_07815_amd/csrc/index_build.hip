@@ -398,10 +398,124 @@ static hipError_t launch_index_rows(const Problem& P, const void* k_src, const v
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Block summaries alone (the standalone block-index build): no staging tile.
+// A work-group takes kSumBlocks consecutive blocks of one unit; thread
+// (row group rg, 16-byte column c) folds the rows rg, rg + nrg, ... of a block
+// in registers with four loads in flight, the nrg partials are combined
+// through LDS, and the first cpr threads write the block's max and min rows
+// (fmax / fmin over the block's valid rows, -0 written as +0, as the fused
+// builder does).  Blocks with no valid row are left untouched.
+// ---------------------------------------------------------------------------
+constexpr int kSumThreads = 256;
+constexpr int kSumBlocks = 4;  // blocks per work-group
+
+template <class E>
+__global__ __launch_bounds__(kSumThreads) void block_summary_kernel(
+    const uint8_t* __restrict__ K, const int32_t* __restrict__ ctx_lens, int H_kv, int T, int d, int B, int m_max,
+    int tok_begin, int tok_end, uint8_t* __restrict__ kmax, uint8_t* __restrict__ kmin, uint32_t* err) {
+  constexpr int V = E::kVec;  // elements per 16 bytes
+  __shared__ float s_mx[kSumThreads][V], s_mn[kSumThreads][V];
+  const int s = blockIdx.z, g = blockIdx.y, tid = threadIdx.x;
+  int n = ctx_lens[s];
+  if (n < 0 || n > T) {
+    if (tid == 0 && blockIdx.x == 0 && g == 0) set_error(err, 1u);
+    n = n < 0 ? 0 : T;
+  }
+  const int hi = min(tok_end, n);
+  const size_t unit = size_t(s) * H_kv + g;
+  const int rb = d * int(sizeof(typename E::T));  // bytes per row (multiple of 16)
+  const int cpr = rb / 16;                         // <= 256
+  const int nrg = kSumThreads / cpr;
+  const int c = tid % cpr, rg = tid / cpr;
+  const int first = tok_begin / B + int(blockIdx.x) * kSumBlocks;
+  for (int bi = 0; bi < kSumBlocks; ++bi) {
+    const int i = first + bi;
+    const int r0 = i * B;
+    if (r0 >= hi) break;  // past the valid end of the range (uniform)
+    const int nr = min(r0 + B, n) - r0;
+    float mx[V], mn[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      mx[e] = -INFINITY;
+      mn[e] = INFINITY;
+    }
+    auto fold = [&](const uint4& x) {
+      float f[V];
+      unpack16<E>(x, f);
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        mx[e] = fmaxf(mx[e], f[e]);
+        mn[e] = fminf(mn[e], f[e]);
+      }
+    };
+    if (rg < nrg) {
+      const uint8_t* base = K + (unit * T + r0) * size_t(rb) + size_t(c) * 16;
+      int r = rg;
+      for (; r + 3 * nrg < nr; r += 4 * nrg) {
+        uint4 x[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) x[u] = ld16_stream(base + size_t(r + u * nrg) * rb);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) fold(x[u]);
+      }
+      for (; r < nr; r += nrg) fold(ld16_stream(base + size_t(r) * rb));
+    }
+    if (bi > 0) __syncthreads();  // the previous block's partials have been read
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      s_mx[tid][e] = mx[e];
+      s_mn[tid][e] = mn[e];
+    }
+    __syncthreads();
+    if (tid < cpr) {
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        mx[e] = s_mx[tid][e];
+        mn[e] = s_mn[tid][e];
+      }
+      for (int q = 1; q < nrg; ++q) {
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+          mx[e] = fmaxf(mx[e], s_mx[q * cpr + tid][e]);
+          mn[e] = fminf(mn[e], s_mn[q * cpr + tid][e]);
+        }
+      }
+      uint32_t wx[4], wn[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if constexpr (E::kIsBf16) {
+          wx[k] = uint32_t(f32_to_bf16(mx[2 * k] + 0.0f)) | (uint32_t(f32_to_bf16(mx[2 * k + 1] + 0.0f)) << 16);
+          wn[k] = uint32_t(f32_to_bf16(mn[2 * k] + 0.0f)) | (uint32_t(f32_to_bf16(mn[2 * k + 1] + 0.0f)) << 16);
+        } else {
+          wx[k] = __float_as_uint(mx[k] + 0.0f);
+          wn[k] = __float_as_uint(mn[k] + 0.0f);
+        }
+      }
+      const size_t off = (unit * m_max + i) * size_t(rb) + size_t(tid) * 16;
+      *reinterpret_cast<uint4*>(kmax + off) = make_uint4(wx[0], wx[1], wx[2], wx[3]);
+      *reinterpret_cast<uint4*>(kmin + off) = make_uint4(wn[0], wn[1], wn[2], wn[3]);
+    }
+  }
+}
+
 hipError_t launch_block_index(const Problem& P, const void* K, const int32_t* ctx_lens, int tok_begin,
                               int tok_end, void* kmax, void* kmin, uint32_t* err, hipStream_t st) {
-  return launch_index_rows(P, nullptr, nullptr, const_cast<void*>(K), nullptr, ctx_lens, nullptr, tok_begin,
-                           tok_end, kmax, kmin, nullptr, nullptr, kIdxBlock, err, st);
+  const int rb = P.d_qk * (P.dtype == 1 ? 2 : 4);
+  if (rb % 16 != 0 || rb / 16 > kSumThreads)  // not the shapes the library accepts; the general builder
+    return launch_index_rows(P, nullptr, nullptr, const_cast<void*>(K), nullptr, ctx_lens, nullptr, tok_begin,
+                             tok_end, kmax, kmin, nullptr, nullptr, kIdxBlock, err, st);
+  const int nblk = (tok_end + P.B - 1) / P.B - tok_begin / P.B;  // blocks overlapping the range
+  dim3 grid(unsigned((nblk + kSumBlocks - 1) / kSumBlocks), unsigned(P.H_kv), unsigned(P.b));
+  if (P.dtype == 1)
+    block_summary_kernel<BF16><<<grid, kSumThreads, 0, st>>>((const uint8_t*)K, ctx_lens, P.H_kv, P.T, P.d_qk, P.B,
+                                                             P.m_max, tok_begin, tok_end, (uint8_t*)kmax,
+                                                             (uint8_t*)kmin, err);
+  else
+    block_summary_kernel<F32><<<grid, kSumThreads, 0, st>>>((const uint8_t*)K, ctx_lens, P.H_kv, P.T, P.d_qk, P.B,
+                                                            P.m_max, tok_begin, tok_end, (uint8_t*)kmax,
+                                                            (uint8_t*)kmin, err);
+  return hipGetLastError();
 }
 
 hipError_t launch_token_index(const Problem& P, const void* K, const int32_t* ctx_lens,
