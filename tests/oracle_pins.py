@@ -188,6 +188,48 @@ def pin_alpha_distribution(seed=15):
     assert list(ids) == list(ref)
 
 
+def pin_channel_projection_golden():
+    """Hand-derived logits and alpha~ with a channel set that is not a prefix
+    of the channels: the query side is gathered at C (q~ = q[C])."""
+    g = _golden("channel_projection_tiny.json")
+    q = np.array(g["queries"], dtype=np.float64)
+    xhat = np.array(g["xhat"], dtype=np.float64)
+    lg = O.token_logits(q, np.array(g["channels"]), xhat, g["sigma"])
+    np.testing.assert_array_equal(lg, np.array(g["logits"], dtype=np.float64))
+    a = O.approx_scores(lg)
+    np.testing.assert_allclose(a, g["alpha"], atol=g["abs_tol"], rtol=0)
+    assert list(O.topk_ascending(a, 1)) == g["top1"]
+
+
+def pin_channel_projection_property(seed=19):
+    """The token selection reads the query only at the channels of C: noise
+    added to the other channels changes neither alpha~ nor S_t, while a query
+    that is zero on C (and arbitrary elsewhere) gives the uniform alpha~ of a
+    zero query, whose top-k is the lowest candidate positions.  C is a random,
+    non-contiguous subset, quantisation on."""
+    r = np.random.default_rng(seed)
+    d, n, B, G, k_t = 96, 300, 16, 3, 20
+    K = synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(r.standard_normal((n, d)).astype(np.float32)))
+    C = np.sort(r.choice(np.arange(1, d), size=32, replace=False))
+    assert not np.array_equal(C, np.arange(32))
+    codes, qp = O.token_index(K, n, C)
+    blocks = np.array([0, 3, 7, 11, 18])
+    sigma = 1.0 / math.sqrt(d)
+    q = r.standard_normal((G, d))
+    off = np.setdiff1d(np.arange(d), C)
+    q_noise = q.copy()
+    q_noise[:, off] += 5.0 * r.standard_normal((G, len(off)))
+    ids, alpha, cand = O.select_tokens(q, C, codes, qp, blocks, n, B, k_t, sigma)
+    ids2, alpha2, _ = O.select_tokens(q_noise, C, codes, qp, blocks, n, B, k_t, sigma)
+    np.testing.assert_array_equal(alpha2, alpha)
+    np.testing.assert_array_equal(ids2, ids)
+    q_off = np.zeros_like(q)
+    q_off[:, off] = r.standard_normal((G, len(off)))
+    ids3, alpha3, cand3 = O.select_tokens(q_off, C, codes, qp, blocks, n, B, k_t, sigma)
+    np.testing.assert_array_equal(alpha3, np.full(len(cand3), 1.0 / len(cand3)))
+    np.testing.assert_array_equal(ids3, cand3[:k_t])
+
+
 # --- attention -------------------------------------------------------------------
 
 def pin_attention_library(seed=16):
@@ -468,7 +510,7 @@ def pin_calibration_properties(seed=17):
 ALL_PINS = [
     pin_quest_golden, pin_quest_forms_agree, pin_quest_upper_bound, pin_topk_bruteforce,
     pin_candidates, pin_quant_golden, pin_quant_bound, pin_alpha_golden, pin_alpha_distribution,
-    pin_attention_library, pin_attention_closed_form, pin_dense_equivalence,
+    pin_channel_projection_golden, pin_channel_projection_property, pin_attention_library, pin_attention_closed_form, pin_dense_equivalence,
     pin_invariants_and_planted, pin_single_level_operators, pin_lagged_schedule, pin_lagged_schedule_growth,
     pin_calibration_golden,
     pin_calibration_properties,

@@ -74,6 +74,14 @@ def _wrong_candidates(block_ids, n, B):      # ignores the ragged tail
 
 _REAL_ATTN = O.sparse_attention
 
+
+def _logits_prefix_channels(q, channels, xhat, sigma):   # q~ = q[:, :d_c] instead of q[:, C]
+    return sigma * (q[:, :len(channels)] @ xhat.T)
+
+
+def _logits_no_sigma(q, channels, xhat, sigma):          # forgets the scale in the approximate score
+    return q[:, np.asarray(channels)] @ xhat.T
+
 def _absmax_signed(x):                       # max of x instead of max of |x|
     x = np.asarray(x, dtype=np.float64)
     return np.zeros(x.shape[1:]) if x.shape[0] == 0 else x.max(axis=0)
@@ -92,6 +100,8 @@ MUTATIONS = [
     ("block_summaries", _floor_blocks),
     ("approx_scores", _single_softmax),
     ("approx_scores", _no_mean),
+    ("token_logits", _logits_prefix_channels),
+    ("token_logits", _logits_no_sigma),
     ("quantize_group", _floor_quant),
     ("pack_codes", _high_nibble_first),
     ("topk_ascending", _ties_high),
