@@ -397,14 +397,15 @@ def lagged_decode(q_steps, K, V, n, channels, k_b, k_t, B, sigma, d_v, mla=False
             kmax, kmin = block_summaries(Ku, nt, B)
             index, index_n = token_index(Ku, nt, channels), nt
         qg = q_steps[t, s, g * G:(g + 1) * G]
-        M_t, _ = select_blocks(qg, kmax, kmin, k_b)
-        S_t, _, _ = select_tokens(qg, channels, index[0], index[1], M_prev, nt, B, k_t, sigma)
+        M_t, bscores = select_blocks(qg, kmax, kmin, k_b)
+        S_t, alpha, cand = select_tokens(qg, channels, index[0], index[1], M_prev, nt, B, k_t, sigma)
         o, lse = sparse_attention(qg, Ku, Vu, S_t, sigma)
         Mset = set(int(x) for x in M_t)
         transfer = sorted(Mset - resident)
         repeat = len(Mset & set(int(x) for x in M_prev)) / max(1, len(Mset))
-        steps.append(dict(block_ids=M_t, lag_block_ids=M_prev, token_ids=S_t, out=o, lse=lse,
-                          transfer=np.asarray(transfer, dtype=np.int64), repeat=repeat))
+        steps.append(dict(block_ids=M_t, block_scores=bscores, lag_block_ids=M_prev, token_ids=S_t, alpha=alpha,
+                          cand=cand, out=o, lse=lse, transfer=np.asarray(transfer, dtype=np.int64),
+                          repeat=repeat, index=index))
         resident = Mset
         M_prev = M_t
     return steps

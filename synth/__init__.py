@@ -32,6 +32,7 @@ __all__ = [
     "DecodeConfig", "CONFIGS", "config", "f32_to_bf16_bits", "bf16_bits_to_f32",
     "to_f64", "draw_ctx_lens", "draw_channels", "draw_plant_starts",
     "draw_queries", "draw_query_walk", "planted_key", "make_host", "make_device",
+    "plant_tie_blocks", "plant_tie_tokens", "draw_block_lists",
 ]
 
 
@@ -323,6 +324,93 @@ def make_device(cfg: DecodeConfig, device="cuda", pad: str = "zero",
                 channels=torch.from_numpy(ch).to(device),
                 plant_starts=starts, planted_key=pk, q_host=q,
                 ctx_host=ctx, channels_host=ch)
+
+
+# ----------------------------------------------------------------------------
+# Inputs with exact ties at the selection cuts
+# ----------------------------------------------------------------------------
+
+def plant_tie_blocks(cfg: DecodeConfig, k: np.ndarray, ctx_lens: np.ndarray, n_hi: int, n_dup: int,
+                     hi_scale: float = 5.0, dup_scale: float = 3.0, seed_offset: int = 800):
+    """Per (sequence, KV head): n_hi blocks whose rows are the drawn rows
+    times hi_scale, and n_dup blocks that are byte-identical copies of one
+    block whose rows are the drawn rows times dup_scale, at seeded distinct
+    positions among the sequence's full blocks.  Identical blocks have
+    identical summaries, so any block budget between n_hi and n_hi + n_dup
+    cuts through a group of exactly equal block scores.
+
+    k: storage-form [b][h_kv][T][d] (modified in place).  Returns
+    (hi [b][h_kv][n_hi], dup [b][h_kv][n_dup]), ascending block ids."""
+    r = _rng(cfg.seed + seed_offset)
+    B = cfg.block
+    hi = np.zeros((cfg.batch, cfg.h_kv, n_hi), dtype=np.int64)
+    dup = np.zeros((cfg.batch, cfg.h_kv, n_dup), dtype=np.int64)
+    for s in range(cfg.batch):
+        full = int(ctx_lens[s]) // B
+        assert full >= n_hi + n_dup, "not enough full blocks for the tie layout"
+        for g in range(cfg.h_kv):
+            pick = r.choice(full, size=n_hi + n_dup, replace=False)
+            hi[s, g] = np.sort(pick[:n_hi])
+            dup[s, g] = np.sort(pick[n_hi:])
+            rows = k[s, g]
+            for b in hi[s, g]:
+                x = to_f64(rows[b * B:(b + 1) * B], cfg.dtype) * hi_scale
+                rows[b * B:(b + 1) * B] = _store(x.astype(np.float32), cfg.dtype)
+            t0 = int(dup[s, g, 0])
+            tmpl = _store((to_f64(rows[t0 * B:(t0 + 1) * B], cfg.dtype) * dup_scale).astype(np.float32), cfg.dtype)
+            for b in dup[s, g]:
+                rows[b * B:(b + 1) * B] = tmpl
+    return hi, dup
+
+
+def draw_block_lists(cfg: DecodeConfig, ctx_lens: np.ndarray, k_b: int, seed_offset: int = 820) -> np.ndarray:
+    """A seeded ascending list of k_b distinct blocks per (sequence, KV head),
+    [b][h_kv][k_b] (a given block selection for the token stage)."""
+    r = _rng(cfg.seed + seed_offset)
+    out = np.zeros((cfg.batch, cfg.h_kv, k_b), dtype=np.int32)
+    for s in range(cfg.batch):
+        m = -(-int(ctx_lens[s]) // cfg.block)
+        for g in range(cfg.h_kv):
+            out[s, g] = np.sort(r.choice(m, size=k_b, replace=False))
+    return out
+
+
+def plant_tie_tokens(cfg: DecodeConfig, q_store: np.ndarray, k: np.ndarray, ctx_lens: np.ndarray,
+                     channels: np.ndarray, blocks: Optional[np.ndarray], n_a: int, n_b: int, dot_a: float,
+                     dot_b: float, seed_offset: int = 850):
+    """Per (sequence, KV head): n_a tokens with the key dot_a * w and n_b
+    tokens with the key dot_b * w, where w is the least-norm vector on the
+    channels of the head's index set C (zero elsewhere) whose dot product
+    with every query of the group is 1, so that every head sees them with
+    the dot products dot_a and dot_b (up to the storage rounding).  Positions are
+    seeded, distinct, valid tokens of `blocks[s][g]` (every block when None).
+    Rows of one kind are byte-identical, so a token budget between n_a and
+    n_a + n_b cuts through a group of exactly equal approximate scores.
+
+    k: storage-form [b][h_kv][T][d] (modified in place).  Returns
+    (pos_a [b][h_kv][n_a], pos_b [b][h_kv][n_b]), ascending positions."""
+    r = _rng(cfg.seed + seed_offset)
+    B = cfg.block
+    q = to_f64(q_store, cfg.dtype).reshape(cfg.batch, cfg.h_kv, cfg.group, cfg.d_qk)
+    pa = np.zeros((cfg.batch, cfg.h_kv, n_a), dtype=np.int64)
+    pb = np.zeros((cfg.batch, cfg.h_kv, n_b), dtype=np.int64)
+    for s in range(cfg.batch):
+        n = int(ctx_lens[s])
+        for g in range(cfg.h_kv):
+            if blocks is None:
+                cand = np.arange(n)
+            else:
+                cand = np.array([b * B + o for b in blocks[s, g] if b >= 0 for o in range(B) if b * B + o < n])
+            pick = r.choice(cand, size=n_a + n_b, replace=False)
+            pa[s, g] = np.sort(pick[:n_a])
+            pb[s, g] = np.sort(pick[n_a:])
+            w = np.zeros(cfg.d_qk)
+            C = channels[g]
+            w[C] = np.linalg.pinv(q[s, g][:, C]) @ np.ones(cfg.group)
+            rows = k[s, g]
+            rows[pa[s, g]] = _store((dot_a * w).astype(np.float32), cfg.dtype)
+            rows[pb[s, g]] = _store((dot_b * w).astype(np.float32), cfg.dtype)
+    return pa, pb
 
 
 def host_to_torch(arr: np.ndarray, dtype: str):

@@ -27,10 +27,10 @@ SMALL = {
                                                       k_t=200, seed=4100), "host", None),
 }
 FULL = {
-    "qwen3_gqa_48k": (synth.config("qwen3_gqa_48k"), None),
-    "batched_gqa": (synth.config("batched_gqa"), 6),
-    "mla": (synth.config("mla"), 3),
-    "offload_gqa_96k": (synth.config("offload_gqa_96k"), 3),
+    "qwen3_gqa_48k": (synth.config("qwen3_gqa_48k"), None),   # all 8 units
+    "batched_gqa": (synth.config("batched_gqa"), 32),          # 32 of 128 units
+    "mla": (synth.config("mla"), None),                        # all 8 units
+    "offload_gqa_96k": (synth.config("offload_gqa_96k"), 32),  # 32 of 256 units
 }
 ALL = list(SMALL) + list(FULL)
 
@@ -74,7 +74,7 @@ def test_index_bit_exact(name):
         m = kmax.shape[0]
         np.testing.assert_array_equal(synth.torch_to_f64(c.kmax[s, g, :m]), kmax, err_msg=f"kmax {(s, g)}")
         np.testing.assert_array_equal(synth.torch_to_f64(c.kmin[s, g, :m]), kmin, err_msg=f"kmin {(s, g)}")
-        codes, qp = O.token_index(Ku, n, c.ch_host[g])
+        codes, qp = c.oracle_index(s, g)
         gc = c.codes[s, g, :n].cpu().numpy()
         assert np.array_equal(gc, codes), f"codes differ in unit {(s, g)}: {np.argwhere(gc != codes)[:5]}"
         np.testing.assert_array_equal(c.qparams[s, g, :n].cpu().numpy(), qp, err_msg=f"qparams {(s, g)}")
