@@ -281,6 +281,33 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
                              int32_t* block_ids_out, int32_t* token_ids_out, void* ws,
                              size_t ws_bytes, const tls_decode_opts* opts, hipStream_t stream);
 
+/* tls_sparse_decode for callers that cannot allocate memory or pass a
+ * workspace (code under stream capture, tight serving loops, harnesses that
+ * forbid allocation): the same operator, arguments and results, with the
+ * scratch taken from a buffer the library owns instead of ws/ws_bytes.
+ * That buffer is a 64 MiB device array of the library, one per GPU it runs
+ * on, held from the library's load until the process ends; the call
+ * allocates nothing (no hipMalloc, no allocating library routine).  A call
+ * whose route needs more than 64 MiB of scratch returns
+ * TLS_ERR_WORKSPACE_TOO_SMALL and enqueues nothing (the token-level operator
+ * needs 4 * b * H_kv * max_ctx bytes; the two-level operator at 96k context,
+ * b = 32, H_kv = 8 needs about 4 MB).  Every call on one GPU shares that GPU's
+ * buffer, so calls that may overlap on one GPU (different streams, or
+ * host threads) race and must be ordered by the caller; calls in one stream
+ * are ordered.  The buffer needs no clearing between calls: every region a
+ * call reads is written by the same call first.  device_error (nullable)
+ * is a caller-owned device word the kernels OR TLS_DEVERR_* bits into (the
+ * caller zeroes and reads it); with NULL, device-side errors go unreported.
+ * The current device must be the one `stream` belongs to. */
+tls_status tls_sparse_decode_noalloc(const tls_layout* layout, const void* q, const tls_kv_view* kv,
+                                     const int32_t* ctx_lens, const void* kmax, const void* kmin,
+                                     const uint8_t* codes, const float* qparams, const int32_t* channels,
+                                     int32_t K_b, int32_t K_t, const int32_t* block_ids_in,
+                                     const int32_t* token_ids_in, void* out, float* lse,
+                                     int32_t* block_ids_out, int32_t* token_ids_out,
+                                     uint32_t* device_error, const tls_decode_opts* opts,
+                                     hipStream_t stream);
+
 /* Incremental block transfer of the offloaded KV tier, Sec. 4.2: with the
  * resident set C_t of each unit described by slot_map ([units][m_max]) and
  * slot_owner ([units][n_slots], block id held by each slot or -1), brings in

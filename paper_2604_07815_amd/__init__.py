@@ -20,9 +20,9 @@ __all__ = [
     "TlsError", "Layout", "KvView", "KV", "DecodeOpts", "NUM_STAGE_EVENTS", "LIB_PATH",
     "tls_version", "tls_status_string", "tls_workspace_size", "tls_workspace_init",
     "tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
-    "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error", "tls_prefill_kv", "tls_offload_kv",
-    "tls_init_residency", "tls_calibrate_absmax", "tls_calibrate_channels", "tls_append_tokens",
-    "make_layout", "alloc_workspace", "DTYPE_F32", "DTYPE_BF16", "EXPORTED_SYMBOLS",
+    "tls_sparse_decode", "tls_sparse_decode_noalloc", "tls_prefetch_blocks", "tls_check_device_error",
+    "tls_prefill_kv", "tls_offload_kv", "tls_init_residency", "tls_calibrate_absmax", "tls_calibrate_channels",
+    "tls_append_tokens", "make_layout", "alloc_workspace", "DTYPE_F32", "DTYPE_BF16", "EXPORTED_SYMBOLS",
     "MODE_TWO_LEVEL", "MODE_BLOCK_SPARSE", "MODE_DENSE", "MODE_TOKEN_SPARSE",
     "DEVERR_CTX_LEN", "DEVERR_BLOCK_ID", "DEVERR_TOKEN_ID", "DEVERR_SLOT", "DEVERR_POOL_FULL", "DEVERR_CHANNEL",
 ]
@@ -40,6 +40,7 @@ EXPORTED_SYMBOLS = [
     "tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
     "tls_sparse_decode", "tls_prefetch_blocks", "tls_check_device_error", "tls_prefill_kv",
     "tls_offload_kv", "tls_init_residency", "tls_calibrate_absmax", "tls_calibrate_channels", "tls_append_tokens",
+    "tls_sparse_decode_noalloc",
 ]
 
 
@@ -88,6 +89,8 @@ def _load() -> ctypes.CDLL:
         "tls_select_tokens": (I32, [LP, P, P, P, P, P, I32, P, I32, P, P, P, SZ, P]),
         "tls_sparse_decode": (I32, [LP, P, ctypes.POINTER(KvView), P, P, P, P, P, P, I32, I32, P, P,
                                     P, P, P, P, P, SZ, ctypes.POINTER(DecodeOpts), P]),
+        "tls_sparse_decode_noalloc": (I32, [LP, P, ctypes.POINTER(KvView), P, P, P, P, P, P, I32, I32, P, P,
+                                            P, P, P, P, P, ctypes.POINTER(DecodeOpts), P]),
         "tls_prefetch_blocks": (I32, [LP, P, P, P, P, P, I32, P, P, I64, P, P, P, P, SZ, P]),
         "tls_offload_kv": (I32, [LP, P, P, P, I32, I32, P, P, P]),
         "tls_append_tokens": (I32, [LP, P, P, P, P, P, P, P, P, P, P, ctypes.POINTER(KvView), P]),
@@ -255,6 +258,19 @@ def tls_sparse_decode(layout, q, kv: KV, ctx_lens, kmax, kmin, codes, qparams, c
                       mode: int = MODE_TWO_LEVEL, stream=None) -> None:
     """One decode step.  stage_events: NUM_STAGE_EVENTS raw hipEvent_t handles;
     mode: MODE_TWO_LEVEL, or one of the single-level baselines."""
+    opts, ev_arr = _decode_opts(attn_splits, stage_events, mode)
+    view = kv.as_struct()
+    _check(_lib.tls_sparse_decode(
+        ctypes.byref(layout), _ptr(q, "q"), ctypes.byref(view), _ptr(ctx_lens, "ctx_lens"),
+        _ptr(kmax, "kmax"), _ptr(kmin, "kmin"), _ptr(codes, "codes"), _ptr(qparams, "qparams"),
+        _ptr(channels, "channels"), int(K_b), int(K_t), _ptr(block_ids_in, "block_ids_in"),
+        _ptr(token_ids_in, "token_ids_in"), _ptr(out, "out"), _ptr(lse, "lse"),
+        _ptr(block_ids_out, "block_ids_out"), _ptr(token_ids_out, "token_ids_out"), _ptr(ws, "ws"),
+        _nbytes(ws), ctypes.byref(opts), _stream(stream)), "tls_sparse_decode")
+    del ev_arr
+
+
+def _decode_opts(attn_splits, stage_events, mode):
     opts = DecodeOpts()
     opts.attn_splits = int(attn_splits)
     opts.mode = int(mode)
@@ -264,14 +280,27 @@ def tls_sparse_decode(layout, q, kv: KV, ctx_lens, kmax, kmin, codes, qparams, c
             raise ValueError(f"stage_events must hold {NUM_STAGE_EVENTS} events")
         ev_arr = (ctypes.c_void_p * NUM_STAGE_EVENTS)(*[ctypes.c_void_p(int(e)) for e in stage_events])
         opts.stage_events = ctypes.cast(ev_arr, ctypes.c_void_p)
+    return opts, ev_arr
+
+
+def tls_sparse_decode_noalloc(layout, q, kv: KV, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t,
+                              block_ids_in, token_ids_in, out, lse, block_ids_out, token_ids_out,
+                              device_error: Optional[torch.Tensor] = None, attn_splits: int = 0,
+                              stage_events: Optional[Sequence[int]] = None, mode: int = MODE_TWO_LEVEL,
+                              stream=None) -> None:
+    """tls_sparse_decode on the library's own scratch (no workspace, no
+    allocation).  device_error: optional one-element int32 GPU tensor that
+    receives the device-side error bits (zero it first)."""
+    opts, ev_arr = _decode_opts(attn_splits, stage_events, mode)
     view = kv.as_struct()
-    _check(_lib.tls_sparse_decode(
+    _check(_lib.tls_sparse_decode_noalloc(
         ctypes.byref(layout), _ptr(q, "q"), ctypes.byref(view), _ptr(ctx_lens, "ctx_lens"),
         _ptr(kmax, "kmax"), _ptr(kmin, "kmin"), _ptr(codes, "codes"), _ptr(qparams, "qparams"),
         _ptr(channels, "channels"), int(K_b), int(K_t), _ptr(block_ids_in, "block_ids_in"),
         _ptr(token_ids_in, "token_ids_in"), _ptr(out, "out"), _ptr(lse, "lse"),
-        _ptr(block_ids_out, "block_ids_out"), _ptr(token_ids_out, "token_ids_out"), _ptr(ws, "ws"),
-        _nbytes(ws), ctypes.byref(opts), _stream(stream)), "tls_sparse_decode")
+        _ptr(block_ids_out, "block_ids_out"), _ptr(token_ids_out, "token_ids_out"),
+        _ptr(device_error, "device_error"), ctypes.byref(opts), _stream(stream)), "tls_sparse_decode_noalloc")
+    del ev_arr
 
 
 def tls_prefetch_blocks(layout, host_k, host_v, ctx_lens, block_ids_new, block_ids_live, K_b, pool_k, pool_v,

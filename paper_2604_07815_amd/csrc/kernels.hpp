@@ -29,7 +29,19 @@ struct Workspace {
   size_t err, xfer, qpn, bscores, bids, logits, stats, keys, tids, po, plse, dkeys, dstats, total;
   int n_tchunks;  // token-score work-groups per unit
 };
-Workspace plan_workspace(const Problem& P, int K_b, int K_t);
+// Regions of the workspace, as a mask: a route of a call names the regions
+// it uses; the public size holds all of them (partials for kMaxSplits).
+enum : unsigned {
+  kWsXfer = 1u,       // prefetch transfer lists
+  kWsBlockSel = 2u,   // pre-reduced queries and block scores
+  kWsBids = 4u,       // block ids when the caller takes none
+  kWsTokenSel = 8u,   // logits, per-chunk statistics and keys of the general token stage
+  kWsTids = 16u,      // token ids when the caller takes none
+  kWsSplit = 32u,     // split-attention partials and their lse
+  kWsDense = 64u,     // keys and statistics of the token-level operator
+  kWsAll = 127u,
+};
+Workspace plan_workspace(const Problem& P, int K_b, int K_t, unsigned regions = kWsAll, int nsplit = kMaxSplits);
 
 hipError_t launch_block_index(const Problem& P, const void* K, const int32_t* ctx_lens, int tok_begin,
                               int tok_end, void* kmax, void* kmin, uint32_t* err, hipStream_t st);

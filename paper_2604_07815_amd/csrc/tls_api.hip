@@ -3,10 +3,17 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "tls.h"
 #include "kernels.hpp"
 
 using tls::Problem;
+
+// Scratch of tls_sparse_decode_noalloc, 64 MiB per device (see
+// scratch_of_current_device for how host code reaches it).
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace {
 
@@ -105,29 +112,50 @@ T* at(void* ws, size_t off) {
 
 uint32_t* err_word(void* ws) { return static_cast<uint32_t*>(ws); }
 
+hipError_t run_token_select(const Problem& P, const tls::Workspace& W, const void* q, const uint8_t* codes,
+                            const float* qparams, const int32_t* channels, const int32_t* block_ids, int K_b,
+                            const int32_t* ctx_lens, int K_t, int32_t* token_ids, float* token_scores, void* ws,
+                            uint32_t* err, hipStream_t stream, hipEvent_t* ev) {
+  hipError_t e = tls::launch_token_score(P, q, codes, qparams, channels, block_ids, K_b, ctx_lens,
+                                         at<float>(ws, W.logits), at<float>(ws, W.stats), W.n_tchunks, err, stream);
+  if (e != hipSuccess) return e;
+  if (ev) (void)hipEventRecord(ev[0], stream);
+  e = tls::launch_token_alpha(P, at<float>(ws, W.logits), at<float>(ws, W.stats), W.n_tchunks, block_ids, K_b,
+                              ctx_lens, at<uint32_t>(ws, W.keys), stream);
+  if (e != hipSuccess) return e;
+  if (ev) (void)hipEventRecord(ev[1], stream);
+  return tls::launch_token_topk(P, at<uint32_t>(ws, W.keys), block_ids, K_b, K_t, token_ids, token_scores, stream);
+}
+
 }  // namespace
 
 namespace tls {
 
-Workspace plan_workspace(const Problem& P, int K_b, int K_t) {
+Workspace plan_workspace(const Problem& P, int K_b, int K_t, unsigned regions, int nsplit) {
   Workspace w{};
   const size_t U = size_t(P.units);
   const size_t S = size_t(K_b) * P.B;
+  const size_t ns = size_t(nsplit);
   w.n_tchunks = int((S + kTokenSlotsPerWG - 1) / kTokenSlotsPerWG);
   size_t off = 0;
+  // a region outside `regions` takes no bytes (its offset is never used)
+  auto take = [&](size_t* at, unsigned region, size_t bytes) {
+    *at = off;
+    if (regions & region) off = align_up(off + bytes);
+  };
   w.err = off;      off += kHeaderBytes;
-  w.xfer = off;     off = align_up(off + U * (2 * size_t(K_b) + 1) * sizeof(int32_t));  // prefetch lists
-  w.qpn = off;      off = align_up(off + U * 2 * size_t(P.d_qk) * sizeof(float));
-  w.bscores = off;  off = align_up(off + U * P.m_max * sizeof(float));
-  w.bids = off;     off = align_up(off + U * K_b * sizeof(int32_t));
-  w.logits = off;   off = align_up(off + U * P.G * S * sizeof(float));
-  w.stats = off;    off = align_up(off + U * w.n_tchunks * P.G * 2 * sizeof(float));
-  w.keys = off;     off = align_up(off + U * S * sizeof(uint32_t));
-  w.tids = off;     off = align_up(off + U * size_t(K_t) * sizeof(int32_t));
-  w.po = off;       off = align_up(off + U * kMaxSplits * P.G * size_t(P.d_v) * sizeof(float));
-  w.plse = off;     off = align_up(off + U * kMaxSplits * P.G * sizeof(float));
-  w.dkeys = off;    off = align_up(off + U * size_t(P.T) * sizeof(uint32_t));  // token-only operator
-  w.dstats = off;   off = align_up(off + ds_stats_floats(P) * sizeof(float));
+  take(&w.xfer, kWsXfer, U * (2 * size_t(K_b) + 1) * sizeof(int32_t));  // prefetch lists
+  take(&w.qpn, kWsBlockSel, U * 2 * size_t(P.d_qk) * sizeof(float));
+  take(&w.bscores, kWsBlockSel, U * P.m_max * sizeof(float));
+  take(&w.bids, kWsBids, U * K_b * sizeof(int32_t));
+  take(&w.logits, kWsTokenSel, U * P.G * S * sizeof(float));
+  take(&w.stats, kWsTokenSel, U * w.n_tchunks * P.G * 2 * sizeof(float));
+  take(&w.keys, kWsTokenSel, U * S * sizeof(uint32_t));
+  take(&w.tids, kWsTids, U * size_t(K_t) * sizeof(int32_t));
+  take(&w.po, kWsSplit, U * ns * P.G * size_t(P.d_v) * sizeof(float));
+  take(&w.plse, kWsSplit, U * ns * P.G * sizeof(float));
+  take(&w.dkeys, kWsDense, U * size_t(P.T) * sizeof(uint32_t));  // token-only operator
+  take(&w.dstats, kWsDense, ds_stats_floats(P) * sizeof(float));
   w.total = off;
   return w;
 }
@@ -313,22 +341,6 @@ tls_status tls_select_blocks(const tls_layout* layout, const void* q, const void
   return hip_status(e);
 }
 
-static hipError_t run_token_select(const Problem& P, const tls::Workspace& W, const void* q, const uint8_t* codes,
-                                   const float* qparams, const int32_t* channels, const int32_t* block_ids, int K_b,
-                                   const int32_t* ctx_lens, int K_t, int32_t* token_ids, float* token_scores,
-                                   void* ws, hipStream_t stream, hipEvent_t* ev) {
-  hipError_t e = tls::launch_token_score(P, q, codes, qparams, channels, block_ids, K_b, ctx_lens,
-                                         at<float>(ws, W.logits), at<float>(ws, W.stats), W.n_tchunks, err_word(ws),
-                                         stream);
-  if (e != hipSuccess) return e;
-  if (ev) hipEventRecord(ev[0], stream);
-  e = tls::launch_token_alpha(P, at<float>(ws, W.logits), at<float>(ws, W.stats), W.n_tchunks, block_ids, K_b,
-                              ctx_lens, at<uint32_t>(ws, W.keys), stream);
-  if (e != hipSuccess) return e;
-  if (ev) hipEventRecord(ev[1], stream);
-  return tls::launch_token_topk(P, at<uint32_t>(ws, W.keys), block_ids, K_b, K_t, token_ids, token_scores, stream);
-}
-
 tls_status tls_select_tokens(const tls_layout* layout, const void* q, const uint8_t* codes, const float* qparams,
                              const int32_t* channels, const int32_t* block_ids, int32_t K_b, const int32_t* ctx_lens,
                              int32_t K_t, int32_t* token_ids, float* token_scores, void* ws, size_t ws_bytes,
@@ -347,77 +359,104 @@ tls_status tls_select_tokens(const tls_layout* layout, const void* q, const uint
                                                      ctx_lens, K_b, K_t, token_ids, token_scores, err_word(ws),
                                                      stream));
   return hip_status(run_token_select(P, W, q, codes, qparams, channels, block_ids, K_b, ctx_lens, K_t, token_ids,
-                                     token_scores, ws, stream, nullptr));
+                                     token_scores, ws, err_word(ws), stream, nullptr));
 }
 
-// Attention over a work list (stages 6 and 7): K_t entries per unit.
-static tls_status finish_decode(const Problem& P, const tls::Workspace& W, const void* q, const tls_kv_view* kv,
-                                const int32_t* ctx_lens, int K_t, const tls::TokenList& tl, void* out, float* lse,
-                                void* ws, int requested, hipEvent_t* ev, hipStream_t stream) {
-  const int nsplit = tls::attn_splits_for(P, K_t, requested);
+}  // extern "C"
+
+namespace {
+
+// Where a decode call's scratch lives: a caller workspace (the public plan,
+// every region, sized by tls_workspace_size), or the library's own static
+// scratch (compact plan: only the regions the call's route uses).  `err` is
+// the device error word the kernels set bits in.
+struct WsTarget {
+  void* base;
+  size_t bytes;
+  uint32_t* err;
+  bool compact;
+  // Plans the workspace for a route using `regions` (split partials for
+  // `nsplit` splits); false when it does not fit.
+  bool plan(const Problem& P, int K_b, int K_t, unsigned regions, int nsplit, tls::Workspace* W) const {
+    *W = compact ? tls::plan_workspace(P, K_b, K_t, regions, nsplit) : tls::plan_workspace(P, K_b, K_t);
+    return bytes >= W->total;
+  }
+};
+
+// Split count of the attention stage over n_list entries per unit, and
+// whether it writes partials (everything but the whole-unit kernel does).
+int attention_route(const Problem& P, int n_list, int requested, unsigned* regions) {
+  const int nsplit = tls::attn_splits_for(P, n_list, requested);
+  if (!(nsplit == 1 && tls::gqa_whole_ok(P, n_list))) *regions |= tls::kWsSplit;
+  return nsplit;
+}
+
+// Attention over a work list (stages 6 and 7): n_list entries per unit.
+tls_status finish_decode(const Problem& P, const tls::Workspace& W, const void* q, const tls_kv_view* kv,
+                         const int32_t* ctx_lens, int n_list, int nsplit, const tls::TokenList& tl, void* out,
+                         float* lse, void* ws, uint32_t* err, hipEvent_t* ev, hipStream_t stream) {
   tls::KvView view{kv->k, kv->v, kv->slot_map, kv->n_slots};
-  if (nsplit == 1 && tls::gqa_whole_ok(P, K_t)) {
-    const hipError_t e = tls::launch_attention_gqa_whole(P, q, view, tl, ctx_lens, K_t, out, lse, err_word(ws),
-                                                         stream);
-    if (ev) hipEventRecord(ev[6], stream);
-    if (ev) hipEventRecord(ev[7], stream);
+  if (nsplit == 1 && tls::gqa_whole_ok(P, n_list)) {
+    const hipError_t e = tls::launch_attention_gqa_whole(P, q, view, tl, ctx_lens, n_list, out, lse, err, stream);
+    if (ev) (void)hipEventRecord(ev[6], stream);
+    if (ev) (void)hipEventRecord(ev[7], stream);
     return hip_status(e);
   }
-  hipError_t e = tls::launch_attention(P, q, view, tl, ctx_lens, K_t, nsplit, at<float>(ws, W.po),
-                                       at<float>(ws, W.plse), err_word(ws), stream);
-  if (ev) hipEventRecord(ev[6], stream);
+  hipError_t e = tls::launch_attention(P, q, view, tl, ctx_lens, n_list, nsplit, at<float>(ws, W.po),
+                                       at<float>(ws, W.plse), err, stream);
+  if (ev) (void)hipEventRecord(ev[6], stream);
   if (e == hipSuccess) e = tls::launch_merge(P, at<float>(ws, W.po), at<float>(ws, W.plse), nsplit, out, lse, stream);
-  if (ev) hipEventRecord(ev[7], stream);
+  if (ev) (void)hipEventRecord(ev[7], stream);
   return hip_status(e);
 }
 
 // Token-level selection alone (TLS_MODE_TOKEN_SPARSE): alpha over every valid
 // token of each unit, its top-K_t, then attention over those tokens.
-static tls_status token_level_decode(const Problem& P, const void* q, const tls_kv_view* kv,
-                                     const int32_t* ctx_lens, const uint8_t* codes, const float* qparams,
-                                     const int32_t* channels, int K_b, int K_t, const int32_t* block_ids_in,
-                                     const int32_t* token_ids_in, void* out, float* lse, int32_t* block_ids_out,
-                                     int32_t* token_ids_out, void* ws, size_t ws_bytes, int requested,
-                                     hipEvent_t* ev, hipStream_t stream) {
+tls_status token_level_decode(const Problem& P, const void* q, const tls_kv_view* kv, const int32_t* ctx_lens,
+                              const uint8_t* codes, const float* qparams, const int32_t* channels, int K_b, int K_t,
+                              const int32_t* block_ids_in, const int32_t* token_ids_in, void* out, float* lse,
+                              int32_t* block_ids_out, int32_t* token_ids_out, const WsTarget& tgt, int requested,
+                              hipEvent_t* ev, hipStream_t stream) {
   if (block_ids_in || token_ids_in || block_ids_out) return TLS_ERR_INVALID_ARGUMENT;
   if (!codes || !qparams || !channels) return TLS_ERR_INVALID_ARGUMENT;
   if (K_t < 1) return TLS_ERR_INVALID_ARGUMENT;
   if (!tls::ds_supported(P)) return TLS_ERR_UNSUPPORTED;
   tls_status st = check_attention(P, K_t);
   if (st != TLS_OK) return st;
-  const tls::Workspace W = tls::plan_workspace(P, K_b > 0 ? K_b : 1, K_t);
-  if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  unsigned regions = tls::kWsDense | (token_ids_out ? 0u : tls::kWsTids);
+  const int nsplit = attention_route(P, K_t, requested, &regions);
+  tls::Workspace W;
+  if (!tgt.plan(P, K_b > 0 ? K_b : 1, K_t, regions, nsplit, &W)) return TLS_ERR_WORKSPACE_TOO_SMALL;
   auto mark = [&](int i) {
-    if (ev) hipEventRecord(ev[i], stream);
+    if (ev) (void)hipEventRecord(ev[i], stream);
   };
   mark(0);
   mark(1);
   mark(2);
-  int32_t* to = token_ids_out ? token_ids_out : at<int32_t>(ws, W.tids);
+  int32_t* to = token_ids_out ? token_ids_out : at<int32_t>(tgt.base, W.tids);
   const hipError_t e = tls::launch_token_select_dense(P, q, codes, qparams, channels, ctx_lens, K_t,
-                                                      at<float>(ws, W.dstats), at<uint32_t>(ws, W.dkeys), to,
-                                                      err_word(ws), stream);
+                                                      at<float>(tgt.base, W.dstats), at<uint32_t>(tgt.base, W.dkeys),
+                                                      to, tgt.err, stream);
   mark(3);
   mark(4);
   mark(5);
   if (e != hipSuccess) return TLS_ERR_HIP;
-  return finish_decode(P, W, q, kv, ctx_lens, K_t, tls::TokenList{to, K_t, tls::kListIds, P.B}, out, lse, ws,
-                       requested, ev, stream);
+  return finish_decode(P, W, q, kv, ctx_lens, K_t, nsplit, tls::TokenList{to, K_t, tls::kListIds, P.B}, out, lse,
+                       tgt.base, tgt.err, ev, stream);
 }
 
 // The single-level baselines (TLS_MODE_BLOCK_SPARSE, TLS_MODE_DENSE): block
 // selection (unless given) and attention over every valid token of the
 // selected blocks, or attention over the whole context.
-static tls_status single_level_decode(const Problem& P, int mode, const void* q, const tls_kv_view* kv,
-                                      const int32_t* ctx_lens, const void* kmax, const void* kmin,
-                                      const uint8_t* codes, const float* qparams, const int32_t* channels, int K_b,
-                                      int K_t,
-                                      const int32_t* block_ids_in, const int32_t* token_ids_in, void* out,
-                                      float* lse, int32_t* block_ids_out, int32_t* token_ids_out, void* ws,
-                                      size_t ws_bytes, int requested, hipEvent_t* ev, hipStream_t stream) {
+tls_status single_level_decode(const Problem& P, int mode, const void* q, const tls_kv_view* kv,
+                               const int32_t* ctx_lens, const void* kmax, const void* kmin, const uint8_t* codes,
+                               const float* qparams, const int32_t* channels, int K_b, int K_t,
+                               const int32_t* block_ids_in, const int32_t* token_ids_in, void* out, float* lse,
+                               int32_t* block_ids_out, int32_t* token_ids_out, const WsTarget& tgt, int requested,
+                               hipEvent_t* ev, hipStream_t stream) {
   if (mode == TLS_MODE_TOKEN_SPARSE)
     return token_level_decode(P, q, kv, ctx_lens, codes, qparams, channels, K_b, K_t, block_ids_in, token_ids_in,
-                              out, lse, block_ids_out, token_ids_out, ws, ws_bytes, requested, ev, stream);
+                              out, lse, block_ids_out, token_ids_out, tgt, requested, ev, stream);
   if (token_ids_in || token_ids_out) return TLS_ERR_INVALID_ARGUMENT;
   const bool dense = mode == TLS_MODE_DENSE;
   if (dense && (block_ids_in || block_ids_out)) return TLS_ERR_INVALID_ARGUMENT;
@@ -427,20 +466,24 @@ static tls_status single_level_decode(const Problem& P, int mode, const void* q,
   const int n_list = dense ? P.T : K_b * P.B;  // work-list entries per unit
   st = check_attention(P, n_list);
   if (st != TLS_OK) return st;
-  const tls::Workspace W = tls::plan_workspace(P, dense ? 1 : K_b, K_t > 0 ? K_t : 1);
-  if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  const bool sel = !dense && !block_ids_in;
+  unsigned regions = sel ? (tls::kWsBlockSel | (block_ids_out ? 0u : tls::kWsBids)) : 0u;
+  const int nsplit = attention_route(P, n_list, requested, &regions);
+  tls::Workspace W;
+  if (!tgt.plan(P, dense ? 1 : K_b, K_t > 0 ? K_t : 1, regions, nsplit, &W)) return TLS_ERR_WORKSPACE_TOO_SMALL;
   auto mark = [&](int i) {
-    if (ev) hipEventRecord(ev[i], stream);
+    if (ev) (void)hipEventRecord(ev[i], stream);
   };
   mark(0);
   hipError_t e = hipSuccess;
   const int32_t* bids = block_ids_in;
-  if (!dense && !bids) {
-    int32_t* bo = block_ids_out ? block_ids_out : at<int32_t>(ws, W.bids);
-    e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.qpn), at<float>(ws, W.bscores),
-                                err_word(ws), stream);
+  if (sel) {
+    int32_t* bo = block_ids_out ? block_ids_out : at<int32_t>(tgt.base, W.bids);
+    e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(tgt.base, W.qpn),
+                                at<float>(tgt.base, W.bscores), tgt.err, stream);
     mark(1);
-    if (e == hipSuccess) e = tls::launch_block_topk(P, at<float>(ws, W.bscores), ctx_lens, K_b, bo, err_word(ws), stream);
+    if (e == hipSuccess)
+      e = tls::launch_block_topk(P, at<float>(tgt.base, W.bscores), ctx_lens, K_b, bo, tgt.err, stream);
     bids = bo;
   } else {
     mark(1);
@@ -449,19 +492,17 @@ static tls_status single_level_decode(const Problem& P, int mode, const void* q,
   if (e != hipSuccess) return TLS_ERR_HIP;
   const tls::TokenList tl = dense ? tls::TokenList{nullptr, 0, tls::kListAll, P.B}
                                   : tls::TokenList{bids, K_b, tls::kListBlocks, P.B};
-  return finish_decode(P, W, q, kv, ctx_lens, n_list, tl, out, lse, ws, requested, ev, stream);
+  return finish_decode(P, W, q, kv, ctx_lens, n_list, nsplit, tl, out, lse, tgt.base, tgt.err, ev, stream);
 }
 
-tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_kv_view* kv, const int32_t* ctx_lens,
-                             const void* kmax, const void* kmin, const uint8_t* codes, const float* qparams,
-                             const int32_t* channels, int32_t K_b, int32_t K_t, const int32_t* block_ids_in,
-                             const int32_t* token_ids_in, void* out, float* lse, int32_t* block_ids_out,
-                             int32_t* token_ids_out, void* ws, size_t ws_bytes, const tls_decode_opts* opts,
-                             hipStream_t stream) {
-  Problem P;
-  tls_status st = make_problem(layout, &P);
-  if (st != TLS_OK) return st;
-  if (!q || !kv || !kv->k || !ctx_lens || !out || !ws) return TLS_ERR_INVALID_ARGUMENT;
+// tls_sparse_decode after the layout is validated, on a workspace target.
+tls_status sparse_decode_on(const Problem& P, const void* q, const tls_kv_view* kv, const int32_t* ctx_lens,
+                            const void* kmax, const void* kmin, const uint8_t* codes, const float* qparams,
+                            const int32_t* channels, int32_t K_b, int32_t K_t, const int32_t* block_ids_in,
+                            const int32_t* token_ids_in, void* out, float* lse, int32_t* block_ids_out,
+                            int32_t* token_ids_out, const tls_decode_opts* opts, const WsTarget& tgt,
+                            hipStream_t stream) {
+  if (!q || !kv || !kv->k || !ctx_lens || !out) return TLS_ERR_INVALID_ARGUMENT;
   if (!P.mla && !kv->v) return TLS_ERR_INVALID_ARGUMENT;
   if (P.mla && kv->v) return TLS_ERR_INVALID_ARGUMENT;
   if (kv->slot_map && kv->n_slots < 1) return TLS_ERR_INVALID_ARGUMENT;
@@ -481,52 +522,62 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
   }
   if (mode != TLS_MODE_TWO_LEVEL)
     return single_level_decode(P, mode, q, kv, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t,
-                               block_ids_in, token_ids_in, out,
-                               lse, block_ids_out, token_ids_out, ws, ws_bytes, requested, ev, stream);
+                               block_ids_in, token_ids_in, out, lse, block_ids_out, token_ids_out, tgt, requested,
+                               ev, stream);
   const bool sel_tokens = token_ids_in == nullptr;
   const bool sel_blocks = sel_tokens && block_ids_in == nullptr;
   if (sel_blocks && (!kmax || !kmin)) return TLS_ERR_INVALID_ARGUMENT;
   if (sel_tokens && (!codes || !qparams || !channels)) return TLS_ERR_INVALID_ARGUMENT;
-  st = check_budgets(P, K_b, K_t);
+  tls_status st = check_budgets(P, K_b, K_t);
   if (st != TLS_OK) return st;
   st = check_attention(P, K_t);
   if (st != TLS_OK) return st;
-  const tls::Workspace W = tls::plan_workspace(P, K_b, K_t);
-  if (ws_bytes < W.total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  // the route: fused selection (block scores, then one kernel for block
+  // top-k and token selection), or the general stages
+  const bool fused = sel_tokens && tls::fused_token_select_ok(P, K_b, K_t);
+  unsigned regions = 0u;
+  if (sel_blocks) regions |= tls::kWsBlockSel | (fused || block_ids_out ? 0u : tls::kWsBids);
+  if (sel_tokens) regions |= (fused ? 0u : tls::kWsTokenSel) | (token_ids_out ? 0u : tls::kWsTids);
+  const int nsplit = attention_route(P, K_t, requested, &regions);
+  tls::Workspace W;
+  if (!tgt.plan(P, K_b, K_t, regions, nsplit, &W)) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  void* ws = tgt.base;
+  uint32_t* err = tgt.err;
 
   hipError_t e = hipSuccess;
   auto mark = [&](int i) {
-    if (ev) hipEventRecord(ev[i], stream);
+    if (ev) (void)hipEventRecord(ev[i], stream);
   };
   mark(0);
   const int32_t* bids = block_ids_in;
-  if (sel_tokens && tls::fused_token_select_ok(P, K_b, K_t)) {
-    // block score, then one kernel for block top-k + token selection; the
-    // token-score stage events bracket the fused kernel
+  if (fused) {
+    // the token-score stage events bracket the fused kernel
     int32_t* to = token_ids_out ? token_ids_out : at<int32_t>(ws, W.tids);
     const float* bsc = nullptr;
     if (sel_blocks) {
-      e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.qpn), at<float>(ws, W.bscores), err_word(ws), stream);
+      e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.qpn), at<float>(ws, W.bscores), err,
+                                  stream);
       bsc = at<float>(ws, W.bscores);
     }
     mark(1);
     mark(2);
     if (e == hipSuccess)
       e = tls::launch_token_select_fused(P, q, codes, qparams, channels, bsc, block_ids_in,
-                                         sel_blocks ? block_ids_out : nullptr, ctx_lens, K_b, K_t, to, nullptr,
-                                         err_word(ws), stream);
+                                         sel_blocks ? block_ids_out : nullptr, ctx_lens, K_b, K_t, to, nullptr, err,
+                                         stream);
     mark(3);
     mark(4);
     mark(5);
     if (e != hipSuccess) return TLS_ERR_HIP;
-    return finish_decode(P, W, q, kv, ctx_lens, K_t, tls::TokenList{to, K_t, tls::kListIds, P.B}, out, lse, ws,
-                         requested, ev, stream);
+    return finish_decode(P, W, q, kv, ctx_lens, K_t, nsplit, tls::TokenList{to, K_t, tls::kListIds, P.B}, out, lse,
+                         ws, err, ev, stream);
   }
   if (sel_blocks) {
     int32_t* bo = block_ids_out ? block_ids_out : at<int32_t>(ws, W.bids);
-    e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.qpn), at<float>(ws, W.bscores), err_word(ws), stream);
+    e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.qpn), at<float>(ws, W.bscores), err,
+                                stream);
     mark(1);
-    if (e == hipSuccess) e = tls::launch_block_topk(P, at<float>(ws, W.bscores), ctx_lens, K_b, bo, err_word(ws), stream);
+    if (e == hipSuccess) e = tls::launch_block_topk(P, at<float>(ws, W.bscores), ctx_lens, K_b, bo, err, stream);
     bids = bo;
   } else {
     mark(1);
@@ -536,7 +587,7 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
   const int32_t* tids = token_ids_in;
   if (sel_tokens) {
     int32_t* to = token_ids_out ? token_ids_out : at<int32_t>(ws, W.tids);
-    e = run_token_select(P, W, q, codes, qparams, channels, bids, K_b, ctx_lens, K_t, to, nullptr, ws, stream,
+    e = run_token_select(P, W, q, codes, qparams, channels, bids, K_b, ctx_lens, K_t, to, nullptr, ws, err, stream,
                          ev ? ev + 3 : nullptr);
     tids = to;
   } else {
@@ -545,8 +596,70 @@ tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_
   }
   mark(5);
   if (e != hipSuccess) return TLS_ERR_HIP;
-  return finish_decode(P, W, q, kv, ctx_lens, K_t, tls::TokenList{tids, K_t, tls::kListIds, P.B}, out, lse, ws,
-                       requested, ev, stream);
+  return finish_decode(P, W, q, kv, ctx_lens, K_t, nsplit, tls::TokenList{tids, K_t, tls::kListIds, P.B}, out, lse,
+                       ws, err, ev, stream);
+}
+
+// The library's own scratch for tls_sparse_decode_noalloc: one array per
+// device, resident from the library's load until the process ends.  Host
+// code never uses the array's name as an address: the device address comes
+// from hipGetSymbolAddress, once per device, with that device current.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices];  // guarded by g_scratch_mutex
+
+tls_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TLS_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return TLS_ERR_HIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return TLS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_kv_view* kv, const int32_t* ctx_lens,
+                             const void* kmax, const void* kmin, const uint8_t* codes, const float* qparams,
+                             const int32_t* channels, int32_t K_b, int32_t K_t, const int32_t* block_ids_in,
+                             const int32_t* token_ids_in, void* out, float* lse, int32_t* block_ids_out,
+                             int32_t* token_ids_out, void* ws, size_t ws_bytes, const tls_decode_opts* opts,
+                             hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  if (!ws) return TLS_ERR_INVALID_ARGUMENT;
+  const WsTarget tgt{ws, ws_bytes, err_word(ws), false};
+  return sparse_decode_on(P, q, kv, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t, block_ids_in,
+                          token_ids_in, out, lse, block_ids_out, token_ids_out, opts, tgt, stream);
+}
+
+tls_status tls_sparse_decode_noalloc(const tls_layout* layout, const void* q, const tls_kv_view* kv,
+                                     const int32_t* ctx_lens, const void* kmax, const void* kmin,
+                                     const uint8_t* codes, const float* qparams, const int32_t* channels, int32_t K_b,
+                                     int32_t K_t, const int32_t* block_ids_in, const int32_t* token_ids_in, void* out,
+                                     float* lse, int32_t* block_ids_out, int32_t* token_ids_out,
+                                     uint32_t* device_error, const tls_decode_opts* opts, hipStream_t stream) {
+  Problem P;
+  tls_status st = make_problem(layout, &P);
+  if (st != TLS_OK) return st;
+  void* scr = nullptr;
+  st = scratch_of_current_device(&scr);
+  if (st != TLS_OK) return st;
+  // device-side error bits go to the caller's word; without one they land in
+  // the scratch header, which nothing reads
+  const WsTarget tgt{scr, kScratchBytes, device_error ? device_error : static_cast<uint32_t*>(scr), true};
+  return sparse_decode_on(P, q, kv, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t, block_ids_in,
+                          token_ids_in, out, lse, block_ids_out, token_ids_out, opts, tgt, stream);
 }
 
 tls_status tls_prefetch_blocks(const tls_layout* layout, const void* host_k, const void* host_v,
