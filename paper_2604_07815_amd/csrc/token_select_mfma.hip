@@ -24,39 +24,9 @@
 // the 128 sum_c q~_c part is folded into the offset term:
 //   l_hj = sigma * (scale_j * dot_hj + (min_j - 128 scale_j) * sum_c q~_hc).
 // All products are exact in fp32; accumulation is fp32.
-#include "token_common.hpp"
+#include "token_select_mfma.hpp"
 
 namespace tls {
-
-typedef short i16x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
-
-constexpr int kSelNT = 1024;
-constexpr int kSelNW = kSelNT / 64;
-constexpr int kSelSPT = 8;  // candidate slots per thread
-constexpr int kSelMaxSlots = kSelNT * kSelSPT;
-constexpr int kSelBPT = 2;  // block scores per thread
-constexpr int kSelMaxBlocks = kSelNT * kSelBPT;
-constexpr int kSelMaxG = 4;
-constexpr size_t kSelMaxLds = 160 * 1024;
-constexpr uint32_t kBf16Base = 0x43434343u;  // high byte of bf16(128 + c), c < 16
-
-// Element order of one 4-channel k-slice: within the 8 channels of code dword
-// w, slice 2w holds channels (0, 2, 1, 3) and slice 2w+1 channels (4, 6, 5, 7)
-// (offsets from 8w): the low nibbles of two bytes, then their high nibbles.
-__device__ constexpr int kSliceChan[8] = {0, 2, 1, 3, 4, 6, 5, 7};
-
-// LDS words: top-k scratch | block list | q~ table (4 heads x 32 channels of
-// bf16, in slice order) | per-wave partials | list of keys in play
-// (max(m_max, S)).
-__host__ __device__ inline size_t list_words(int S, int m_max) { return size_t(S > m_max ? S : m_max); }
-
-size_t mfma_select_lds_bytes(int S, int K_b, int m_max) {
-  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(K_b)) + 64 + kSelNW * 12 +
-          align4w(int(list_words(S, m_max)))) *
-         sizeof(uint32_t);
-}
 
 template <int G>
 __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
@@ -65,213 +35,9 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
     const int32_t* __restrict__ block_ids_in, int32_t* __restrict__ block_ids_out,
     const int32_t* __restrict__ ctx_lens, int H_q, int H_kv, int d, int B, int T, int m_max, int K_b, int K_t,
     float sigma, int32_t* __restrict__ token_ids, float* __restrict__ token_scores, uint32_t* err) {
-  constexpr int NT = kSelNT, NW = kSelNW;
   extern __shared__ uint32_t smem[];
-  uint32_t* scratch = smem;
-  int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(NT));
-  uint16_t* s_qt = reinterpret_cast<uint16_t*>(s_bl + align4w(K_b));  // [4][32] (64 words)
-  float* s_red = reinterpret_cast<float*>(s_qt + 128);                    // [NW][12]
-  uint32_t* list = reinterpret_cast<uint32_t*>(s_red + NW * 12);
-  const int S = K_b * B;
-
-  const int unit = blockIdx.x;
-  const int s = unit / H_kv, g = unit % H_kv;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  int n = ctx_lens[s];
-  if (n < 0 || n > T) {
-    if (tid == 0) set_error(err, 1u);
-    n = n < 0 ? 0 : T;
-  }
-  const int m = (n + B - 1) / B;
-  const int lgB = __builtin_ctz(unsigned(B));  // B is a power of two here
-  const float sigma2 = sigma * 1.4426950408889634f;  // logits in base 2
-
-  // block scores as keys (requested first: the longest dependency)
-  uint32_t bk[kSelBPT];
-  if (block_scores) {
-    const float* sc = block_scores + size_t(unit) * m_max;
-#pragma unroll
-    for (int j = 0; j < kSelBPT; ++j) {
-      const int i = tid + j * NT;
-      bk[j] = i < m ? float_key(sc[i]) : kInvalidKey;
-    }
-  } else {
-    for (int i = tid; i < K_b; i += NT) {
-      int b = block_ids_in[size_t(unit) * K_b + i];
-      if (b >= m) {
-        set_error(err, 2u);
-        b = -1;
-      }
-      s_bl[i] = b < 0 ? -1 : b;
-    }
-  }
-  // q~ table in slice order: entry (h, 4k + e) = q[h][C[8(k/2) + kSliceChan[4(k%2) + e]]]
-  if (tid < 4 * 32) {
-    const int h = tid >> 5, x = tid & 31;
-    uint16_t v = 0;
-    if (h < G) {
-      const int k = x >> 2, e = x & 3;
-      int ch = channels[g * 32 + 8 * (k >> 1) + kSliceChan[4 * (k & 1) + e]];
-      if (ch < 0 || ch >= d) {
-        set_error(err, 32u);
-        ch = 0;
-      }
-      v = q[(size_t(s) * H_q + size_t(g) * G + h) * d + ch];
-    }
-    s_qt[tid] = v;
-  }
-  if (block_scores) {
-    wg_topk_regs<NT, kSelBPT>(bk, K_b, s_bl, K_b, nullptr, [](int, int i) { return int32_t(i); }, scratch, list);
-  }
-  __syncthreads();
-
-  // A operands (row = head lane%4, slice k) and the per-head q~ sums
-  i16x4_t qa[8];
-  float qsum[4];
-  {
-    const uint4* row = reinterpret_cast<const uint4*>(s_qt + (lane & 3) * 32);
-    float own = 0.f;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const uint4 w = row[v];
-      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        i16x4_t a;
-        a[0] = short(ws[2 * k2] & 0xffffu);
-        a[1] = short(ws[2 * k2] >> 16);
-        a[2] = short(ws[2 * k2 + 1] & 0xffffu);
-        a[3] = short(ws[2 * k2 + 1] >> 16);
-        qa[2 * v + k2] = a;
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) own += __uint_as_float(ws[e] << 16) + __uint_as_float(ws[e] & 0xffff0000u);
-    }
-    // broadcast the four heads' sums inside each quad (lane 4b + h holds head h)
-    const int oi = __float_as_int(own);
-    qsum[0] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0x00, 0xF, 0xF, false));
-    qsum[1] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0x55, 0xF, 0xF, false));
-    qsum[2] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0xAA, 0xF, 0xF, false));
-    qsum[3] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0xFF, 0xF, 0xF, false));
-  }
-
-  // 1. index rows of the owned slots
-  uint4 cw[kSelSPT];
-  float2 qp[kSelSPT];
-  int32_t tokpos[kSelSPT];  // token position of each owned slot (for the output)
-  uint32_t vmask = 0;
-#pragma unroll
-  for (int i = 0; i < kSelSPT; ++i) {
-    const int slot = tid + i * NT;
-    const int e = slot >> lgB, o = slot & (B - 1);
-    cw[i] = make_uint4(0, 0, 0, 0);
-    qp[i] = make_float2(0.f, 0.f);
-    tokpos[i] = -1;
-    if (slot < S) {
-      const int blk = s_bl[e];
-      const int tok = blk * B + o;
-      tokpos[i] = tok;
-      if (blk >= 0 && tok < n) {
-        const size_t r = size_t(unit) * T + tok;
-        cw[i] = ld16_stream(codes + r * 16);
-        const float* pr = qparams + r * 2;
-        qp[i] = make_float2(__builtin_nontemporal_load(pr), __builtin_nontemporal_load(pr + 1));
-        vmask |= 1u << i;
-      }
-    }
-  }
-
-  // 2. dots on the matrix cores, logits, per-head max
-  float lg[kSelSPT][G];
-  float mx[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) mx[h] = -INFINITY;
-#pragma unroll
-  for (int i = 0; i < kSelSPT; ++i) {
-    const uint32_t wd[4] = {cw[i].x, cw[i].y, cw[i].z, cw[i].w};
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const uint32_t lo = wd[w] & 0x0f0f0f0fu, hi = (wd[w] >> 4) & 0x0f0f0f0fu;
-      const u32x2_t b0 = {__builtin_amdgcn_perm(kBf16Base, lo, 0x04010400u),
-                          __builtin_amdgcn_perm(kBf16Base, hi, 0x04010400u)};
-      const u32x2_t b1 = {__builtin_amdgcn_perm(kBf16Base, lo, 0x04030402u),
-                          __builtin_amdgcn_perm(kBf16Base, hi, 0x04030402u)};
-      acc = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(qa[2 * w], __builtin_bit_cast(i16x4_t, b0), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(qa[2 * w + 1], __builtin_bit_cast(i16x4_t, b1), acc, 0, 0, 0);
-    }
-    const bool valid = (vmask >> i) & 1u;
-    const float sc = qp[i].x, off = qp[i].y - 128.0f * qp[i].x;
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      lg[i][h] = valid ? sigma2 * fmaf(sc, acc[h], off * qsum[h]) : -INFINITY;
-      mx[h] = fmaxf(mx[h], lg[i][h]);
-    }
-  }
-  const uint32_t wcnt = wave_reduce_bits(uint32_t(__popc(vmask)), [](uint32_t a, uint32_t b) { return a + b; });
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const float w = wave_max_f32(mx[h]);
-    if (lane == 0) s_red[wid * 12 + h] = w;
-  }
-  if (lane == 0) s_red[wid * 12 + 8] = __uint_as_float(wcnt);
-  __syncthreads();
-  static_assert(NW == 16, "one wave value per lane of a 16-lane row");
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    mx[h] = combine_waves_max_f32(s_red[(lane & 15) * 12 + h]);
-    if (mx[h] == -INFINITY) mx[h] = 0.f;  // no candidate: every logit is -inf, every exponential 0
-  }
-  const uint32_t n_valid = combine_waves_sum_u32(__float_as_uint(s_red[(lane & 15) * 12 + 8]));
-  // 3. exponentials (base 2: the logits carry log2(e)) and their per-head sums
-  float sum[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) sum[h] = 0.f;
-#pragma unroll
-  for (int i = 0; i < kSelSPT; ++i)
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float e = __builtin_amdgcn_exp2f(lg[i][h] - mx[h]);  // 0 for an empty slot (logit -inf)
-      lg[i][h] = e;
-      sum[h] += e;
-    }
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const float w = wave_sum_f32(sum[h]);
-    if (lane == 0) s_red[wid * 12 + 4 + h] = w;
-  }
-  topk_prepare<NT>(scratch);  // the token top-k's histograms, cleared before the barrier below
-  __syncthreads();
-  float iz[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const float Z = combine_waves_sum_f32(s_red[(lane & 15) * 12 + 4 + h]);
-    iz[h] = Z > 0.f ? 1.0f / Z : 0.f;
-  }
-  // 4. alpha keys in registers, top-K_t
-  // Every alpha lies in [0, bound] with bound = (1/G) sum_h 1/Z_h, evaluated in
-  // the same operation order (each exponential is <= 1 and rounding is
-  // monotone), so the top-k needs no statistics pass of its own.  A NaN alpha
-  // (NaN inputs only) ranks as 0.
-  const float invG = 1.0f / float(G);
-  float bsum = 0.f;
-#pragma unroll
-  for (int h = 0; h < G; ++h) bsum = fmaf(1.0f, iz[h], bsum);
-  uint32_t keys[kSelSPT];
-#pragma unroll
-  for (int i = 0; i < kSelSPT; ++i) {
-    float a = 0.f;
-#pragma unroll
-    for (int h = 0; h < G; ++h) a = fmaf(lg[i][h], iz[h], a);
-    const float av = a * invG;
-    keys[i] = ((vmask >> i) & 1u) ? (av == av ? float_key(av) : float_key(0.f)) : kInvalidKey;
-  }
-  const TopkKnown known{n_valid, float_key(bsum * invG), float_key(0.f)};
-  wg_topk_regs<NT, kSelSPT>(keys, K_t, token_ids + size_t(unit) * K_t, K_t,
-                            token_scores ? token_scores + size_t(unit) * K_t : nullptr,
-                            [&](int j, int) { return tokpos[j]; }, scratch, list, &known);
-  if (block_scores && block_ids_out)
-    for (int i = tid; i < K_b; i += NT) block_ids_out[size_t(unit) * K_b + i] = s_bl[i];
+  token_select_mfma_body<G>(smem, q, codes, qparams, channels, block_scores, block_ids_in, block_ids_out, ctx_lens,
+                            H_q, H_kv, d, B, T, m_max, K_b, K_t, sigma, token_ids, token_scores, err, blockIdx.x);
 }
 
 bool fused_token_select_ok(const Problem& P, int K_b, int K_t) {
