@@ -579,8 +579,43 @@ def setup_decode(tls, synth, torch, workload, copies_arg=0):
                               L["qparams"], ch_t, cfg.k_b, cfg.k_t, None, None, out, lse, bids, tids, ws,
                               stage_events=events)
 
+    def step_args(i):
+        L = layers[i % len(layers)]
+        return tls.sparse_decode_args(layout, L["q"], tls.KV(L["k"], L["v"]), ctx_t, L["kmax"], L["kmin"],
+                                      L["codes"], L["qparams"], ch_t, cfg.k_b, cfg.k_t, None, None, out, lse, bids,
+                                      tids, ws)
+
     return types.SimpleNamespace(cfg=cfg, d=d, layout=layout, layers=layers, copies=copies, e=e, dev=dev, dt=dt,
-                                 ctx_t=ctx_t, ch_t=ch_t, ws=ws, out=out, lse=lse, bids=bids, tids=tids, step=step)
+                                 ctx_t=ctx_t, ch_t=ch_t, ws=ws, out=out, lse=lse, bids=bids, tids=tids, step=step,
+                                 step_args=step_args)
+
+
+def host_call_us(tls, torch, s, n=48):
+    """Host time per decode call: `n` back-to-back calls issued with no wait
+    (the GPU runs behind them), timed on the host clock.  `binding`: through
+    the Python binding (argument checks and marshalling included); `c_abi`:
+    the C entry point alone, its arguments marshalled once beforehand."""
+    prepared = [s.step_args(i) for i in range(n)]
+    fn = tls.lib().tls_sparse_decode
+
+    def run(f):
+        best = float("inf")
+        for _ in range(3):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(n):
+                f(i)
+            t1 = time.perf_counter()
+            torch.cuda.synchronize()
+            best = min(best, (t1 - t0) * 1e6 / n)
+        return round(best, 2)
+
+    def raw(i):
+        if fn(*prepared[i][0]) != 0:
+            raise RuntimeError("tls_sparse_decode failed")
+
+    return {"binding": run(s.step), "c_abi": run(raw), "calls": n,
+            "method": "best of 3 runs of back-to-back calls, host clock, no wait between calls"}
 
 
 def secondary_workload(tls, synth, torch, np, workload, steps, warmup):
@@ -726,6 +761,7 @@ def main():
         return round(start.elapsed_time(stop) * 1e3 / (reps * len(layers)), 2)
 
     graph_us = graph_replay_us()
+    host_us = host_call_us(tls, torch, W)
 
     # ---- per-stage timing with HIP events on the launch stream --------------------
     hev = HipEvents()
@@ -834,6 +870,7 @@ def main():
         "step_us_distribution": dist,
         "step_us_after_1GiB_flush": dist_flush,
         "step_us_graph_replay": graph_us,
+        "host_us_per_call": host_us,
         "stage_us": {k: round(float(v) * 1e3, 2) for k, v in zip(STAGES, stage_ms)},
         "stage_marked_step_us": round(marked_ms * 1e3, 2),
         "prefill": prefill,

@@ -22,7 +22,8 @@ __all__ = [
     "tls_build_block_index", "tls_build_token_index", "tls_select_blocks", "tls_select_tokens",
     "tls_sparse_decode", "tls_sparse_decode_noalloc", "tls_prefetch_blocks", "tls_check_device_error",
     "tls_prefill_kv", "tls_offload_kv", "tls_init_residency", "tls_calibrate_absmax", "tls_calibrate_channels",
-    "tls_append_tokens", "make_layout", "alloc_workspace", "DTYPE_F32", "DTYPE_BF16", "EXPORTED_SYMBOLS",
+    "tls_append_tokens", "sparse_decode_args", "lib", "make_layout", "alloc_workspace", "DTYPE_F32", "DTYPE_BF16",
+    "EXPORTED_SYMBOLS",
     "MODE_TWO_LEVEL", "MODE_BLOCK_SPARSE", "MODE_DENSE", "MODE_TOKEN_SPARSE",
     "DEVERR_CTX_LEN", "DEVERR_BLOCK_ID", "DEVERR_TOKEN_ID", "DEVERR_SLOT", "DEVERR_POOL_FULL", "DEVERR_CHANNEL",
 ]
@@ -107,6 +108,11 @@ def _load() -> ctypes.CDLL:
 
 
 _lib = _load()
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libtls.so (its C entry points with their ctypes signatures)."""
+    return _lib
 
 
 # ----------------------------------------------------------------------------
@@ -258,16 +264,30 @@ def tls_sparse_decode(layout, q, kv: KV, ctx_lens, kmax, kmin, codes, qparams, c
                       mode: int = MODE_TWO_LEVEL, stream=None) -> None:
     """One decode step.  stage_events: NUM_STAGE_EVENTS raw hipEvent_t handles;
     mode: MODE_TWO_LEVEL, or one of the single-level baselines."""
+    args, keep = sparse_decode_args(layout, q, kv, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t,
+                                     block_ids_in, token_ids_in, out, lse, block_ids_out, token_ids_out, ws,
+                                     attn_splits, stage_events, mode, stream)
+    _check(_lib.tls_sparse_decode(*args), "tls_sparse_decode")
+    del keep
+
+
+def sparse_decode_args(layout, q, kv: KV, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t,
+                       block_ids_in, token_ids_in, out, lse, block_ids_out, token_ids_out, ws,
+                       attn_splits: int = 0, stage_events: Optional[Sequence[int]] = None,
+                       mode: int = MODE_TWO_LEVEL, stream=None):
+    """The marshalled argument tuple of tls_sparse_decode, and the ctypes
+    objects it points into (keep them alive while the tuple is used).  A
+    caller that repeats one call can marshal it once and call
+    `lib().tls_sparse_decode(*args)` (returns the TLS_* status)."""
     opts, ev_arr = _decode_opts(attn_splits, stage_events, mode)
     view = kv.as_struct()
-    _check(_lib.tls_sparse_decode(
-        ctypes.byref(layout), _ptr(q, "q"), ctypes.byref(view), _ptr(ctx_lens, "ctx_lens"),
-        _ptr(kmax, "kmax"), _ptr(kmin, "kmin"), _ptr(codes, "codes"), _ptr(qparams, "qparams"),
-        _ptr(channels, "channels"), int(K_b), int(K_t), _ptr(block_ids_in, "block_ids_in"),
-        _ptr(token_ids_in, "token_ids_in"), _ptr(out, "out"), _ptr(lse, "lse"),
-        _ptr(block_ids_out, "block_ids_out"), _ptr(token_ids_out, "token_ids_out"), _ptr(ws, "ws"),
-        _nbytes(ws), ctypes.byref(opts), _stream(stream)), "tls_sparse_decode")
-    del ev_arr
+    args = (ctypes.byref(layout), _ptr(q, "q"), ctypes.byref(view), _ptr(ctx_lens, "ctx_lens"),
+            _ptr(kmax, "kmax"), _ptr(kmin, "kmin"), _ptr(codes, "codes"), _ptr(qparams, "qparams"),
+            _ptr(channels, "channels"), int(K_b), int(K_t), _ptr(block_ids_in, "block_ids_in"),
+            _ptr(token_ids_in, "token_ids_in"), _ptr(out, "out"), _ptr(lse, "lse"),
+            _ptr(block_ids_out, "block_ids_out"), _ptr(token_ids_out, "token_ids_out"), _ptr(ws, "ws"),
+            _nbytes(ws), ctypes.byref(opts), _stream(stream))
+    return args, (opts, ev_arr, view, layout)
 
 
 def _decode_opts(attn_splits, stage_events, mode):

@@ -270,14 +270,6 @@ static int mfma_wgs_per_cu_g(int G) {
   }
 }
 
-static int device_cus() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
-    cus = 256;
-  return cus;
-}
-
 constexpr int kWideMinTokens = 768;  // tokens per 12-wave split work-group worth its prologue
 
 // Split mode with 12-wave work-groups (the whole-unit kernel writing

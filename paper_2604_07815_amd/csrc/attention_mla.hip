@@ -275,10 +275,7 @@ int mla_mfma_tokens_per_split() { return kMlaMaxTPW; }
 
 // Split count: about one work-group per compute unit, whole chunks each.
 int mla_mfma_splits(const Problem& P, int K_t) {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
-    cus = 256;
+  const int cus = device_cus();
   const int need = (K_t + kMlaMaxTPW - 1) / kMlaMaxTPW;
   int ns = (cus + P.units - 1) / P.units;
   const int max_ns = (K_t + kMlaChunk - 1) / kMlaChunk;

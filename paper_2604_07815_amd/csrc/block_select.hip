@@ -229,11 +229,8 @@ hipError_t launch_block_topk(const Problem& P, const float* scores, const int32_
   const size_t lds = (topk_scratch_words(1024) + size_t(P.m_max)) * sizeof(uint32_t);
   const int ept = (P.m_max + 1023) / 1024;
   auto go = [&](auto kern) {
-    if (lds > 65536) {
-      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-      if (e != hipSuccess) return e;
-    }
+    const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), lds);
+    if (e != hipSuccess) return e;
     kern<<<P.units, 1024, lds, st>>>(scores, ctx_lens, P.H_kv, P.T, P.B, P.m_max, K_b, block_ids);
     return hipGetLastError();
   };

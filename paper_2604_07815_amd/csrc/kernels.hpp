@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "common.hpp"
+#include "host_cache.hpp"
 
 namespace tls {
 

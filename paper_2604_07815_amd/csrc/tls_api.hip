@@ -370,16 +370,56 @@ namespace {
 // every region, sized by tls_workspace_size), or the library's own static
 // scratch (compact plan: only the regions the call's route uses).  `err` is
 // the device error word the kernels set bits in.
+// The library's own scratch for tls_sparse_decode_noalloc: one array per
+// device, resident from the library's load until the process ends.  Host
+// code never uses the array's name as an address: the device address comes
+// from hipGetSymbolAddress, once per device, with that device current.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices];  // guarded by g_scratch_mutex
+
+tls_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TLS_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return TLS_ERR_HIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return TLS_OK;
+}
+
+// Where a decode call's scratch lives: the caller's workspace (base, bytes,
+// its error word), or the library's own scratch (base == nullptr, compact
+// plan; the error word is the caller's device_error, else the scratch's
+// first word, which nothing reads).
 struct WsTarget {
   void* base;
   size_t bytes;
   uint32_t* err;
   bool compact;
   // Plans the workspace for a route using `regions` (split partials for
-  // `nsplit` splits); false when it does not fit.
-  bool plan(const Problem& P, int K_b, int K_t, unsigned regions, int nsplit, tls::Workspace* W) const {
+  // `nsplit` splits) and binds its memory: TLS_ERR_WORKSPACE_TOO_SMALL when
+  // the plan does not fit.  The library scratch is looked up only here, after
+  // every argument check, so a rejected call touches no device.
+  tls_status bind(const Problem& P, int K_b, int K_t, unsigned regions, int nsplit, tls::Workspace* W, void** ws,
+                  uint32_t** err_word_out) const {
     *W = compact ? tls::plan_workspace(P, K_b, K_t, regions, nsplit) : tls::plan_workspace(P, K_b, K_t);
-    return bytes >= W->total;
+    if (bytes < W->total) return TLS_ERR_WORKSPACE_TOO_SMALL;
+    if (base) {
+      *ws = base;
+      *err_word_out = err;
+      return TLS_OK;
+    }
+    const tls_status st = scratch_of_current_device(ws);
+    if (st != TLS_OK) return st;
+    *err_word_out = err ? err : static_cast<uint32_t*>(*ws);
+    return TLS_OK;
   }
 };
 
@@ -426,23 +466,26 @@ tls_status token_level_decode(const Problem& P, const void* q, const tls_kv_view
   unsigned regions = tls::kWsDense | (token_ids_out ? 0u : tls::kWsTids);
   const int nsplit = attention_route(P, K_t, requested, &regions);
   tls::Workspace W;
-  if (!tgt.plan(P, K_b > 0 ? K_b : 1, K_t, regions, nsplit, &W)) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  void* ws = nullptr;
+  uint32_t* err = nullptr;
+  st = tgt.bind(P, K_b > 0 ? K_b : 1, K_t, regions, nsplit, &W, &ws, &err);
+  if (st != TLS_OK) return st;
   auto mark = [&](int i) {
     if (ev) (void)hipEventRecord(ev[i], stream);
   };
   mark(0);
   mark(1);
   mark(2);
-  int32_t* to = token_ids_out ? token_ids_out : at<int32_t>(tgt.base, W.tids);
+  int32_t* to = token_ids_out ? token_ids_out : at<int32_t>(ws, W.tids);
   const hipError_t e = tls::launch_token_select_dense(P, q, codes, qparams, channels, ctx_lens, K_t,
-                                                      at<float>(tgt.base, W.dstats), at<uint32_t>(tgt.base, W.dkeys),
-                                                      to, tgt.err, stream);
+                                                      at<float>(ws, W.dstats), at<uint32_t>(ws, W.dkeys), to, err,
+                                                      stream);
   mark(3);
   mark(4);
   mark(5);
   if (e != hipSuccess) return TLS_ERR_HIP;
   return finish_decode(P, W, q, kv, ctx_lens, K_t, nsplit, tls::TokenList{to, K_t, tls::kListIds, P.B}, out, lse,
-                       tgt.base, tgt.err, ev, stream);
+                       ws, err, ev, stream);
 }
 
 // The single-level baselines (TLS_MODE_BLOCK_SPARSE, TLS_MODE_DENSE): block
@@ -470,7 +513,10 @@ tls_status single_level_decode(const Problem& P, int mode, const void* q, const 
   unsigned regions = sel ? (tls::kWsBlockSel | (block_ids_out ? 0u : tls::kWsBids)) : 0u;
   const int nsplit = attention_route(P, n_list, requested, &regions);
   tls::Workspace W;
-  if (!tgt.plan(P, dense ? 1 : K_b, K_t > 0 ? K_t : 1, regions, nsplit, &W)) return TLS_ERR_WORKSPACE_TOO_SMALL;
+  void* ws = nullptr;
+  uint32_t* err = nullptr;
+  st = tgt.bind(P, dense ? 1 : K_b, K_t > 0 ? K_t : 1, regions, nsplit, &W, &ws, &err);
+  if (st != TLS_OK) return st;
   auto mark = [&](int i) {
     if (ev) (void)hipEventRecord(ev[i], stream);
   };
@@ -478,12 +524,11 @@ tls_status single_level_decode(const Problem& P, int mode, const void* q, const 
   hipError_t e = hipSuccess;
   const int32_t* bids = block_ids_in;
   if (sel) {
-    int32_t* bo = block_ids_out ? block_ids_out : at<int32_t>(tgt.base, W.bids);
-    e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(tgt.base, W.qpn),
-                                at<float>(tgt.base, W.bscores), tgt.err, stream);
+    int32_t* bo = block_ids_out ? block_ids_out : at<int32_t>(ws, W.bids);
+    e = tls::launch_block_score(P, q, kmax, kmin, ctx_lens, at<float>(ws, W.qpn), at<float>(ws, W.bscores), err,
+                                stream);
     mark(1);
-    if (e == hipSuccess)
-      e = tls::launch_block_topk(P, at<float>(tgt.base, W.bscores), ctx_lens, K_b, bo, tgt.err, stream);
+    if (e == hipSuccess) e = tls::launch_block_topk(P, at<float>(ws, W.bscores), ctx_lens, K_b, bo, err, stream);
     bids = bo;
   } else {
     mark(1);
@@ -492,7 +537,7 @@ tls_status single_level_decode(const Problem& P, int mode, const void* q, const 
   if (e != hipSuccess) return TLS_ERR_HIP;
   const tls::TokenList tl = dense ? tls::TokenList{nullptr, 0, tls::kListAll, P.B}
                                   : tls::TokenList{bids, K_b, tls::kListBlocks, P.B};
-  return finish_decode(P, W, q, kv, ctx_lens, n_list, nsplit, tl, out, lse, tgt.base, tgt.err, ev, stream);
+  return finish_decode(P, W, q, kv, ctx_lens, n_list, nsplit, tl, out, lse, ws, err, ev, stream);
 }
 
 // tls_sparse_decode after the layout is validated, on a workspace target.
@@ -540,9 +585,10 @@ tls_status sparse_decode_on(const Problem& P, const void* q, const tls_kv_view* 
   if (sel_tokens) regions |= (fused ? 0u : tls::kWsTokenSel) | (token_ids_out ? 0u : tls::kWsTids);
   const int nsplit = attention_route(P, K_t, requested, &regions);
   tls::Workspace W;
-  if (!tgt.plan(P, K_b, K_t, regions, nsplit, &W)) return TLS_ERR_WORKSPACE_TOO_SMALL;
-  void* ws = tgt.base;
-  uint32_t* err = tgt.err;
+  void* ws = nullptr;
+  uint32_t* err = nullptr;
+  st = tgt.bind(P, K_b, K_t, regions, nsplit, &W, &ws, &err);
+  if (st != TLS_OK) return st;
 
   hipError_t e = hipSuccess;
   auto mark = [&](int i) {
@@ -600,30 +646,6 @@ tls_status sparse_decode_on(const Problem& P, const void* q, const tls_kv_view* 
                        ws, err, ev, stream);
 }
 
-// The library's own scratch for tls_sparse_decode_noalloc: one array per
-// device, resident from the library's load until the process ends.  Host
-// code never uses the array's name as an address: the device address comes
-// from hipGetSymbolAddress, once per device, with that device current.
-constexpr int kMaxDevices = 64;
-std::mutex g_scratch_mutex;
-void* g_scratch_ptr[kMaxDevices];  // guarded by g_scratch_mutex
-
-tls_status scratch_of_current_device(void** out) {
-  int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TLS_ERR_HIP;
-  std::lock_guard<std::mutex> lock(g_scratch_mutex);
-  if (!g_scratch_ptr[dev]) {
-    void* p = nullptr;
-    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
-      (void)hipGetLastError();
-      return TLS_ERR_HIP;
-    }
-    g_scratch_ptr[dev] = p;
-  }
-  *out = g_scratch_ptr[dev];
-  return TLS_OK;
-}
-
 }  // namespace
 
 extern "C" {
@@ -652,12 +674,8 @@ tls_status tls_sparse_decode_noalloc(const tls_layout* layout, const void* q, co
   Problem P;
   tls_status st = make_problem(layout, &P);
   if (st != TLS_OK) return st;
-  void* scr = nullptr;
-  st = scratch_of_current_device(&scr);
-  if (st != TLS_OK) return st;
-  // device-side error bits go to the caller's word; without one they land in
-  // the scratch header, which nothing reads
-  const WsTarget tgt{scr, kScratchBytes, device_error ? device_error : static_cast<uint32_t*>(scr), true};
+  // the scratch address is resolved once the arguments have passed (bind)
+  const WsTarget tgt{nullptr, kScratchBytes, device_error, true};
   return sparse_decode_on(P, q, kv, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t, block_ids_in,
                           token_ids_in, out, lse, block_ids_out, token_ids_out, opts, tgt, stream);
 }

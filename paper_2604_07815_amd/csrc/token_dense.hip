@@ -293,8 +293,7 @@ hipError_t launch_token_select_dense(const Problem& P, const void* q, const uint
                                     : launch_ds_e<F32>(P, q, codes, qparams, channels, ctx_lens, stats, keys, err, st);
   if (e != hipSuccess) return e;
   const size_t lds = (size_t(topk_scratch_words(kDsTopkThreads)) + kDsListCap) * sizeof(uint32_t);
-  const hipError_t a = hipFuncSetAttribute(reinterpret_cast<const void*>(ds_topk_kernel),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  const hipError_t a = allow_dynamic_lds(reinterpret_cast<const void*>(ds_topk_kernel), lds);
   if (a != hipSuccess) return a;
   ds_topk_kernel<<<P.units, kDsTopkThreads, lds, st>>>(keys, ctx_lens, P.H_kv, P.T, K_t, token_ids);
   return hipGetLastError();

@@ -513,11 +513,8 @@ hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32
   const size_t lds = (topk_scratch_words(1024) + size_t(align4w(K_b)) + size_t(S)) * sizeof(uint32_t);
   const int ept = (S + 1023) / 1024;
   auto go = [&](auto kern) {
-    if (lds > 65536) {
-      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-      if (e != hipSuccess) return e;
-    }
+    const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), lds);
+    if (e != hipSuccess) return e;
     kern<<<P.units, 1024, lds, st>>>(keys, block_ids, K_b, P.B, K_t, token_ids, token_scores);
     return hipGetLastError();
   };

@@ -53,11 +53,8 @@ static hipError_t launch_g(const Problem& P, const void* q, const uint8_t* codes
                            float* token_scores, uint32_t* err, hipStream_t st) {
   const size_t lds = mfma_select_lds_bytes(K_b * P.B, K_b, P.m_max);
   auto kern = token_select_mfma_kernel<G>;
-  if (lds > 65536) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-    if (e != hipSuccess) return e;
-  }
+  const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), lds);
+  if (e != hipSuccess) return e;
   kern<<<P.units, kSelNT, lds, st>>>((const uint16_t*)q, codes, qparams, channels, block_scores, block_ids_in,
                                      block_ids_out, ctx_lens, P.H_q, P.H_kv, P.d_qk, P.B, P.T, P.m_max, K_b, K_t,
                                      P.sigma, token_ids, token_scores, err);
