@@ -171,7 +171,6 @@ __global__ __launch_bounds__(1024) void block_topk_kernel(const float* __restric
                                                           int32_t* __restrict__ block_ids) {
   extern __shared__ uint32_t smem[];
   uint32_t* scratch = smem;
-  uint32_t* list = smem + topk_scratch_words(1024);
   const int unit = blockIdx.x;
   const int s = unit / H_kv;
   int n = ctx_lens[s];
@@ -185,7 +184,7 @@ __global__ __launch_bounds__(1024) void block_topk_kernel(const float* __restric
     kr[j] = i < m ? float_key(sc[i]) : kInvalidKey;
   }
   wg_topk_regs<1024, EPT>(kr, K_b, block_ids + size_t(unit) * K_b, K_b, nullptr, [](int, int i) { return int32_t(i); },
-                          scratch, list);
+                          scratch);
 }
 
 template <class E, int LPB, int CPL>
@@ -226,7 +225,7 @@ hipError_t launch_block_score(const Problem& P, const void* q, const void* kmax,
 hipError_t launch_block_topk(const Problem& P, const float* scores, const int32_t* ctx_lens, int K_b,
                              int32_t* block_ids, uint32_t* err, hipStream_t st) {
   (void)err;
-  const size_t lds = (topk_scratch_words(1024) + size_t(P.m_max)) * sizeof(uint32_t);
+  const size_t lds = size_t(topk_scratch_words(1024)) * sizeof(uint32_t);
   const int ept = (P.m_max + 1023) / 1024;
   auto go = [&](auto kern) {
     const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), lds);

@@ -433,7 +433,7 @@ __global__ __launch_bounds__(256) void token_alpha_kernel_g(
 
 // Top-K_t of the alpha keys of each unit, one work-group per unit.  Thread t
 // holds the keys of slots t + 1024 j (j < EPT), requested together straight
-// into registers; the list of keys in play lives in LDS.
+// into registers.
 template <int EPT>
 __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __restrict__ keys,
                                                            const int32_t* __restrict__ block_ids, int K_b,
@@ -443,7 +443,6 @@ __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __rest
   uint32_t* scratch = smem;
   int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(1024));
   const int S = K_b * B;
-  uint32_t* list = smem + topk_scratch_words(1024) + align4w(K_b);
   const int unit = blockIdx.x;
   uint32_t kr[EPT];
 #pragma unroll
@@ -455,7 +454,7 @@ __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __rest
   __syncthreads();
   wg_topk_regs<1024, EPT>(kr, K_t, token_ids + size_t(unit) * K_t, K_t,
                           token_scores ? token_scores + size_t(unit) * K_t : nullptr,
-                          [=](int, int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch, list);
+                          [=](int, int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch);
 }
 
 template <int HT, int NGR>
@@ -510,7 +509,7 @@ hipError_t launch_token_alpha(const Problem& P, const float* logits, const float
 hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32_t* block_ids, int K_b,
                              int K_t, int32_t* token_ids, float* token_scores, hipStream_t st) {
   const int S = K_b * P.B;
-  const size_t lds = (topk_scratch_words(1024) + size_t(align4w(K_b)) + size_t(S)) * sizeof(uint32_t);
+  const size_t lds = (topk_scratch_words(1024) + size_t(align4w(K_b))) * sizeof(uint32_t);
   const int ept = (S + 1023) / 1024;
   auto go = [&](auto kern) {
     const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), lds);

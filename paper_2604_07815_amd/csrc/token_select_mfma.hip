@@ -43,7 +43,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
 bool fused_token_select_ok(const Problem& P, int K_b, int K_t) {
   const int S = K_b * P.B;
   return P.dtype == 1 && P.G >= 1 && P.G <= kSelMaxG && P.d_c == 32 && (P.B & (P.B - 1)) == 0 && S <= kSelMaxSlots &&
-         P.m_max <= kSelMaxBlocks && mfma_select_lds_bytes(S, K_b, P.m_max) <= kSelMaxLds;
+         P.m_max <= kSelMaxBlocks && mfma_select_lds_bytes(K_b) <= kSelMaxLds;
 }
 
 template <int G>
@@ -51,7 +51,7 @@ static hipError_t launch_g(const Problem& P, const void* q, const uint8_t* codes
                            const int32_t* channels, const float* block_scores, const int32_t* block_ids_in,
                            int32_t* block_ids_out, const int32_t* ctx_lens, int K_b, int K_t, int32_t* token_ids,
                            float* token_scores, uint32_t* err, hipStream_t st) {
-  const size_t lds = mfma_select_lds_bytes(K_b * P.B, K_b, P.m_max);
+  const size_t lds = mfma_select_lds_bytes(K_b);
   auto kern = token_select_mfma_kernel<G>;
   const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), lds);
   if (e != hipSuccess) return e;

@@ -26,14 +26,9 @@ constexpr uint32_t kBf16Base = 0x43434343u;  // high byte of bf16(128 + c), c < 
 __device__ constexpr int kSliceChan[8] = {0, 2, 1, 3, 4, 6, 5, 7};
 
 // LDS words: top-k scratch | block list | q~ table (4 heads x 32 channels of
-// bf16, in slice order) | per-wave partials | list of keys in play
-// (max(m_max, S)).
-__host__ __device__ inline size_t list_words(int S, int m_max) { return size_t(S > m_max ? S : m_max); }
-
-inline size_t mfma_select_lds_bytes(int S, int K_b, int m_max) {
-  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(K_b)) + 64 + kSelNW * 12 +
-          align4w(int(list_words(S, m_max)))) *
-         sizeof(uint32_t);
+// bf16, in slice order) | per-wave partials.
+inline size_t mfma_select_lds_bytes(int K_b) {
+  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(K_b)) + 64 + kSelNW * 12) * sizeof(uint32_t);
 }
 
 // The fused selection of one unit by a 1024-thread work-group, on LDS
@@ -50,7 +45,6 @@ __device__ inline void token_select_mfma_body(
   int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(NT));
   uint16_t* s_qt = reinterpret_cast<uint16_t*>(s_bl + align4w(K_b));  // [4][32] (64 words)
   float* s_red = reinterpret_cast<float*>(s_qt + 128);                    // [NW][12]
-  uint32_t* list = reinterpret_cast<uint32_t*>(s_red + NW * 12);
   const int S = K_b * B;
 
   const int s = unit / H_kv, g = unit % H_kv;
@@ -99,7 +93,7 @@ __device__ inline void token_select_mfma_body(
     s_qt[tid] = v;
   }
   if (block_scores) {
-    wg_topk_regs<NT, kSelBPT>(bk, K_b, s_bl, K_b, nullptr, [](int, int i) { return int32_t(i); }, scratch, list);
+    wg_topk_regs<NT, kSelBPT>(bk, K_b, s_bl, K_b, nullptr, [](int, int i) { return int32_t(i); }, scratch);
   }
   __syncthreads();
 
@@ -247,7 +241,7 @@ __device__ inline void token_select_mfma_body(
   const TopkKnown known{n_valid, float_key(bsum * invG), float_key(0.f)};
   wg_topk_regs<NT, kSelSPT>(keys, K_t, token_ids + size_t(unit) * K_t, K_t,
                             token_scores ? token_scores + size_t(unit) * K_t : nullptr,
-                            [&](int j, int) { return tokpos[j]; }, scratch, list, &known);
+                            [&](int j, int) { return tokpos[j]; }, scratch, &known);
   if (block_scores && block_ids_out)
     for (int i = tid; i < K_b; i += NT) block_ids_out[size_t(unit) * K_b + i] = s_bl[i];
 }

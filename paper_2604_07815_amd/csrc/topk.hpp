@@ -34,56 +34,71 @@ __host__ __device__ constexpr int align4w(int words) { return (words + 3) & ~3; 
 // ascending position order to out[0, k'), k' = min(k, #valid keys), then -1
 // up to out_cap.  Thread t holds the keys of positions t + j*NT, j < EPT
 // (kInvalidKey marks an empty position, never selected).  out_scores
-// (nullable) receives key_float of each selected key.  `list` (LDS, as many
-// words as there are valid keys) is clobbered.  Each thread writes its own
-// selected positions straight to `out` (global memory, or LDS that the
+// (nullable) receives key_float of each selected key.  Each thread writes its
+// own selected positions straight to `out` (global memory, or LDS that the
 // caller reads after a barrier): no staging and no trailing barrier.  Every
 // thread of the work-group must call it, with k uniform.
 //
 // Method: an MSB-first radix select over the bits where the valid keys
 // differ (8-bit digits, LDS histograms) finds the k'-th largest key T and the
-// number r of keys equal to T to take.  The first pass reads the registers;
-// the keys still in play after it are gathered into `list`, so the later
-// passes touch only those.  An ordered compaction then emits every key > T
-// and the first r keys == T: per (key slot j, wave) counts in position order
-// (j-major, then wave, then lane) give every key its output index with one
-// barrier, so the output is ordered by position without a sort.
-// Run by one whole wave after a pass's histogram is complete: finds the
-// digit holding the remaining-th largest key in play (digits scanned from
-// the top; lane L owns digits 255-4L .. 252-4L, summed over the histogram
-// copies) and publishes misc[48] = digit, misc[49] = keys in higher digits,
-// misc[51] = 1 when the digit's keys are all taken, misc[52] = its key count.
-__device__ inline void topk_scan_pass(const uint32_t* h, int remaining, uint32_t* misc) {
+// number r of keys equal to T to take.  Every pass counts the keys still in
+// play straight from the registers (a key is only compared with the prefix
+// found so far, so later passes cost a few compares per key), into a
+// histogram of its own; after the pass's one barrier every wave scans that
+// histogram itself, so no broadcast and no second barrier follow.  An ordered
+// compaction then emits every key > T and the first r keys == T: per (key
+// slot j, wave) counts in position order (j-major, then wave, then lane) give
+// every key its output index with one barrier, so the output is ordered by
+// position without a sort.
+// The digit of one radix pass: the digit holding the remaining-th largest key
+// in play, the number of keys in play in higher digits, and its own count.
+struct TopkDigit {
+  uint32_t digit, above, cnt;
+};
+
+// Run by a whole wave after a pass's histogram is complete: scans the digits
+// from the top and returns the pass's digit, the same in every lane.  Lane L
+// reads digits 255 - (64 j + L), j < 4 (summed over the histogram copies), so
+// the lanes of one read touch consecutive words (no bank conflicts); a wave
+// prefix sum per quarter, from the top quarter down, locates the digit.
+// Every wave that runs it on the same histogram gets the same answer, so no
+// broadcast (and no barrier after it) is needed.
+__device__ inline TopkDigit topk_scan_wave(const uint32_t* h, int remaining) {
   const int lane = __lane_id();
-  uint32_t c[4];
-  uint32_t local = 0;
+  TopkDigit r{255u, 0u, 0u};  // stands in if the histogram held fewer keys than `remaining`
+  uint32_t before = 0;        // keys in play in the quarters above (uniform)
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    c[j] = 0;
+    const int dgt = 255 - 64 * j - lane;
+    uint32_t c = 0;
 #pragma unroll
-    for (int cp = 0; cp < kTopkHistCopies; ++cp) c[j] += h[cp * kTopkHistStride + 255 - 4 * lane - j];
-    local += c[j];
-  }
-  const uint32_t incl = wave_incl_scan_u32(local);
-  uint32_t run = incl - local;
-  int found = -1;
-  uint32_t found_above = 0, found_cnt = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (found < 0 && run + c[j] >= uint32_t(remaining)) {
-      found = 255 - 4 * lane - j;
-      found_above = run;
-      found_cnt = c[j];
+    for (int cp = 0; cp < kTopkHistCopies; ++cp) c += h[cp * kTopkHistStride + dgt];
+    const uint32_t incl = wave_incl_scan_u32(c);
+    const uint32_t tot = uint32_t(__builtin_amdgcn_readlane(int(incl), 63));
+    if (before + tot >= uint32_t(remaining)) {
+      // the first lane whose running count reaches `remaining` holds the digit
+      const uint64_t hit = __ballot(before + incl >= uint32_t(remaining));
+      const int src = __ffsll((unsigned long long)hit) - 1;
+      r.digit = uint32_t(255 - 64 * j - src);
+      r.above = before + uint32_t(__builtin_amdgcn_readlane(int(incl - c), src));
+      r.cnt = uint32_t(__builtin_amdgcn_readlane(int(c), src));
+      break;
     }
-    run += c[j];
+    before += tot;
   }
-  const uint64_t hit = __ballot(found >= 0);
-  const int src = __ffsll((unsigned long long)hit) - 1;
-  if (lane == src) {
-    misc[48] = uint32_t(found);
-    misc[49] = found_above;
-    misc[51] = found_cnt == uint32_t(remaining) - found_above ? 1u : 0u;
-    misc[52] = found_cnt;
+  return r;
+}
+
+// topk_scan_wave run by one wave, publishing misc[48] = digit, misc[49] =
+// keys in higher digits, misc[51] = 1 when the digit's keys are all taken,
+// misc[52] = its key count (for the other waves, after a barrier).
+__device__ inline void topk_scan_pass(const uint32_t* h, int remaining, uint32_t* misc) {
+  const TopkDigit r = topk_scan_wave(h, remaining);
+  if (__lane_id() == 0) {
+    misc[48] = r.digit;
+    misc[49] = r.above;
+    misc[51] = r.cnt == uint32_t(remaining) - r.above ? 1u : 0u;
+    misc[52] = r.cnt;
   }
 }
 
@@ -174,12 +189,11 @@ template <int NT>
 __device__ inline void topk_prepare(uint32_t* scratch) {
   constexpr int kHistAll = align4w_c(4 * kTopkHistWords);
   for (int i = threadIdx.x; i < kHistAll; i += NT) scratch[i] = 0u;
-  if (threadIdx.x == 0) scratch[kHistAll + 50] = 0u;
 }
 
 template <int NT, int EPT, class Map>
 __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int out_cap, float* out_scores,
-                             Map map, uint32_t* scratch, uint32_t* list, const TopkKnown* known = nullptr) {
+                             Map map, uint32_t* scratch, const TopkKnown* known = nullptr) {
   constexpr int NW = NT / 64;
   static_assert(NW >= 1 && NW <= kTopkMaxNW && EPT >= 1 && EPT <= kTopkMaxEPT, "work-group shape");
   // the ordered compaction gives lane L the (slot, wave) entries L*PER ..
@@ -189,7 +203,7 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   constexpr int kHistAll = align4w_c(4 * kTopkHistWords);
   uint32_t* hist = scratch;             // [4 passes][copies][stride]
-  uint32_t* misc = scratch + kHistAll;  // [64]: 0..47 wave partials, 48/49/51/52 pass result, 50 list length
+  uint32_t* misc = scratch + kHistAll;  // [64]: 0..47 wave partials
   uint32_t* cg = misc + 64;             // [EPT][NW] keys > T per (slot, wave)
   uint32_t* ce = cg + kTopkMaxEPT * kTopkMaxNW;  // [EPT][NW] keys == T
 
@@ -217,7 +231,6 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
       misc[16 + wid] = kmx;
       misc[32 + wid] = kmn;
     }
-    if (tid == 0) misc[50] = 0u;
     __syncthreads();
     {
       const int w = lane & 15;
@@ -238,60 +251,31 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
     pmask = bits_left >= 32 ? 0u : ~((1u << bits_left) - 1u);
     prefix = kmx & pmask;
   }
-  int list_n = -1;  // < 0: the keys in play are still the registers
+  // at most four 8-bit passes, each on its own histogram: a wave still
+  // scanning pass p's histogram never sees pass p+1's counts
   for (int pass = 0; bits_left > 0; ++pass) {
     const int nb = bits_left < 8 ? bits_left : 8;
     const int shift = bits_left - nb;
     const uint32_t dmask = (1u << nb) - 1u;
     uint32_t* h = hist + kTopkHistWords * pass;
     uint32_t* hc = h + (lane % kTopkHistCopies) * kTopkHistStride;
-    if (list_n < 0) {
 #pragma unroll
-      for (int j = 0; j < EPT; ++j) {
-        const uint32_t key = kr[j];
-        if (key != kInvalidKey && (key & pmask) == prefix) atomicAdd(&hc[(key >> shift) & dmask], 1u);
-      }
-    } else {
-      for (int i = tid; i < list_n; i += NT) {
-        const uint32_t key = list[i];
-        if ((key & pmask) == prefix) atomicAdd(&hc[(key >> shift) & dmask], 1u);
-      }
+    for (int j = 0; j < EPT; ++j) {
+      const uint32_t key = kr[j];
+      if (key != kInvalidKey && (key & pmask) == prefix) atomicAdd(&hc[(key >> shift) & dmask], 1u);
     }
     __syncthreads();
-    if (wid == 0) topk_scan_pass(h, remaining, misc);
-    __syncthreads();
-    prefix |= misc[48] << shift;
-    remaining -= int(misc[49]);
+    const TopkDigit dg = topk_scan_wave(h, remaining);
+    prefix |= dg.digit << shift;
+    remaining -= int(dg.above);
     pmask |= dmask << shift;
     bits_left -= nb;
-    if (misc[51] && bits_left > 0 && prefix != 0u) {
+    if (dg.cnt == uint32_t(remaining) && bits_left > 0 && prefix != 0u) {
       // the threshold's bucket is taken whole: every key >= prefix is
       // selected, i.e. T = prefix - 1 with no equal keys to take
       prefix -= 1u;
       remaining = 0;
       bits_left = 0;
-    }
-    if (list_n < 0 && bits_left > 0) {
-      // gather the keys still in play; one list reservation per wave
-      uint32_t wcount = 0;
-#pragma unroll
-      for (int j = 0; j < EPT; ++j) {
-        const uint32_t key = kr[j];
-        wcount += uint32_t(__popcll(__ballot(key != kInvalidKey && (key & pmask) == prefix)));
-      }
-      uint32_t base = 0;
-      if (lane == 0 && wcount) base = atomicAdd(&misc[50], wcount);
-      base = uint32_t(__builtin_amdgcn_readfirstlane(int(base)));
-#pragma unroll
-      for (int j = 0; j < EPT; ++j) {
-        const uint32_t key = kr[j];
-        const bool in = key != kInvalidKey && (key & pmask) == prefix;
-        const uint64_t bal = __ballot(in);
-        if (in) list[base + lanes_below(bal)] = key;
-        base += uint32_t(__popcll(bal));
-      }
-      __syncthreads();
-      list_n = int(misc[50]);
     }
   }
   const uint32_t T = prefix;
@@ -306,33 +290,6 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
     if (out_scores) out_scores[i] = 0.0f;
   }
 }
-
-template <int NT, int EPT, class Map>
-__device__ void wg_topk_lds_ept(uint32_t* keys, int n, int k, int32_t* out, int out_cap, float* out_scores, Map map,
-                                uint32_t* scratch) {
-  uint32_t kr[EPT];
-#pragma unroll
-  for (int j = 0; j < EPT; ++j) {
-    const int p = threadIdx.x + j * NT;
-    kr[j] = p < n ? keys[p] : kInvalidKey;
-  }
-  // the key array becomes the list of keys in play once every thread has
-  // read it (the selection's first barrier comes before any list write)
-  wg_topk_regs<NT, EPT>(kr, k, out, out_cap, out_scores, map, scratch, keys);
-}
-
-// The same selection over keys[0, n) in LDS (clobbered), n <= NT*kTopkMaxEPT.
-template <int NT, class Map>
-__device__ void wg_topk_ascending(uint32_t* keys, int n, int k, int32_t* out, int out_cap, float* out_scores,
-                                  Map map, uint32_t* scratch) {
-  const int ept = (n + NT - 1) / NT;
-  if (ept <= 1) wg_topk_lds_ept<NT, 1>(keys, n, k, out, out_cap, out_scores, map, scratch);
-  else if (ept <= 2) wg_topk_lds_ept<NT, 2>(keys, n, k, out, out_cap, out_scores, map, scratch);
-  else if (ept <= 4) wg_topk_lds_ept<NT, 4>(keys, n, k, out, out_cap, out_scores, map, scratch);
-  else if (ept <= 8) wg_topk_lds_ept<NT, 8>(keys, n, k, out, out_cap, out_scores, map, scratch);
-  else wg_topk_lds_ept<NT, 16>(keys, n, k, out, out_cap, out_scores, map, scratch);
-}
-
 
 // The same selection over keys[0, n) in global memory, for more keys than
 // the registers hold (token-level selection over a whole context): every
