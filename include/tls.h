@@ -142,8 +142,27 @@ typedef struct tls_kv_view {
  *                         largest, then attention over those tokens.  kmax
  *                         and kmin are not used; the block-id arguments and
  *                         token_ids_in must be NULL; token_ids_out receives
- *                         the selection.  G must be 1, 2, 4, 8, 16 or 32. */
-enum { TLS_MODE_TWO_LEVEL = 0, TLS_MODE_BLOCK_SPARSE = 1, TLS_MODE_DENSE = 2, TLS_MODE_TOKEN_SPARSE = 3 };
+ *                         the selection.  G must be 1, 2, 4, 8, 16 or 32.
+ *   TLS_MODE_LAGGED       the two-level operator with the one-step lag of the
+ *                         offloaded tier (Sec. 4.2): block selection from
+ *                         this step's query writes M_t to block_ids_out (the
+ *                         blocks to bring in for the next step), while token
+ *                         selection and attention run over the blocks of
+ *                         block_ids_in (M_{t-1}, already resident).  Both
+ *                         lists are required and must not overlap; kmax,
+ *                         kmin, codes, qparams and channels are required;
+ *                         token_ids_in must be NULL.  The same results as
+ *                         tls_select_blocks into block_ids_out followed by
+ *                         the two-level operator with block_ids_in, in one
+ *                         call; stage event 5 (after token selection) marks
+ *                         the point where block_ids_out is complete. */
+enum {
+  TLS_MODE_TWO_LEVEL = 0,
+  TLS_MODE_BLOCK_SPARSE = 1,
+  TLS_MODE_DENSE = 2,
+  TLS_MODE_TOKEN_SPARSE = 3,
+  TLS_MODE_LAGGED = 4
+};
 
 /* Optional knobs of tls_sparse_decode; pass NULL for defaults. */
 typedef struct tls_decode_opts {
@@ -272,7 +291,10 @@ tls_status tls_select_tokens(const tls_layout* layout, const void* q, const uint
  * codes, qparams and channels may be NULL).  out receives the attention
  * output in the input dtype (round to nearest even for bf16), lse (nullable)
  * the fp32 log-sum-exp; an empty selection gives out = 0, lse = -inf.
- * block_ids_out / token_ids_out (nullable) receive the selections. */
+ * block_ids_out / token_ids_out (nullable) receive the selections.  With
+ * opts->mode = TLS_MODE_LAGGED (Sec. 4.2) block_ids_in is the previous
+ * step's selection the tokens are chosen from, and block_ids_out receives
+ * this step's block selection. */
 tls_status tls_sparse_decode(const tls_layout* layout, const void* q, const tls_kv_view* kv,
                              const int32_t* ctx_lens, const void* kmax, const void* kmin,
                              const uint8_t* codes, const float* qparams, const int32_t* channels,

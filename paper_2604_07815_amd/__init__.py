@@ -24,7 +24,7 @@ __all__ = [
     "tls_prefill_kv", "tls_offload_kv", "tls_init_residency", "tls_calibrate_absmax", "tls_calibrate_channels",
     "tls_append_tokens", "sparse_decode_args", "lib", "make_layout", "alloc_workspace", "DTYPE_F32", "DTYPE_BF16",
     "EXPORTED_SYMBOLS",
-    "MODE_TWO_LEVEL", "MODE_BLOCK_SPARSE", "MODE_DENSE", "MODE_TOKEN_SPARSE",
+    "MODE_TWO_LEVEL", "MODE_BLOCK_SPARSE", "MODE_DENSE", "MODE_TOKEN_SPARSE", "MODE_LAGGED",
     "DEVERR_CTX_LEN", "DEVERR_BLOCK_ID", "DEVERR_TOKEN_ID", "DEVERR_SLOT", "DEVERR_POOL_FULL", "DEVERR_CHANNEL",
 ]
 
@@ -32,7 +32,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtls.so")
 
 OK, INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP_ERROR = 0, 1, 2, 3, 4
 DTYPE_F32, DTYPE_BF16 = 0, 1
-MODE_TWO_LEVEL, MODE_BLOCK_SPARSE, MODE_DENSE, MODE_TOKEN_SPARSE = 0, 1, 2, 3
+MODE_TWO_LEVEL, MODE_BLOCK_SPARSE, MODE_DENSE, MODE_TOKEN_SPARSE, MODE_LAGGED = 0, 1, 2, 3, 4
 NUM_STAGE_EVENTS = 8
 DEVERR_CTX_LEN, DEVERR_BLOCK_ID, DEVERR_TOKEN_ID, DEVERR_SLOT, DEVERR_POOL_FULL, DEVERR_CHANNEL = 1, 2, 4, 8, 16, 32
 
@@ -263,7 +263,8 @@ def tls_sparse_decode(layout, q, kv: KV, ctx_lens, kmax, kmin, codes, qparams, c
                       attn_splits: int = 0, stage_events: Optional[Sequence[int]] = None,
                       mode: int = MODE_TWO_LEVEL, stream=None) -> None:
     """One decode step.  stage_events: NUM_STAGE_EVENTS raw hipEvent_t handles;
-    mode: MODE_TWO_LEVEL, or one of the single-level baselines."""
+    mode: MODE_TWO_LEVEL, MODE_LAGGED (tokens from block_ids_in, this step's
+    block selection to block_ids_out), or one of the single-level baselines."""
     args, keep = sparse_decode_args(layout, q, kv, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t,
                                      block_ids_in, token_ids_in, out, lse, block_ids_out, token_ids_out, ws,
                                      attn_splits, stage_events, mode, stream)

@@ -65,9 +65,10 @@ __global__ __launch_bounds__(256) void block_score_kernel(
   using S = typename E::T;
   constexpr int V = E::kVec;
   constexpr int NG = 256 / LPB;  // lane groups per work-group
-  __shared__ float s_qp[1024], s_qn[1024];
   const int unit = blockIdx.y;
   const int s = unit / H_kv, g = unit % H_kv;
+  const int li = threadIdx.x % LPB, grp = threadIdx.x / LPB;
+  const int nch = d / V;
   int n = ctx_lens[s];
   if (n < 0 || n > T) {
     if (threadIdx.x == 0 && blockIdx.x == 0) set_error(err, 1u);
@@ -80,12 +81,49 @@ __global__ __launch_bounds__(256) void block_score_kernel(
     for (int i = c0 + threadIdx.x; i < c1; i += 256) out[i] = -INFINITY;
     return;
   }
+  const size_t ubase = size_t(unit) * m_max;
+  // Loads are unconditional at clamped rows so that, with no branch around
+  // each load, all of them stay in flight together: a block past the
+  // work-group's last valid one re-reads that block (its result is replaced
+  // by -inf below), a lane past d reads channel 0 (its partial is dropped).
+  // Every row read is a written summary of the unit.
+  const int blk_hi = min(c1, m) - 1;  // >= c0 here
+  uint4 vmax[kBlkUnroll][CPL], vmin[kBlkUnroll][CPL];
+  auto request = [&](int b0) {
+#pragma unroll
+    for (int u = 0; u < kBlkUnroll; ++u) {
+      const int blk = b0 + u * NG;
+      const int rb = blk < blk_hi ? blk : blk_hi;
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) {
+        const int c = li + k * LPB;
+        const int rc = c < nch ? c : 0;
+        vmax[u][k] = ld16_stream(kmax + (ubase + rb) * d + rc * V);
+        vmin[u][k] = ld16_stream(kmin + (ubase + rb) * d + rc * V);
+      }
+    }
+  };
+  // Q+ / Q- of this lane's channels.  Narrow groups sum the heads here, in
+  // ascending order (one channel per thread, through LDS), before the first
+  // batch of summaries is requested; wide groups read the per-unit sums
+  // straight into registers after requesting it, so those reads overlap.
+  float qp[CPL][V], qn[CPL][V];
+  int b0 = c0 + grp;
   if (qpn) {
-    for (int c = threadIdx.x; c < d; c += 256) {
-      s_qp[c] = qpn[(size_t(unit) * 2) * d + c];
-      s_qn[c] = qpn[(size_t(unit) * 2 + 1) * d + c];
+    request(b0);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) {
+      const int c = li + k * LPB;
+      const float* pp = qpn + (size_t(unit) * 2) * d + (c < nch ? c : 0) * V;
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        qp[k][e] = pp[e];
+        qn[k][e] = pp[d + e];
+      }
     }
   } else {
+    __shared__ float s_qp[1024], s_qn[1024];
     const S* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
     for (int c = threadIdx.x; c < d; c += 256) {
       float p = 0.f, ng = 0.f;
@@ -106,42 +144,20 @@ __global__ __launch_bounds__(256) void block_score_kernel(
       s_qp[c] = p;
       s_qn[c] = ng;
     }
-  }
-  __syncthreads();
-  const int li = threadIdx.x % LPB, grp = threadIdx.x / LPB;
-  const int nch = d / V;
-  float qp[CPL][V], qn[CPL][V];
+    __syncthreads();
 #pragma unroll
-  for (int k = 0; k < CPL; ++k) {
-    const int c = li + k * LPB;
+    for (int k = 0; k < CPL; ++k) {
+      const int c = li + k * LPB;
 #pragma unroll
-    for (int e = 0; e < V; ++e) {
-      qp[k][e] = c < nch ? s_qp[c * V + e] : 0.f;
-      qn[k][e] = c < nch ? s_qn[c * V + e] : 0.f;
-    }
-  }
-  const size_t ubase = size_t(unit) * m_max;
-  // Loads are unconditional at clamped rows so that, with no branch around
-  // each load, all of them stay in flight together: a block past the
-  // work-group's last valid one re-reads that block (its result is replaced
-  // by -inf below), a lane past d reads channel 0 (its partial is dropped).
-  // Every row read is a written summary of the unit.
-  const int blk_hi = min(c1, m) - 1;  // >= c0 here
-  for (int b0 = c0 + grp; b0 < c1; b0 += NG * kBlkUnroll) {
-    uint4 vmax[kBlkUnroll][CPL], vmin[kBlkUnroll][CPL];
-#pragma unroll
-    for (int u = 0; u < kBlkUnroll; ++u) {
-      const int blk = b0 + u * NG;
-      const int rb = blk < blk_hi ? blk : blk_hi;
-#pragma unroll
-      for (int k = 0; k < CPL; ++k) {
-        const int c = li + k * LPB;
-        const int rc = c < nch ? c : 0;
-        vmax[u][k] = ld16_stream(kmax + (ubase + rb) * d + rc * V);
-        vmin[u][k] = ld16_stream(kmin + (ubase + rb) * d + rc * V);
+      for (int e = 0; e < V; ++e) {
+        qp[k][e] = c < nch ? s_qp[c * V + e] : 0.f;
+        qn[k][e] = c < nch ? s_qn[c * V + e] : 0.f;
       }
     }
-    __builtin_amdgcn_sched_barrier(0);  // every load of the batch is issued before the first use
+    request(b0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (;;) {
 #pragma unroll
     for (int u = 0; u < kBlkUnroll; ++u) {
       const int blk = b0 + u * NG;
@@ -159,6 +175,10 @@ __global__ __launch_bounds__(256) void block_score_kernel(
       acc = wave_sum<LPB>(acc);
       if (li == 0 && blk < c1) out[blk] = blk < m ? acc : -INFINITY;
     }
+    b0 += NG * kBlkUnroll;
+    if (b0 >= c1) break;
+    request(b0);
+    __builtin_amdgcn_sched_barrier(0);  // every load of the batch is issued before the first use
   }
 }
 

@@ -78,7 +78,10 @@ hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32
                              int K_t, int32_t* token_ids, float* token_scores, hipStream_t st);
 
 // One work-group per unit: (optional) block top-k from block_scores, then the
-// whole token selection on chip.  Valid when fused_token_select_ok().
+// whole token selection on chip, over the selected blocks or, when
+// block_ids_in is given, over those (with block_scores as well, the new
+// selection is written to block_ids_out: the lagged operator).  Valid when
+// fused_token_select_ok().
 bool fused_token_select_ok(const Problem& P, int K_b, int K_t);
 hipError_t launch_token_select_fused(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,
                                      const int32_t* channels, const float* block_scores,

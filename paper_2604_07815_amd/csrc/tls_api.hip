@@ -557,7 +557,7 @@ tls_status sparse_decode_on(const Problem& P, const void* q, const tls_kv_view* 
     for (int i = 0; i < 6; ++i)
       if (opts->reserved[i] != 0) return TLS_ERR_INVALID_ARGUMENT;
     if (opts->attn_splits < 0 || opts->attn_splits > tls::kMaxSplits) return TLS_ERR_INVALID_ARGUMENT;
-    if (opts->mode < TLS_MODE_TWO_LEVEL || opts->mode > TLS_MODE_TOKEN_SPARSE) return TLS_ERR_INVALID_ARGUMENT;
+    if (opts->mode < TLS_MODE_TWO_LEVEL || opts->mode > TLS_MODE_LAGGED) return TLS_ERR_INVALID_ARGUMENT;
     requested = opts->attn_splits;
     mode = opts->mode;
     ev = opts->stage_events;
@@ -565,12 +565,21 @@ tls_status sparse_decode_on(const Problem& P, const void* q, const tls_kv_view* 
       for (int i = 0; i < TLS_NUM_STAGE_EVENTS; ++i)
         if (!ev[i]) return TLS_ERR_INVALID_ARGUMENT;
   }
-  if (mode != TLS_MODE_TWO_LEVEL)
+  const bool lagged = mode == TLS_MODE_LAGGED;
+  if (mode != TLS_MODE_TWO_LEVEL && !lagged)
     return single_level_decode(P, mode, q, kv, ctx_lens, kmax, kmin, codes, qparams, channels, K_b, K_t,
                                block_ids_in, token_ids_in, out, lse, block_ids_out, token_ids_out, tgt, requested,
                                ev, stream);
+  if (lagged) {
+    // tokens from the given (previous step's) blocks, this step's block
+    // selection to block_ids_out; the two lists must not overlap
+    if (!block_ids_in || !block_ids_out || token_ids_in) return TLS_ERR_INVALID_ARGUMENT;
+    const size_t n_ids = size_t(P.units) * size_t(K_b > 0 ? K_b : 0);
+    const int32_t* out_end = block_ids_out + n_ids;
+    if (block_ids_in < out_end && block_ids_out < block_ids_in + n_ids) return TLS_ERR_INVALID_ARGUMENT;
+  }
   const bool sel_tokens = token_ids_in == nullptr;
-  const bool sel_blocks = sel_tokens && block_ids_in == nullptr;
+  const bool sel_blocks = lagged || (sel_tokens && block_ids_in == nullptr);
   if (sel_blocks && (!kmax || !kmin)) return TLS_ERR_INVALID_ARGUMENT;
   if (sel_tokens && (!codes || !qparams || !channels)) return TLS_ERR_INVALID_ARGUMENT;
   tls_status st = check_budgets(P, K_b, K_t);
@@ -610,7 +619,7 @@ tls_status sparse_decode_on(const Problem& P, const void* q, const tls_kv_view* 
     if (e == hipSuccess)
       e = tls::launch_token_select_fused(P, q, codes, qparams, channels, bsc, block_ids_in,
                                          sel_blocks ? block_ids_out : nullptr, ctx_lens, K_b, K_t, to, nullptr, err,
-                                         stream);
+                                         stream);  // scores and a given list: the lagged operator
     mark(3);
     mark(4);
     mark(5);
@@ -624,7 +633,7 @@ tls_status sparse_decode_on(const Problem& P, const void* q, const tls_kv_view* 
                                 stream);
     mark(1);
     if (e == hipSuccess) e = tls::launch_block_topk(P, at<float>(ws, W.bscores), ctx_lens, K_b, bo, err, stream);
-    bids = bo;
+    if (!lagged) bids = bo;  // the lagged operator selects tokens from the given blocks
   } else {
     mark(1);
   }

@@ -1,6 +1,8 @@
 // Fused two-level selection for grouped-query layouts (AsyncTLS Sec. 4.1):
 // one 1024-thread work-group per (sequence, KV head) unit runs, on chip,
-//   1. top-K_b over the unit's block scores (or takes a given block list);
+//   1. top-K_b over the unit's block scores (or takes a given block list;
+//      with both, the lagged operator of Sec. 4.2: the new top-K_b goes to
+//      the output list and the tokens are chosen from the given blocks);
 //   2. the approximate logits of every candidate token,
 //        l_hj = sigma * q~_h . dequant(k~_j)
 //             = sigma * (min_j * sum_c q~_hc + scale_j * sum_c q~_hc code_jc);

@@ -67,7 +67,10 @@ __device__ inline void token_select_mfma_body(
       const int i = tid + j * NT;
       bk[j] = i < m ? float_key(sc[i]) : kInvalidKey;
     }
-  } else {
+  }
+  if (block_ids_in) {
+    // the candidate blocks are given (with block scores too: the lagged
+    // operator, whose new block selection goes to block_ids_out)
     for (int i = tid; i < K_b; i += NT) {
       int b = block_ids_in[size_t(unit) * K_b + i];
       if (b >= m) {
@@ -93,7 +96,8 @@ __device__ inline void token_select_mfma_body(
     s_qt[tid] = v;
   }
   if (block_scores) {
-    wg_topk_regs<NT, kSelBPT>(bk, K_b, s_bl, K_b, nullptr, [](int, int i) { return int32_t(i); }, scratch);
+    int32_t* dst = block_ids_in ? block_ids_out + size_t(unit) * K_b : s_bl;
+    wg_topk_regs<NT, kSelBPT>(bk, K_b, dst, K_b, nullptr, [](int, int i) { return int32_t(i); }, scratch);
   }
   __syncthreads();
 
@@ -242,7 +246,7 @@ __device__ inline void token_select_mfma_body(
   wg_topk_regs<NT, kSelSPT>(keys, K_t, token_ids + size_t(unit) * K_t, K_t,
                             token_scores ? token_scores + size_t(unit) * K_t : nullptr,
                             [&](int j, int) { return tokpos[j]; }, scratch, &known);
-  if (block_scores && block_ids_out)
+  if (block_scores && !block_ids_in && block_ids_out)
     for (int i = tid; i < K_b; i += NT) block_ids_out[size_t(unit) * K_b + i] = s_bl[i];
 }
 

@@ -216,3 +216,12 @@ def test_decode_modes_are_validated_before_launch(tls):
     assert call(tls.MODE_DENSE, bids_out=dummy) == 1
     assert call(tls.MODE_BLOCK_SPARSE, tids_in=dummy) == 1
     assert call(tls.MODE_BLOCK_SPARSE, tids_out=dummy) == 1
+    # the lagged operator: both block lists, distinct, no given tokens
+    other = ctypes.c_void_p(0x100000)
+    assert call(5) == 1
+    assert call(tls.MODE_LAGGED) == 1
+    assert call(tls.MODE_LAGGED, bids_in=dummy) == 1
+    assert call(tls.MODE_LAGGED, bids_out=dummy) == 1
+    assert call(tls.MODE_LAGGED, bids_in=dummy, bids_out=dummy) == 1
+    assert call(tls.MODE_LAGGED, bids_in=dummy, bids_out=ctypes.c_void_p(0x1000 + 4)) == 1  # overlapping
+    assert call(tls.MODE_LAGGED, bids_in=dummy, bids_out=other, tids_in=dummy) == 1
