@@ -178,7 +178,7 @@ def _cpu_unit_timed(u):
     return time.perf_counter() - t0, t_index
 
 
-ATTN_SOURCES = ["attention_gqa.hip", "attn_common.hpp", "common.hpp", "kernels.hpp"]
+ATTN_SOURCES = ["attention_gqa.hip", "attn_gqa_mfma.hpp", "attn_common.hpp", "common.hpp", "kernels.hpp"]
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "attention_gqa_b32_ctx96k_traffic.json")
 COPY_BYTES = 1 << 30
 
