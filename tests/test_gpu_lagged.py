@@ -126,6 +126,35 @@ def test_lagged_equals_the_two_calls(name):
     assert torch.equal(c.res["lse"], two["lse"])
 
 
+@pytest.mark.parametrize("name", ["toy_f32", "ragged_bf16", "mla_small"])
+def test_lagged_over_a_pool(name):
+    """The lagged call reading K/V through a block pool holding M_{t-1}
+    (filled by tls_init_residency from the cache) gives, bit for bit, what
+    it gives over the cache itself."""
+    c = get_case(name)
+    cfg = c.cfg
+    units, B, n_slots = cfg.batch * cfg.h_kv, cfg.block, 2 * cfg.k_b
+    dt = H.torch_dtype(cfg)
+    pool_k = torch.full((units, n_slots, B, cfg.d_qk), float("nan"), dtype=dt, device="cuda")
+    pool_v = None if cfg.mla else torch.full((units, n_slots, B, cfg.d_v), float("nan"), dtype=dt, device="cuda")
+    slot_map = torch.empty((units, c.m_max), dtype=torch.int32, device="cuda")
+    slot_owner = torch.empty((units, n_slots), dtype=torch.int32, device="cuda")
+    tls.tls_init_residency(c.layout, c.k, c.v, c.ctx, c.M_prev, cfg.k_b, pool_k, pool_v, n_slots, slot_map,
+                           slot_owner, c.ws)
+    pooled = tls.KV(pool_k, pool_v, slot_map, n_slots)
+    dtp = H.torch_dtype(cfg)
+    out = torch.empty((cfg.batch, cfg.h_q, cfg.d_v), dtype=dtp, device="cuda")
+    lse = torch.empty((cfg.batch, cfg.h_q), dtype=torch.float32, device="cuda")
+    M_t = torch.empty((cfg.batch, cfg.h_kv, cfg.k_b), dtype=torch.int32, device="cuda")
+    tids = torch.empty((cfg.batch, cfg.h_kv, cfg.k_t), dtype=torch.int32, device="cuda")
+    tls.tls_sparse_decode(c.layout, c.q, pooled, c.ctx, c.kmax, c.kmin, c.codes, c.qparams, c.ch, cfg.k_b,
+                          cfg.k_t, c.M_prev, None, out, lse, M_t, tids, c.ws, mode=tls.MODE_LAGGED)
+    torch.cuda.synchronize()
+    assert tls.tls_check_device_error(c.ws) == 0
+    assert torch.equal(M_t, c.res["M_t"]) and torch.equal(tids, c.res["tids"])
+    assert torch.equal(out, c.res["out"]) and torch.equal(lse, c.res["lse"])
+
+
 def test_lagged_argument_rules():
     """The lagged operator needs both block lists, distinct, and no given tokens."""
     c = get_case("ragged_bf16")

@@ -6,8 +6,8 @@ must be identical: selections, attention output and lse.  Each case makes
 two calls in a row on the shared scratch, the second with a smaller input,
 and covers the routes of the operator: the fused bf16 selection with the
 whole-unit attention, the general selection stages (fp32, absorbed MLA)
-with split attention and its merge, the single-level operators, and given
-token ids.  A request beyond the scratch is rejected before any launch, and
+with split attention and its merge, the single-level operators, the lagged
+operator, and given token ids.  A request beyond the scratch is rejected before any launch, and
 device-side error bits reach the caller's word.
 """
 import numpy as np
@@ -49,9 +49,10 @@ def _both(c, mode=tls.MODE_TWO_LEVEL, attn_splits=0, token_ids_in=None, block_id
         lse = torch.full((cfg.batch, cfg.h_q), float("nan"), dtype=torch.float32, device="cuda")
         bids = tids = None
         sel_tokens = token_ids_in is None
-        if mode in (tls.MODE_TWO_LEVEL, tls.MODE_BLOCK_SPARSE) and sel_tokens and block_ids_in is None:
+        if mode == tls.MODE_LAGGED or (mode in (tls.MODE_TWO_LEVEL, tls.MODE_BLOCK_SPARSE) and sel_tokens
+                                       and block_ids_in is None):
             bids = torch.full((cfg.batch, cfg.h_kv, cfg.k_b), -7, dtype=torch.int32, device="cuda")
-        if mode in (tls.MODE_TWO_LEVEL, tls.MODE_TOKEN_SPARSE) and sel_tokens:
+        if mode in (tls.MODE_TWO_LEVEL, tls.MODE_TOKEN_SPARSE, tls.MODE_LAGGED) and sel_tokens:
             tids = torch.full((cfg.batch, cfg.h_kv, cfg.k_t), -7, dtype=torch.int32, device="cuda")
         idx = mode != tls.MODE_DENSE and sel_tokens
         args = (c.layout, c.q, c.kv(), c.ctx, c.kmax if idx else None, c.kmin if idx else None,
@@ -91,6 +92,9 @@ def test_noalloc_equals_workspace_decode(name):
         # split attention (partials and their merge in the scratch)
         a, b = _both(c, attn_splits=4)
         _same(a, b, f"{name} call {i} split")
+        # the lagged operator (Sec. 4.2): tokens from a given previous selection
+        a, b = _both(c, mode=tls.MODE_LAGGED, block_ids_in=ws_run["bids"])
+        _same(a, b, f"{name} call {i} lagged")
 
 
 def test_noalloc_routes_and_modes():
