@@ -574,9 +574,9 @@ tls_status sparse_decode_on(const Problem& P, const void* q, const tls_kv_view* 
     // tokens from the given (previous step's) blocks, this step's block
     // selection to block_ids_out; the two lists must not overlap
     if (!block_ids_in || !block_ids_out || token_ids_in) return TLS_ERR_INVALID_ARGUMENT;
-    const size_t n_ids = size_t(P.units) * size_t(K_b > 0 ? K_b : 0);
-    const int32_t* out_end = block_ids_out + n_ids;
-    if (block_ids_in < out_end && block_ids_out < block_ids_in + n_ids) return TLS_ERR_INVALID_ARGUMENT;
+    const uintptr_t bytes = uintptr_t(P.units) * uintptr_t(K_b > 0 ? K_b : 0) * sizeof(int32_t);
+    const uintptr_t a = reinterpret_cast<uintptr_t>(block_ids_in), b = reinterpret_cast<uintptr_t>(block_ids_out);
+    if (a < b + bytes && b < a + bytes) return TLS_ERR_INVALID_ARGUMENT;
   }
   const bool sel_tokens = token_ids_in == nullptr;
   const bool sel_blocks = lagged || (sel_tokens && block_ids_in == nullptr);

@@ -168,6 +168,16 @@ static void decode_validation(void) {
   m.mode = TLS_MODE_BLOCK_SPARSE;
   EXPECT(decode(&L, &kv, 8, 128, NULL, D, NULL, NULL, huge, &m) == TLS_ERR_INVALID_ARGUMENT);
   EXPECT(decode(&L, &kv, 8, 128, NULL, NULL, NULL, D, huge, &m) == TLS_ERR_INVALID_ARGUMENT);
+  /* the lagged operator: both block lists, not overlapping, no given tokens */
+  m.mode = TLS_MODE_LAGGED;
+  EXPECT(decode(&L, &kv, 8, 128, NULL, NULL, NULL, NULL, huge, &m) == TLS_ERR_INVALID_ARGUMENT);
+  EXPECT(decode(&L, &kv, 8, 128, D, NULL, NULL, NULL, huge, &m) == TLS_ERR_INVALID_ARGUMENT);
+  EXPECT(decode(&L, &kv, 8, 128, NULL, NULL, D, NULL, huge, &m) == TLS_ERR_INVALID_ARGUMENT);
+  EXPECT(decode(&L, &kv, 8, 128, D, NULL, D, NULL, huge, &m) == TLS_ERR_INVALID_ARGUMENT);
+  EXPECT(decode(&L, &kv, 8, 128, D, NULL, (char*)D + 4, NULL, huge, &m) == TLS_ERR_INVALID_ARGUMENT);
+  EXPECT(decode(&L, &kv, 8, 128, D, D, (char*)D + (1 << 20), NULL, huge, &m) == TLS_ERR_INVALID_ARGUMENT);
+  m.mode = 5;
+  EXPECT(decode(&L, &kv, 8, 128, NULL, NULL, NULL, NULL, huge, &m) == TLS_ERR_INVALID_ARGUMENT);
   /* pooled view: slot map without slots */
   tls_kv_view pool = {D, D, (const int32_t*)D, 0};
   EXPECT(decode(&L, &pool, 8, 128, NULL, NULL, NULL, NULL, huge, &o) == TLS_ERR_INVALID_ARGUMENT);
