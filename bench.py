@@ -143,7 +143,7 @@ def cpu_baseline(units, cores):
                                                 initializer=_cpu_worker_init) as ex:
         res = list(ex.map(_cpu_unit_timed, units, chunksize=max(1, len(units) // (4 * cores))))
     wall = time.perf_counter() - t0
-    return [r[0] for r in res], [r[1] for r in res], wall
+    return [r[0] for r in res], [r[1] for r in res], wall, [r[2] for r in res]
 
 
 def _cpu_worker_init():
@@ -174,8 +174,65 @@ def _cpu_unit_timed(u):
     index = O.token_index(Ku, n, ch)
     t_index = time.perf_counter() - t0
     t0 = time.perf_counter()
-    O.decode_unit(qg, Ku, Vu, n, ch, cfg.k_b, cfg.k_t, cfg.block, cfg.sigma, index=index, summaries=summ)
-    return time.perf_counter() - t0, t_index
+    res = O.decode_unit(qg, Ku, Vu, n, ch, cfg.k_b, cfg.k_t, cfg.block, cfg.sigma, index=index, summaries=summ)
+    t_dec = time.perf_counter() - t0
+    gpu = _CPU.get("gpu")
+    return t_dec, t_index, (_unit_parity(O, u, cfg, qg, Ku, Vu, n, ch, index, res, gpu) if gpu else None)
+
+
+def _unit_parity(O, u, cfg, qg, Ku, Vu, n, ch, index, res, gpu):
+    """The GPU step's result for unit u against the oracle's, by the
+    selection rule of the parity tests: equal id sets except ids whose oracle
+    score lies within 1e-3 relative of the oracle's k-th score; a block swap
+    is followed by the oracle's token stage on the GPU's blocks, any swap by
+    the oracle's attention on the GPU's tokens; the output within the dtype's
+    tolerance.  (After the timed decode; not part of the baseline.)"""
+    import numpy as np
+    s, g = divmod(u, cfg.h_kv)
+    rel = 1e-3
+    tol = 2e-2 if cfg.dtype == "bf16" else 1e-5
+
+    def ids(row):
+        k = int((row >= 0).sum())
+        ok = bool(np.all(row[:k] >= 0) and np.all(row[k:] == -1) and np.all(np.diff(row[:k]) > 0))
+        return row[:k], ok
+
+    def swaps(got, want, score):
+        gs, ws = set(int(x) for x in got), set(int(x) for x in want)
+        diff = gs ^ ws
+        if len(gs) != len(ws):
+            return len(diff), False
+        if not diff:
+            return 0, True
+        kth = min(score(i) for i in ws)
+        return len(diff) // 2, all(abs(score(i) - kth) <= rel * abs(kth) for i in diff)
+
+    M, ok_m = ids(gpu["bids"][s, g])
+    S, ok_s = ids(gpu["tids"][s, g])
+    sb, ok_b = swaps(M, res["block_ids"], lambda i: float(res["block_scores"][i]))
+    tok = res
+    if sb:
+        S_ref, alpha, cand = O.select_tokens(qg, ch, index[0], index[1], M, n, cfg.block, cfg.k_t, cfg.sigma)
+        tok = dict(token_ids=S_ref, alpha=alpha, cand=cand)
+    pos = {int(t): i for i, t in enumerate(tok["cand"])}
+    if not all(int(t) in pos for t in S):
+        st, ok_t = len(S), False
+    else:
+        st, ok_t = swaps(S, tok["token_ids"], lambda t: float(tok["alpha"][pos[int(t)]]))
+    o_ref, lse_ref = (O.sparse_attention(qg, Ku, Vu, S, cfg.sigma) if (sb or st) else (res["out"], res["lse"]))
+    G = cfg.group
+    o = gpu["out"][s, g * G:(g + 1) * G].astype(np.float64)
+    lse = gpu["lse"][s, g * G:(g + 1) * G].astype(np.float64)
+    err_o = float(np.max(np.abs(o - o_ref))) if o.size else 0.0
+    fin = np.isfinite(lse_ref)
+    err_l = float(np.max(np.abs(lse[fin] - lse_ref[fin]))) if fin.any() else 0.0
+    within = bool(np.all(np.abs(o - o_ref) <= tol + tol * np.abs(o_ref)) and
+                  np.all(np.abs(lse[fin] - lse_ref[fin]) <= tol + tol * np.abs(lse_ref[fin])) and
+                  np.array_equal(np.isfinite(lse), fin))
+    want = set(int(x) for x in res["token_ids"])
+    recall = len(want & set(int(x) for x in S)) / len(want) if want else 1.0
+    return dict(block_swaps=sb, token_swaps=st, ok=bool(ok_m and ok_s and ok_b and ok_t and within),
+                err_out=err_o, err_lse=err_l, recall=recall)
 
 
 ATTN_SOURCES = ["attention_gqa.hip", "attn_gqa_mfma.hpp", "attn_common.hpp", "common.hpp", "kernels.hpp"]
@@ -251,24 +308,44 @@ def traffic_from_profiles(kernel_src_hash):
     return d.get("traffic_bytes_per_launch")
 
 
-def cpu_baseline_record(cfg, d, np, torch):
+def cpu_baseline_record(cfg, d, np, torch, gpu=None):
     """The oracle's decode step (block scores, top-K_b, token scores over the
     candidates, top-K_t, attention; float64 NumPy, prebuilt indices) over
     every (sequence, KV head) unit of the workload's step, on the host
     cores: the value is the summed per-unit decode time divided by the
-    worker count (the step's time with the units spread evenly)."""
+    worker count (the step's time with the units spread evenly).  With
+    `gpu` (host copies of one GPU step's out, lse, block and token ids on
+    the same inputs), each worker also compares its unit with the GPU's
+    after timing it; returns (baseline record, parity record or None)."""
     def host(t):
         if t is None:
             return None
         return t.view(torch.int16).cpu().numpy().view(np.uint16) if cfg.dtype == "bf16" else t.cpu().numpy()
     _CPU.update(cfg=cfg, q=d["q_host"], k=host(d["k"]), v=host(d["v"]), ctx=d["ctx_host"],
-                channels=d["channels_host"])
+                channels=d["channels_host"], gpu=gpu)
     units = list(range(cfg.batch * cfg.h_kv))
     cores = max(1, min(16, len(os.sched_getaffinity(0)), len(units)))
-    dec, idx, wall = cpu_baseline(units, cores)
+    dec, idx, wall, par = cpu_baseline(units, cores)
     # one unit on one core in this process, nothing else running
+    _CPU["gpu"] = None
     one = min(_cpu_unit_timed(units[0])[0] for _ in range(3))
     _CPU.clear()
+    parity = None
+    if gpu is not None:
+        parity = {
+            "units": len(par),
+            "all_within_rule": all(p["ok"] for p in par),
+            "units_with_block_swap": sum(p["block_swaps"] > 0 for p in par),
+            "units_with_token_swap": sum(p["token_swaps"] > 0 for p in par),
+            "max_abs_err_out": float(f"{max(p['err_out'] for p in par):.3g}"),
+            "max_abs_err_lse": float(f"{max(p['err_lse'] for p in par):.3g}"),
+            "token_recall_min": round(min(p["recall"] for p in par), 5),
+            "token_recall_mean": round(float(np.mean([p["recall"] for p in par])), 5),
+            "rule": "every unit of one GPU step against the oracle on the same inputs: block and token id sets "
+                    "equal except near ties (oracle score within 1e-3 relative of its k-th), a swap followed "
+                    "by the oracle's later stages on the GPU's selection; out and lse within "
+                    + ("2e-2" if cfg.dtype == "bf16" else "1e-5") + " abs+rel; recall = |S_gpu & S_oracle| / |S_oracle|",
+        }
     value_s = sum(dec) / cores
     ratio = value_s / (one * len(units) / cores)
     if not 0.5 <= ratio <= 2.0:
@@ -292,7 +369,7 @@ def cpu_baseline_record(cfg, d, np, torch):
         "value_vs_single_core_estimate": round(ratio, 3),
         "index_build_s_per_unit": round(float(np.mean(idx)), 4),
         "pool_wall_s": round(wall, 2),
-    }
+    }, parity
 
 
 def prefill_timing(tls, torch, cfg, layout, d, L, e, reps=3):
@@ -903,7 +980,13 @@ def main():
 
     # ---- CPU baseline: the oracle's decode step over every unit of the step -------
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline_record(cfg, d, np, torch)
+        # one more step on the resident layer: its outputs are checked against
+        # the oracle unit by unit inside the baseline leg
+        step(0)
+        torch.cuda.synchronize()
+        gpu = dict(out=out.float().cpu().numpy(), lse=lse.cpu().numpy(), bids=bids.cpu().numpy(),
+                   tids=tids.cpu().numpy())
+        result["cpu_baseline"], result["parity"] = cpu_baseline_record(cfg, d, np, torch, gpu)
     # ---- the other legs of the 60 % gate: the batched 48k-96k step and the
     # offloaded 96k workload's decode over the HBM pool (with and without the
     # PCIe transfer running), reported beside the headline -----------------------
