@@ -230,6 +230,51 @@ def pin_channel_projection_property(seed=19):
     np.testing.assert_array_equal(ids3, cand3[:k_t])
 
 
+def pin_token_index_projection(seed=21):
+    """The token index reads the key only at the channels of C (Sec. 4.1,
+    k~ = Quantize(k[C])): it equals the index of the projected key matrix
+    K[:, C] built on its own channels 0..d_c-1, and noise on the channels
+    outside C changes no code and no (scale, min).  C is a random,
+    non-contiguous subset."""
+    r = np.random.default_rng(seed)
+    d, n = 80, 45
+    K = r.standard_normal((n, d)).astype(np.float32).astype(np.float64)
+    C = np.sort(r.choice(np.arange(1, d), size=32, replace=False))
+    assert not np.array_equal(C, np.arange(32))
+    codes, qp = O.token_index(K, n, C)
+    codes_p, qp_p = O.token_index(np.ascontiguousarray(K[:, C]), n, np.arange(32))
+    np.testing.assert_array_equal(codes, codes_p)
+    np.testing.assert_array_equal(qp, qp_p)
+    off = np.setdiff1d(np.arange(d), C)
+    K2 = K.copy()
+    K2[:, off] = (K2[:, off] + 7.0 * r.standard_normal((n, len(off)))).astype(np.float32)
+    codes2, qp2 = O.token_index(K2, n, C)
+    np.testing.assert_array_equal(codes2, codes)
+    np.testing.assert_array_equal(qp2, qp)
+
+
+def pin_block_summaries_tail(seed=20):
+    """The block summaries cover only the n valid tokens (R1): rows at or past
+    n — here huge values of both signs, and NaN — change nothing, the tail
+    block is summarised over its valid rows alone, and every summary is
+    finite; each summary is the brute-force max / min of its block's rows."""
+    r = np.random.default_rng(seed)
+    B, d, n = 16, 8, 53  # 4 blocks, the last with 5 valid rows
+    K = r.standard_normal((n, d))
+    pad = np.full((3 * B, d), 1e30)
+    pad[1::2] = -1e30
+    pad[5] = np.nan
+    kmax, kmin = O.block_summaries(np.vstack([K, pad]), n, B)
+    kmax0, kmin0 = O.block_summaries(K, n, B)
+    assert kmax.shape == (4, d) and np.all(np.isfinite(kmax)) and np.all(np.isfinite(kmin))
+    np.testing.assert_array_equal(kmax, kmax0)
+    np.testing.assert_array_equal(kmin, kmin0)
+    for i in range(4):
+        for c in range(d):
+            vals = [K[j, c] for j in range(i * B, min((i + 1) * B, n))]
+            assert kmax[i, c] == max(vals) and kmin[i, c] == min(vals)
+
+
 # --- attention -------------------------------------------------------------------
 
 def pin_attention_library(seed=16):
@@ -510,7 +555,8 @@ def pin_calibration_properties(seed=17):
 ALL_PINS = [
     pin_quest_golden, pin_quest_forms_agree, pin_quest_upper_bound, pin_topk_bruteforce,
     pin_candidates, pin_quant_golden, pin_quant_bound, pin_alpha_golden, pin_alpha_distribution,
-    pin_channel_projection_golden, pin_channel_projection_property, pin_attention_library, pin_attention_closed_form, pin_dense_equivalence,
+    pin_channel_projection_golden, pin_channel_projection_property, pin_token_index_projection,
+    pin_block_summaries_tail, pin_attention_library, pin_attention_closed_form, pin_dense_equivalence,
     pin_invariants_and_planted, pin_single_level_operators, pin_lagged_schedule, pin_lagged_schedule_growth,
     pin_calibration_golden,
     pin_calibration_properties,

@@ -73,6 +73,7 @@ def _wrong_candidates(block_ids, n, B):      # ignores the ragged tail
 
 
 _REAL_ATTN = O.sparse_attention
+_REAL_INDEX = O.token_index
 
 
 def _logits_prefix_channels(q, channels, xhat, sigma):   # q~ = q[:, :d_c] instead of q[:, C]
@@ -81,6 +82,16 @@ def _logits_prefix_channels(q, channels, xhat, sigma):   # q~ = q[:, :d_c] inste
 
 def _logits_no_sigma(q, channels, xhat, sigma):          # forgets the scale in the approximate score
     return q[:, np.asarray(channels)] @ xhat.T
+
+def _summaries_past_n(K, n, B):              # reads whole blocks, past the valid tokens
+    m = -(-n // B)
+    return (np.array([K[i * B:(i + 1) * B].max(axis=0) for i in range(m)]),
+            np.array([K[i * B:(i + 1) * B].min(axis=0) for i in range(m)]))
+
+
+def _index_prefix_channels(K, n, channels):   # k~ = Quantize(k[:d_c]) instead of k[C]
+    return _REAL_INDEX(K, n, np.arange(len(channels)))
+
 
 def _absmax_signed(x):                       # max of x instead of max of |x|
     x = np.asarray(x, dtype=np.float64)
@@ -98,6 +109,8 @@ def _importance_max_heads(qa, ka):           # max over the heads instead of the
 MUTATIONS = [
     ("quest_scores", _swap_max_min),
     ("block_summaries", _floor_blocks),
+    ("block_summaries", _summaries_past_n),
+    ("token_index", _index_prefix_channels),
     ("approx_scores", _single_softmax),
     ("approx_scores", _no_mean),
     ("token_logits", _logits_prefix_channels),
