@@ -26,9 +26,9 @@ constexpr uint32_t kBf16Base = 0x43434343u;  // high byte of bf16(128 + c), c < 
 __device__ constexpr int kSliceChan[8] = {0, 2, 1, 3, 4, 6, 5, 7};
 
 // LDS words: top-k scratch | block list | q~ table (4 heads x 32 channels of
-// bf16, in slice order) | per-wave partials.
+// bf16, in slice order) | the heads' q~ sums (4) | per-wave partials.
 inline size_t mfma_select_lds_bytes(int K_b) {
-  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(K_b)) + 64 + kSelNW * 12) * sizeof(uint32_t);
+  return (size_t(topk_scratch_words(kSelNT)) + size_t(align4w(K_b)) + 64 + 4 + kSelNW * 12) * sizeof(uint32_t);
 }
 
 // The fused selection of one unit by a 1024-thread work-group, on LDS
@@ -44,7 +44,8 @@ __device__ inline void token_select_mfma_body(
   uint32_t* scratch = smem;
   int32_t* s_bl = reinterpret_cast<int32_t*>(smem + topk_scratch_words(NT));
   uint16_t* s_qt = reinterpret_cast<uint16_t*>(s_bl + align4w(K_b));  // [4][32] (64 words)
-  float* s_red = reinterpret_cast<float*>(s_qt + 128);                    // [NW][12]
+  float* s_qsum = reinterpret_cast<float*>(s_qt + 128);                   // [4]
+  float* s_red = s_qsum + 4;                                              // [NW][12]
   const int S = K_b * B;
 
   const int s = unit / H_kv, g = unit % H_kv;
@@ -94,6 +95,11 @@ __device__ inline void token_select_mfma_body(
       v = q[(size_t(s) * H_q + size_t(g) * G + h) * d + ch];
     }
     s_qt[tid] = v;
+    // the head's q~ sum, over the 32 lanes holding its channels
+    float sum = __uint_as_float(uint32_t(v) << 16);
+#pragma unroll
+    for (int m = 16; m >= 1; m >>= 1) sum += __shfl_xor(sum, m, 32);
+    if (x == 0) s_qsum[h] = sum;
   }
   if (block_scores) {
     int32_t* dst = block_ids_in ? block_ids_out + size_t(unit) * K_b : s_bl;
@@ -101,34 +107,19 @@ __device__ inline void token_select_mfma_body(
   }
   __syncthreads();
 
-  // A operands (row = head lane%4, slice k) and the per-head q~ sums
+  // A operands (row = head lane%4, slice k: four bf16 channels, as they lie
+  // in the table) and the per-head q~ sums
   i16x4_t qa[8];
   float qsum[4];
   {
-    const uint4* row = reinterpret_cast<const uint4*>(s_qt + (lane & 3) * 32);
-    float own = 0.f;
+    const uint2* row = reinterpret_cast<const uint2*>(s_qt + (lane & 3) * 32);
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const uint4 w = row[v];
-      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        i16x4_t a;
-        a[0] = short(ws[2 * k2] & 0xffffu);
-        a[1] = short(ws[2 * k2] >> 16);
-        a[2] = short(ws[2 * k2 + 1] & 0xffffu);
-        a[3] = short(ws[2 * k2 + 1] >> 16);
-        qa[2 * v + k2] = a;
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) own += __uint_as_float(ws[e] << 16) + __uint_as_float(ws[e] & 0xffff0000u);
-    }
-    // broadcast the four heads' sums inside each quad (lane 4b + h holds head h)
-    const int oi = __float_as_int(own);
-    qsum[0] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0x00, 0xF, 0xF, false));
-    qsum[1] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0x55, 0xF, 0xF, false));
-    qsum[2] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0xAA, 0xF, 0xF, false));
-    qsum[3] = __int_as_float(__builtin_amdgcn_update_dpp(oi, oi, 0xFF, 0xF, 0xF, false));
+    for (int k = 0; k < 8; ++k) qa[k] = __builtin_bit_cast(i16x4_t, row[k]);
+    const float4 qs = *reinterpret_cast<const float4*>(s_qsum);
+    qsum[0] = qs.x;
+    qsum[1] = qs.y;
+    qsum[2] = qs.z;
+    qsum[3] = qs.w;
   }
 
   // 1. index rows of the owned slots
@@ -222,7 +213,7 @@ __device__ inline void token_select_mfma_body(
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     const float Z = combine_waves_sum_f32(s_red[(lane & 15) * 12 + 4 + h]);
-    iz[h] = Z > 0.f ? 1.0f / Z : 0.f;
+    iz[h] = Z > 0.f ? __builtin_amdgcn_rcpf(Z) : 0.f;
   }
   // 4. alpha keys in registers, top-K_t
   // Every alpha lies in [0, bound] with bound = (1/G) sum_h 1/Z_h, evaluated in
