@@ -104,14 +104,23 @@ __device__ inline int lanes_below(uint64_t mask) {
 // active.  The result is wave-uniform.
 //   quad_perm [1,0,3,2] / [2,3,0,1]: xor 1 / xor 2 inside a quad
 //   row_half_mirror / row_mirror: the other quad of 8 / the other 8 of 16
+// Each of these moves reads a valid lane of the same row for every lane, so
+// the move's "old" operand is never used; passing 0 there lets the compiler
+// fold the move into the integer or float-add instruction that consumes it
+// (one v_*_dpp instruction per step).
 // ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ inline int dpp_perm(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, true);
+}
+
 template <class Op>
 __device__ inline uint32_t wave_reduce_bits(uint32_t x, Op op) {
   int v = int(x);
-  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false))));
-  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false))));
-  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false))));
-  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false))));
+  v = int(op(uint32_t(v), uint32_t(dpp_perm<0xB1>(v))));
+  v = int(op(uint32_t(v), uint32_t(dpp_perm<0x4E>(v))));
+  v = int(op(uint32_t(v), uint32_t(dpp_perm<0x141>(v))));
+  v = int(op(uint32_t(v), uint32_t(dpp_perm<0x140>(v))));
   const uint32_t r0 = uint32_t(__builtin_amdgcn_readlane(v, 0)), r1 = uint32_t(__builtin_amdgcn_readlane(v, 16));
   const uint32_t r2 = uint32_t(__builtin_amdgcn_readlane(v, 32)), r3 = uint32_t(__builtin_amdgcn_readlane(v, 48));
   return op(op(r0, r1), op(r2, r3));
@@ -123,10 +132,27 @@ __device__ inline uint32_t wave_max_u32(uint32_t x) {
 __device__ inline uint32_t wave_min_u32(uint32_t x) {
   return wave_reduce_bits(x, [](uint32_t a, uint32_t b) { return a < b ? a : b; });
 }
+// Order-preserving map of a float to a signed int (an involution on the
+// bits: non-negative floats keep their bits, negative ones flip the
+// magnitude bits), so float maxima reduce as integer maxima, which fold into
+// DPP instructions.  A NaN enters as -inf, so that, as with fmaxf, it is
+// ignored unless every value is NaN or -inf (the result is then -inf).
+__device__ inline int f32_ord(float f) {
+  const int b = f == f ? __float_as_int(f) : int(0xff800000u);
+  return b ^ ((b >> 31) & 0x7fffffff);
+}
+__device__ inline float ord_f32(int o) { return __int_as_float(o ^ ((o >> 31) & 0x7fffffff)); }
+
+// Wave maximum as an order-preserving int (f32_ord form), for callers that
+// keep combining it as an integer.
+__device__ inline int wave_max_ord(float x) {
+  return int(wave_reduce_bits(uint32_t(f32_ord(x)), [](uint32_t a, uint32_t b) { return uint32_t(max(int(a), int(b))); }));
+}
+
 __device__ inline float wave_max_f32(float x) {
-  return __uint_as_float(wave_reduce_bits(__float_as_uint(x), [](uint32_t a, uint32_t b) {
-    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
-  }));
+  return ord_f32(int(wave_reduce_bits(uint32_t(f32_ord(x)), [](uint32_t a, uint32_t b) {
+    return uint32_t(max(int(a), int(b)));
+  })));
 }
 __device__ inline float wave_sum_f32(float x) {
   return __uint_as_float(wave_reduce_bits(__float_as_uint(x), [](uint32_t a, uint32_t b) {
@@ -142,10 +168,10 @@ __device__ inline float wave_sum_f32(float x) {
 template <class Op>
 __device__ inline uint32_t row16_reduce_bits(uint32_t x, Op op) {
   int v = int(x);
-  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false))));
-  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false))));
-  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false))));
-  v = int(op(uint32_t(v), uint32_t(__builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false))));
+  v = int(op(uint32_t(v), uint32_t(dpp_perm<0xB1>(v))));
+  v = int(op(uint32_t(v), uint32_t(dpp_perm<0x4E>(v))));
+  v = int(op(uint32_t(v), uint32_t(dpp_perm<0x141>(v))));
+  v = int(op(uint32_t(v), uint32_t(dpp_perm<0x140>(v))));
   return uint32_t(v);
 }
 
@@ -157,14 +183,17 @@ __device__ inline uint32_t combine_waves_bits(uint32_t mine, Op op) {
   return uint32_t(__builtin_amdgcn_readfirstlane(int(row16_reduce_bits(mine, op))));
 }
 __device__ inline float combine_waves_max_f32(float mine) {
-  return __uint_as_float(combine_waves_bits(__float_as_uint(mine), [](uint32_t a, uint32_t b) {
-    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
-  }));
+  return ord_f32(int(combine_waves_bits(uint32_t(f32_ord(mine)), [](uint32_t a, uint32_t b) {
+    return uint32_t(max(int(a), int(b)));
+  })));
 }
 __device__ inline float combine_waves_sum_f32(float mine) {
   return __uint_as_float(combine_waves_bits(__float_as_uint(mine), [](uint32_t a, uint32_t b) {
     return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
   }));
+}
+__device__ inline int combine_waves_max_i32(int mine) {
+  return int(combine_waves_bits(uint32_t(mine), [](uint32_t a, uint32_t b) { return uint32_t(max(int(a), int(b))); }));
 }
 __device__ inline uint32_t combine_waves_sum_u32(uint32_t mine) {
   return combine_waves_bits(mine, [](uint32_t a, uint32_t b) { return a + b; });

@@ -30,7 +30,7 @@
 
 namespace tls {
 
-template <int G>
+template <int G, bool WB>
 __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
     const uint16_t* __restrict__ q, const uint8_t* __restrict__ codes, const float* __restrict__ qparams,
     const int32_t* __restrict__ channels, const float* __restrict__ block_scores,
@@ -38,7 +38,7 @@ __global__ __launch_bounds__(kSelNT) void token_select_mfma_kernel(
     const int32_t* __restrict__ ctx_lens, int H_q, int H_kv, int d, int B, int T, int m_max, int K_b, int K_t,
     float sigma, int32_t* __restrict__ token_ids, float* __restrict__ token_scores, uint32_t* err) {
   extern __shared__ uint32_t smem[];
-  token_select_mfma_body<G>(smem, q, codes, qparams, channels, block_scores, block_ids_in, block_ids_out, ctx_lens,
+  token_select_mfma_body<G, WB>(smem, q, codes, qparams, channels, block_scores, block_ids_in, block_ids_out, ctx_lens,
                             H_q, H_kv, d, B, T, m_max, K_b, K_t, sigma, token_ids, token_scores, err, blockIdx.x);
 }
 
@@ -48,19 +48,31 @@ bool fused_token_select_ok(const Problem& P, int K_b, int K_t) {
          P.m_max <= kSelMaxBlocks && mfma_select_lds_bytes(K_b) <= kSelMaxLds;
 }
 
-template <int G>
-static hipError_t launch_g(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,
+template <int G, bool WB>
+static hipError_t launch_gw(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,
                            const int32_t* channels, const float* block_scores, const int32_t* block_ids_in,
                            int32_t* block_ids_out, const int32_t* ctx_lens, int K_b, int K_t, int32_t* token_ids,
                            float* token_scores, uint32_t* err, hipStream_t st) {
   const size_t lds = mfma_select_lds_bytes(K_b);
-  auto kern = token_select_mfma_kernel<G>;
+  auto kern = token_select_mfma_kernel<G, WB>;
   const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), lds);
   if (e != hipSuccess) return e;
   kern<<<P.units, kSelNT, lds, st>>>((const uint16_t*)q, codes, qparams, channels, block_scores, block_ids_in,
                                      block_ids_out, ctx_lens, P.H_q, P.H_kv, P.d_qk, P.B, P.T, P.m_max, K_b, K_t,
                                      P.sigma, token_ids, token_scores, err);
   return hipGetLastError();
+}
+
+template <int G>
+static hipError_t launch_g(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,
+                           const int32_t* channels, const float* block_scores, const int32_t* block_ids_in,
+                           int32_t* block_ids_out, const int32_t* ctx_lens, int K_b, int K_t, int32_t* token_ids,
+                           float* token_scores, uint32_t* err, hipStream_t st) {
+  if (P.B >= 64)
+    return launch_gw<G, true>(P, q, codes, qparams, channels, block_scores, block_ids_in, block_ids_out, ctx_lens,
+                              K_b, K_t, token_ids, token_scores, err, st);
+  return launch_gw<G, false>(P, q, codes, qparams, channels, block_scores, block_ids_in, block_ids_out, ctx_lens,
+                             K_b, K_t, token_ids, token_scores, err, st);
 }
 
 hipError_t launch_token_select_fused(const Problem& P, const void* q, const uint8_t* codes, const float* qparams,

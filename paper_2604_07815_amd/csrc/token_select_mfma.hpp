@@ -32,8 +32,8 @@ inline size_t mfma_select_lds_bytes(int K_b) {
 }
 
 // The fused selection of one unit by a 1024-thread work-group, on LDS
-// `smem` (mfma_select_lds_bytes).
-template <int G>
+// `smem` (mfma_select_lds_bytes).  WB: B >= 64 (whole blocks per wave).
+template <int G, bool WB>
 __device__ inline void token_select_mfma_body(
     uint32_t* smem, const uint16_t* __restrict__ q, const uint8_t* __restrict__ codes,
     const float* __restrict__ qparams, const int32_t* __restrict__ channels, const float* __restrict__ block_scores,
@@ -127,28 +127,59 @@ __device__ inline void token_select_mfma_body(
   float2 qp[kSelSPT];
   int32_t tokpos[kSelSPT];  // token position of each owned slot (for the output)
   uint32_t vmask = 0;
+  if constexpr (WB) {
+    // B >= 64: the 64 slots a wave owns for one i lie in one block, so the
+    // block id and the row base are wave-uniform (scalar).  Every lane loads
+    // unconditionally from a row inside the unit's index (row 0 for an empty
+    // list entry, at most T - 1 past the context); vmask drops those slots.
+    const int wv = __builtin_amdgcn_readfirstlane(wid);
+    // (32-bit byte offsets from the unit's base: T is far below 2^28 rows)
+    const uint8_t* ucodes = codes + size_t(unit) * T * 16;
+    const uint8_t* uqp = reinterpret_cast<const uint8_t*>(qparams + size_t(unit) * T * 2);
 #pragma unroll
-  for (int i = 0; i < kSelSPT; ++i) {
-    const int slot = tid + i * NT;
-    const int e = slot >> lgB, o = slot & (B - 1);
-    cw[i] = make_uint4(0, 0, 0, 0);
-    qp[i] = make_float2(0.f, 0.f);
-    tokpos[i] = -1;
-    if (slot < S) {
-      const int blk = s_bl[e];
-      const int tok = blk * B + o;
+    for (int i = 0; i < kSelSPT; ++i) {
+      const int s0 = wv * 64 + i * NT;  // the wave's first slot (uniform)
+      const int e = s0 >> lgB;
+      const int bl = __builtin_amdgcn_readfirstlane(s_bl[min(e, K_b - 1)]);
+      const int blk = s0 < S ? bl : -1;
+      const int tok = blk * B + (s0 & (B - 1)) + lane;
       tokpos[i] = tok;
-      if (blk >= 0 && tok < n) {
-        const size_t r = size_t(unit) * T + tok;
-        cw[i] = ld16_stream(codes + r * 16);
-        const float* pr = qparams + r * 2;
-        qp[i] = make_float2(__builtin_nontemporal_load(pr), __builtin_nontemporal_load(pr + 1));
-        vmask |= 1u << i;
+      const bool ok = blk >= 0 && tok < n;
+      const uint32_t rr = blk < 0 ? 0u : uint32_t(min(tok, T - 1));
+      cw[i] = ld16_stream(ucodes + (rr << 4));
+      const float* pr = reinterpret_cast<const float*>(uqp + (rr << 3));
+      qp[i] = make_float2(__builtin_nontemporal_load(pr), __builtin_nontemporal_load(pr + 1));
+      vmask |= ok ? 1u << i : 0u;
+    }
+    // every row request leaves before the first use waits on them
+    __builtin_amdgcn_sched_barrier(0);
+  } else {
+#pragma unroll
+    for (int i = 0; i < kSelSPT; ++i) {
+      const int slot = tid + i * NT;
+      const int e = slot >> lgB, o = slot & (B - 1);
+      cw[i] = make_uint4(0, 0, 0, 0);
+      qp[i] = make_float2(0.f, 0.f);
+      tokpos[i] = -1;
+      if (slot < S) {
+        const int blk = s_bl[e];
+        const int tok = blk * B + o;
+        tokpos[i] = tok;
+        if (blk >= 0 && tok < n) {
+          const size_t r = size_t(unit) * T + tok;
+          cw[i] = ld16_stream(codes + r * 16);
+          const float* pr = qparams + r * 2;
+          qp[i] = make_float2(__builtin_nontemporal_load(pr), __builtin_nontemporal_load(pr + 1));
+          vmask |= 1u << i;
+        }
       }
     }
   }
 
   // 2. dots on the matrix cores, logits, per-head max
+  float qs2[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) qs2[h] = sigma2 * qsum[h];
   float lg[kSelSPT][G];
   float mx[G];
 #pragma unroll
@@ -168,25 +199,26 @@ __device__ inline void token_select_mfma_body(
       acc = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(qa[2 * w + 1], __builtin_bit_cast(i16x4_t, b1), acc, 0, 0, 0);
     }
     const bool valid = (vmask >> i) & 1u;
-    const float sc = qp[i].x, off = qp[i].y - 128.0f * qp[i].x;
+    // sigma (base 2) folded into the slot's scale and the heads' q~ sums
+    const float sc = sigma2 * qp[i].x, off = qp[i].y - 128.0f * qp[i].x;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      lg[i][h] = valid ? sigma2 * fmaf(sc, acc[h], off * qsum[h]) : -INFINITY;
+      lg[i][h] = valid ? fmaf(sc, acc[h], off * qs2[h]) : -INFINITY;
       mx[h] = fmaxf(mx[h], lg[i][h]);
     }
   }
   const uint32_t wcnt = wave_reduce_bits(uint32_t(__popc(vmask)), [](uint32_t a, uint32_t b) { return a + b; });
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    const float w = wave_max_f32(mx[h]);
-    if (lane == 0) s_red[wid * 12 + h] = w;
+    const int w = wave_max_ord(mx[h]);  // order-preserving int form
+    if (lane == 0) s_red[wid * 12 + h] = __int_as_float(w);
   }
   if (lane == 0) s_red[wid * 12 + 8] = __uint_as_float(wcnt);
   __syncthreads();
   static_assert(NW == 16, "one wave value per lane of a 16-lane row");
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    mx[h] = combine_waves_max_f32(s_red[(lane & 15) * 12 + h]);
+    mx[h] = ord_f32(combine_waves_max_i32(__float_as_int(s_red[(lane & 15) * 12 + h])));
     if (mx[h] == -INFINITY) mx[h] = 0.f;  // no candidate: every logit is -inf, every exponential 0
   }
   const uint32_t n_valid = combine_waves_sum_u32(__float_as_uint(s_red[(lane & 15) * 12 + 8]));
@@ -219,7 +251,8 @@ __device__ inline void token_select_mfma_body(
   // Every alpha lies in [0, bound] with bound = (1/G) sum_h 1/Z_h, evaluated in
   // the same operation order (each exponential is <= 1 and rounding is
   // monotone), so the top-k needs no statistics pass of its own.  A NaN alpha
-  // (NaN inputs only) ranks as 0.
+  // (NaN inputs only; arithmetic NaNs are quiet) ranks as 0: fmaxf(alpha, 0)
+  // is then 0, and for alpha >= +0 the key bits | 2^31 equal float_key.
   const float invG = 1.0f / float(G);
   float bsum = 0.f;
 #pragma unroll
@@ -230,8 +263,8 @@ __device__ inline void token_select_mfma_body(
     float a = 0.f;
 #pragma unroll
     for (int h = 0; h < G; ++h) a = fmaf(lg[i][h], iz[h], a);
-    const float av = a * invG;
-    keys[i] = ((vmask >> i) & 1u) ? (av == av ? float_key(av) : float_key(0.f)) : kInvalidKey;
+    const float av = fmaxf(a * invG, 0.f);
+    keys[i] = ((vmask >> i) & 1u) ? (__float_as_uint(av) | 0x80000000u) : kInvalidKey;
   }
   const TopkKnown known{n_valid, float_key(bsum * invG), float_key(0.f)};
   wg_topk_regs<NT, kSelSPT>(keys, K_t, token_ids + size_t(unit) * K_t, K_t,
