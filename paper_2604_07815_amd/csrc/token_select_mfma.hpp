@@ -23,7 +23,9 @@ constexpr uint32_t kBf16Base = 0x43434343u;  // high byte of bf16(128 + c), c < 
 // Element order of one 4-channel k-slice: within the 8 channels of code dword
 // w, slice 2w holds channels (0, 2, 1, 3) and slice 2w+1 channels (4, 6, 5, 7)
 // (offsets from 8w): the low nibbles of two bytes, then their high nibbles.
-__device__ constexpr int kSliceChan[8] = {0, 2, 1, 3, 4, 6, 5, 7};
+// slice_chan(j) = {0, 2, 1, 3, 4, 6, 5, 7}[j], computed (a table would be one
+// more dependent memory request in the prologue).
+__device__ inline int slice_chan(int j) { return (j & 4) | ((j & 1) << 1) | ((j >> 1) & 1); }
 
 // LDS words: top-k scratch | block list | q~ table (4 heads x 32 channels of
 // bf16, in slice order) | the heads' q~ sums (4) | per-wave partials.
@@ -59,14 +61,28 @@ __device__ inline void token_select_mfma_body(
   const int lgB = __builtin_ctz(unsigned(B));  // B is a power of two here
   const float sigma2 = sigma * 1.4426950408889634f;  // logits in base 2
 
-  // block scores as keys (requested first: the longest dependency)
-  uint32_t bk[kSelBPT];
+  // block scores (requested first: the longest dependency); every lane loads
+  // from a clamped index, so that both requests leave before either is used
+  float bsv[kSelBPT];
   if (block_scores) {
     const float* sc = block_scores + size_t(unit) * m_max;
 #pragma unroll
-    for (int j = 0; j < kSelBPT; ++j) {
-      const int i = tid + j * NT;
-      bk[j] = i < m ? float_key(sc[i]) : kInvalidKey;
+    for (int j = 0; j < kSelBPT; ++j) bsv[j] = sc[min(tid + j * NT, m_max - 1)];
+  }
+  // q~ entries in slice order: entry (h, 4k + e) = q[h][C[8(k/2) + slice_chan(4(k%2) + e)]]
+  // (channel id, then the query element: two dependent requests, issued
+  // here and written to LDS only after the block top-k, which hides them)
+  uint16_t qv = 0;
+  if (tid < 4 * 32) {
+    const int h = tid >> 5, x = tid & 31;
+    if (h < G) {
+      const int k = x >> 2, e = x & 3;
+      int ch = channels[g * 32 + 8 * (k >> 1) + slice_chan(4 * (k & 1) + e)];
+      if (ch < 0 || ch >= d) {
+        set_error(err, 32u);
+        ch = 0;
+      }
+      qv = q[(size_t(s) * H_q + size_t(g) * G + h) * d + ch];
     }
   }
   if (block_ids_in) {
@@ -81,29 +97,20 @@ __device__ inline void token_select_mfma_body(
       s_bl[i] = b < 0 ? -1 : b;
     }
   }
-  // q~ table in slice order: entry (h, 4k + e) = q[h][C[8(k/2) + kSliceChan[4(k%2) + e]]]
-  if (tid < 4 * 32) {
-    const int h = tid >> 5, x = tid & 31;
-    uint16_t v = 0;
-    if (h < G) {
-      const int k = x >> 2, e = x & 3;
-      int ch = channels[g * 32 + 8 * (k >> 1) + kSliceChan[4 * (k & 1) + e]];
-      if (ch < 0 || ch >= d) {
-        set_error(err, 32u);
-        ch = 0;
-      }
-      v = q[(size_t(s) * H_q + size_t(g) * G + h) * d + ch];
-    }
-    s_qt[tid] = v;
-    // the head's q~ sum, over the 32 lanes holding its channels
-    float sum = __uint_as_float(uint32_t(v) << 16);
-#pragma unroll
-    for (int m = 16; m >= 1; m >>= 1) sum += __shfl_xor(sum, m, 32);
-    if (x == 0) s_qsum[h] = sum;
-  }
   if (block_scores) {
+    uint32_t bk[kSelBPT];
+#pragma unroll
+    for (int j = 0; j < kSelBPT; ++j) bk[j] = tid + j * NT < m ? float_key(bsv[j]) : kInvalidKey;
     int32_t* dst = block_ids_in ? block_ids_out + size_t(unit) * K_b : s_bl;
     wg_topk_regs<NT, kSelBPT>(bk, K_b, dst, K_b, nullptr, [](int, int i) { return int32_t(i); }, scratch);
+  }
+  if (tid < 4 * 32) {
+    s_qt[tid] = qv;
+    // the head's q~ sum, over the 32 lanes holding its channels
+    float sum = __uint_as_float(uint32_t(qv) << 16);
+#pragma unroll
+    for (int m = 16; m >= 1; m >>= 1) sum += __shfl_xor(sum, m, 32);
+    if ((tid & 31) == 0) s_qsum[tid >> 5] = sum;
   }
   __syncthreads();
 
@@ -133,15 +140,16 @@ __device__ inline void token_select_mfma_body(
     // unconditionally from a row inside the unit's index (row 0 for an empty
     // list entry, at most T - 1 past the context); vmask drops those slots.
     const int wv = __builtin_amdgcn_readfirstlane(wid);
+    // lane j < 8 reads the wave's block-list entry for slot group j (one LDS
+    // round trip for all eight)
+    const int blv = s_bl[min((wv * 64 + (lane & 7) * NT) >> lgB, K_b - 1)];
     // (32-bit byte offsets from the unit's base: T is far below 2^28 rows)
     const uint8_t* ucodes = codes + size_t(unit) * T * 16;
     const uint8_t* uqp = reinterpret_cast<const uint8_t*>(qparams + size_t(unit) * T * 2);
 #pragma unroll
     for (int i = 0; i < kSelSPT; ++i) {
       const int s0 = wv * 64 + i * NT;  // the wave's first slot (uniform)
-      const int e = s0 >> lgB;
-      const int bl = __builtin_amdgcn_readfirstlane(s_bl[min(e, K_b - 1)]);
-      const int blk = s0 < S ? bl : -1;
+      const int blk = s0 < S ? __builtin_amdgcn_readlane(blv, i) : -1;
       const int tok = blk * B + (s0 & (B - 1)) + lane;
       tokpos[i] = tok;
       const bool ok = blk >= 0 && tok < n;
