@@ -275,7 +275,7 @@ __device__ inline void token_select_mfma_body(
     keys[i] = ((vmask >> i) & 1u) ? (__float_as_uint(av) | 0x80000000u) : kInvalidKey;
   }
   const TopkKnown known{n_valid, float_key(bsum * invG), float_key(0.f)};
-  wg_topk_regs<NT, kSelSPT>(keys, K_t, token_ids + size_t(unit) * K_t, K_t,
+  wg_topk_regs<NT, kSelSPT, true>(keys, K_t, token_ids + size_t(unit) * K_t, K_t,
                             token_scores ? token_scores + size_t(unit) * K_t : nullptr,
                             [&](int j, int) { return tokpos[j]; }, scratch, &known);
   if (block_scores && !block_ids_in && block_ids_out)

@@ -17,12 +17,13 @@ constexpr int kTopkMaxNW = 16;   // waves per work-group
 constexpr int kTopkHistCopies = 4;
 constexpr int kTopkHistStride = 257;
 constexpr int kTopkHistWords = kTopkHistCopies * kTopkHistStride;  // per pass
+constexpr int kTopkPasses = 5;  // histograms: a spread first pass plus up to four 8-bit passes
 
-// LDS words of the scratch area: the four passes' histograms (cleared on
+// LDS words of the scratch area: the passes' histograms (cleared on
 // entry), broadcast slots, and the per-(key slot, wave) counts of the ordered
 // compaction.
 __host__ __device__ constexpr int topk_scratch_words(int /*nt*/) {
-  return align4w_c(4 * kTopkHistWords) + 64 + 2 * kTopkMaxEPT * kTopkMaxNW;
+  return align4w_c(kTopkPasses * kTopkHistWords) + 64 + 2 * kTopkMaxEPT * kTopkMaxNW;
 }
 
 // Round a count of 32-bit LDS words up to a multiple of 4 (16 bytes), so the
@@ -107,20 +108,25 @@ __device__ inline void topk_scan_pass(const uint32_t* h, int remaining, uint32_t
 // lane): writes every key > T and, in position order, the keys == T while
 // fewer than r ties have been taken, at out[#earlier keys > T + min(#earlier
 // ties, r)] (map(j, tile position) gives the value written).  gbase / ebase
-// count the keys > T and == T of earlier tiles (uniform) and are advanced by
-// this tile's counts.  One work-group barrier inside; cg / ce (LDS) must not
-// be rewritten before every thread has returned.
+// count the keys > T and == T of earlier tiles (uniform); the return value
+// holds this tile's counts (x: keys > T, y: keys == T, 0 when r == 0).  One
+// work-group barrier inside; cg / ce (LDS) must not be rewritten before every
+// thread has returned.
+// r == 0 (no key equal to T is taken, the usual case, see wg_topk_regs)
+// needs one count per (slot, wave) and one prefix sum.
 template <int NT, int EPT, class Map>
-__device__ void topk_compact_tile(const uint32_t (&kr)[EPT], uint32_t T, int r, int& gbase, int& ebase, int32_t* out,
-                                  float* out_scores, Map map, uint32_t* cg, uint32_t* ce) {
+__device__ __forceinline__ int2 topk_compact_tile(const uint32_t (&kr)[EPT], uint32_t T, int r, int gbase,
+                                                  int ebase, int32_t* out, float* out_scores, Map map,
+                                                  uint32_t* cg, uint32_t* ce) {
   constexpr int NW = NT / 64;
   static_assert(NW % ((EPT * NW + 63) / 64) == 0, "keys per thread must keep NW a multiple of PER");
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const bool ties = r > 0;  // uniform
 #pragma unroll
   for (int j = 0; j < EPT; ++j) {
     const uint32_t key = kr[j];
     const uint64_t bg = __ballot(key != kInvalidKey && key > T);
-    const uint64_t be = __ballot(key != kInvalidKey && key == T);
+    const uint64_t be = ties ? __ballot(key != kInvalidKey && key == T) : 0ull;
     if (lane == 0) {
       cg[j * NW + wid] = uint32_t(__popcll(bg));
       ce[j * NW + wid] = uint32_t(__popcll(be));
@@ -140,12 +146,13 @@ __device__ void topk_compact_tile(const uint32_t (&kr)[EPT], uint32_t T, int r, 
     xe[q] = se;
     if (t < NE) {
       sg += cg[t];
-      se += ce[t];
+      if (ties) se += ce[t];
     }
   }
-  const uint32_t ig = wave_incl_scan_u32(sg), ie = wave_incl_scan_u32(se);
-  const uint32_t lg0 = ig - sg, le0 = ie - se;
-  const int tot_g = __builtin_amdgcn_readlane(int(ig), 63), tot_e = __builtin_amdgcn_readlane(int(ie), 63);
+  const uint32_t ig = wave_incl_scan_u32(sg);
+  const uint32_t ie = ties ? wave_incl_scan_u32(se) : 0u;
+  const int tot_g = __builtin_amdgcn_readlane(int(ig), 63);
+  const int tot_e = ties ? __builtin_amdgcn_readlane(int(ie), 63) : 0;
   // entry (j, wid) sits at t = j*NW + wid: lane t / PER, slot t % PER = wid % PER
   uint32_t pg = xg[0], pe = xe[0];
 #pragma unroll
@@ -155,26 +162,28 @@ __device__ void topk_compact_tile(const uint32_t (&kr)[EPT], uint32_t T, int r, 
       pe = xe[q];
     }
   }
-  pg += lg0;
-  pe += le0;
+  pg += ig - sg;
+  pe += ie - se;
 #pragma unroll
   for (int j = 0; j < EPT; ++j) {
     const int src = (j * NW + wid) / PER;
     const uint32_t key = kr[j];
     const bool g = key != kInvalidKey && key > T;
-    const bool e = key != kInvalidKey && key == T;
+    const bool e = ties && key != kInvalidKey && key == T;
     const uint64_t bg = __ballot(g);
-    const uint64_t be = __ballot(e);
     const int gb = gbase + __builtin_amdgcn_readlane(int(pg), src) + lanes_below(bg);
-    const int eb = ebase + __builtin_amdgcn_readlane(int(pe), src) + lanes_below(be);
+    int eb = 0;
+    if (ties) {
+      const uint64_t be = __ballot(e);
+      eb = ebase + __builtin_amdgcn_readlane(int(pe), src) + lanes_below(be);
+    }
     if (g || (e && eb < r)) {
       const int pos = gb + min(eb, r);
       out[pos] = map(j, tid + j * NT);
       if (out_scores) out_scores[pos] = key_float(key);
     }
   }
-  gbase += tot_g;
-  ebase += tot_e;
+  return make_int2(tot_g, tot_e);
 }
 
 // Counts the caller already knows about its keys: the number of valid keys
@@ -185,13 +194,24 @@ struct TopkKnown {
   uint32_t cnt, hi, lo;
 };
 
+// Spread first pass (wg_topk_regs<..., true>): bucket b of the first pass
+// holds the keys with key >> kTopkSpreadShift == base + b, base =
+// (hi >> kTopkSpreadShift) - 255, bucket 0 also every key below; for the
+// keys of non-negative floats (float_key) that is an eighth of an octave
+// per bucket over the 32 octaves below the upper bound, where the top-k of
+// softmax-like scores spreads over many buckets instead of the few that the
+// leading bits of the key span (fewer colliding histogram updates, and
+// usually one pass fewer).  Bucket 0 is refined by ordinary passes with the
+// keys above its range excluded.
+constexpr int kTopkSpreadShift = 20;
+
 template <int NT>
 __device__ inline void topk_prepare(uint32_t* scratch) {
-  constexpr int kHistAll = align4w_c(4 * kTopkHistWords);
+  constexpr int kHistAll = align4w_c(kTopkPasses * kTopkHistWords);
   for (int i = threadIdx.x; i < kHistAll; i += NT) scratch[i] = 0u;
 }
 
-template <int NT, int EPT, class Map>
+template <int NT, int EPT, bool SPREAD = false, class Map>
 __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int out_cap, float* out_scores,
                              Map map, uint32_t* scratch, const TopkKnown* known = nullptr) {
   constexpr int NW = NT / 64;
@@ -201,7 +221,7 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
   // which needs NW to be a multiple of PER
   static_assert(NW % ((EPT * NW + 63) / 64) == 0, "keys per thread must keep NW a multiple of PER");
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  constexpr int kHistAll = align4w_c(4 * kTopkHistWords);
+  constexpr int kHistAll = align4w_c(kTopkPasses * kTopkHistWords);
   uint32_t* hist = scratch;             // [4 passes][copies][stride]
   uint32_t* misc = scratch + kHistAll;  // [64]: 0..47 wave partials
   uint32_t* cg = misc + 64;             // [EPT][NW] keys > T per (slot, wave)
@@ -245,15 +265,56 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
   uint32_t prefix = 0u, pmask = 0u;
   int remaining = kk;
   int bits_left = 0;
+  // keys equal to the running prefix's bucket: after the last pass, the
+  // number of keys equal to T (all valid keys when they are all equal)
+  uint32_t cnt_T = cnt;
+  uint32_t cap = 0xffffffffu;  // keys above cap are out of play (spread pass, bucket 0)
+  int pass = 0;
   if (kk > 0) {
     const uint32_t diff = kmx ^ kmn;
     bits_left = diff ? 32 - __clz(diff) : 0;
     pmask = bits_left >= 32 ? 0u : ~((1u << bits_left) - 1u);
     prefix = kmx & pmask;
   }
-  // at most four 8-bit passes, each on its own histogram: a wave still
-  // scanning pass p's histogram never sees pass p+1's counts
-  for (int pass = 0; bits_left > 0; ++pass) {
+  if (SPREAD && kk > 0 && int(kmx >> kTopkSpreadShift) - int(kmn >> kTopkSpreadShift) > 255) {
+    constexpr int fs = kTopkSpreadShift;
+    const int base = int(kmx >> fs) - 255;  // above kmn's bucket: bucket 0 is clamped
+    uint32_t* h = hist;
+    uint32_t* hc = h + (lane % kTopkHistCopies) * kTopkHistStride;
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) {
+      const uint32_t key = kr[j];
+      // (clamped to the 256 buckets also if a key exceeded the stated bound)
+      if (key != kInvalidKey) atomicAdd(&hc[min(max(int(key >> fs) - base, 0), 255)], 1u);
+    }
+    __syncthreads();
+    const TopkDigit dg = topk_scan_wave(h, remaining);
+    remaining -= int(dg.above);
+    cnt_T = dg.cnt;
+    pass = 1;
+    uint32_t lowest;  // the smallest key the bucket can hold
+    if (dg.digit > 0) {
+      lowest = uint32_t(base + int(dg.digit)) << fs;
+      prefix = lowest;
+      pmask = ~((1u << fs) - 1u);
+      bits_left = fs;
+    } else {
+      lowest = kmn;
+      cap = (uint32_t(base + 1) << fs) - 1u;
+      bits_left = 32 - __clz(kmn ^ cap);
+      pmask = bits_left >= 32 ? 0u : ~((1u << bits_left) - 1u);
+      prefix = cap & pmask;
+    }
+    if (dg.cnt == uint32_t(remaining)) {
+      // the bucket is taken whole (lowest >= 1: valid keys are >= 1)
+      prefix = lowest - 1u;
+      remaining = 0;
+      bits_left = 0;
+    }
+  }
+  // 8-bit passes, each on its own histogram: a wave still scanning pass p's
+  // histogram never sees pass p+1's counts
+  for (; bits_left > 0; ++pass) {
     const int nb = bits_left < 8 ? bits_left : 8;
     const int shift = bits_left - nb;
     const uint32_t dmask = (1u << nb) - 1u;
@@ -262,7 +323,8 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
 #pragma unroll
     for (int j = 0; j < EPT; ++j) {
       const uint32_t key = kr[j];
-      if (key != kInvalidKey && (key & pmask) == prefix) atomicAdd(&hc[(key >> shift) & dmask], 1u);
+      if (key != kInvalidKey && (key & pmask) == prefix && (!SPREAD || key <= cap))
+        atomicAdd(&hc[(key >> shift) & dmask], 1u);
     }
     __syncthreads();
     const TopkDigit dg = topk_scan_wave(h, remaining);
@@ -270,6 +332,7 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
     remaining -= int(dg.above);
     pmask |= dmask << shift;
     bits_left -= nb;
+    cnt_T = dg.cnt;
     if (dg.cnt == uint32_t(remaining) && bits_left > 0 && prefix != 0u) {
       // the threshold's bucket is taken whole: every key >= prefix is
       // selected, i.e. T = prefix - 1 with no equal keys to take
@@ -278,13 +341,16 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
       bits_left = 0;
     }
   }
-  const uint32_t T = prefix;
-  const int r = remaining;  // keys equal to T still to take, lowest positions first
-
-  if (kk > 0) {
-    int gbase = 0, ebase = 0;
-    topk_compact_tile<NT, EPT>(kr, T, r, gbase, ebase, out, out_scores, map, cg, ce);
+  uint32_t T = prefix;
+  int r = remaining;  // keys equal to T still to take, lowest positions first
+  if (r > 0 && uint32_t(r) == cnt_T) {
+    // every key equal to T is taken: select the keys > T - 1 instead, which
+    // the compaction handles with one count per key (valid keys are >= 1)
+    T -= 1u;
+    r = 0;
   }
+
+  if (kk > 0) topk_compact_tile<NT, EPT>(kr, T, r, 0, 0, out, out_scores, map, cg, ce);
   for (int i = kk + tid; i < out_cap; i += NT) {
     out[i] = -1;
     if (out_scores) out_scores[i] = 0.0f;
@@ -305,7 +371,7 @@ __device__ void wg_topk_global(const uint32_t* __restrict__ keys, int n, int k, 
   constexpr int EPT = kTopkMaxEPT;
   constexpr int TILE = NT * EPT;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  constexpr int kHistAll = align4w_c(4 * kTopkHistWords);
+  constexpr int kHistAll = align4w_c(kTopkPasses * kTopkHistWords);
   uint32_t* hist = scratch;
   uint32_t* misc = scratch + kHistAll;
   uint32_t* cg = misc + 64;
@@ -360,6 +426,7 @@ __device__ void wg_topk_global(const uint32_t* __restrict__ keys, int n, int k, 
     prefix = kmx & pmask;
   }
   int list_n = -1;  // < 0: the keys in play are read from global memory
+  uint32_t cnt_T = cnt;  // as in wg_topk_regs
   for (int pass = 0; bits_left > 0; ++pass) {
     const int nb = bits_left < 8 ? bits_left : 8;
     const int shift = bits_left - nb;
@@ -389,6 +456,7 @@ __device__ void wg_topk_global(const uint32_t* __restrict__ keys, int n, int k, 
     remaining -= int(misc[49]);
     pmask |= dmask << shift;
     bits_left -= nb;
+    cnt_T = misc[52];
     if (misc[51] && bits_left > 0 && prefix != 0u) {
       prefix -= 1u;
       remaining = 0;
@@ -420,15 +488,21 @@ __device__ void wg_topk_global(const uint32_t* __restrict__ keys, int n, int k, 
       list_n = int(misc[50]);
     }
   }
-  const uint32_t T = prefix;
-  const int r = remaining;
+  uint32_t T = prefix;
+  int r = remaining;
+  if (r > 0 && uint32_t(r) == cnt_T) {
+    T -= 1u;
+    r = 0;
+  }
   if (kk > 0) {
     int gbase = 0, ebase = 0;
     for (int t = 0; t < ntiles; ++t) {
       uint32_t kr[EPT];
       load_tile(t, kr);
-      topk_compact_tile<NT, EPT>(kr, T, r, gbase, ebase, out, nullptr,
-                                 [=](int, int p) { return int32_t(t * TILE + p); }, cg, ce);
+      const int2 c = topk_compact_tile<NT, EPT>(kr, T, r, gbase, ebase, out, nullptr,
+                                                [=](int, int p) { return int32_t(t * TILE + p); }, cg, ce);
+      gbase += c.x;
+      ebase += c.y;
       __syncthreads();  // cg / ce are rewritten by the next tile
     }
   }

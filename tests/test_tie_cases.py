@@ -49,3 +49,17 @@ def test_zero_query_closed_form(name):
         _, _, Vu = TC.unit_arrays(cfg, dz, s, g)
         np.testing.assert_allclose(r["out"], np.tile(Vu[toks].mean(axis=0), (cfg.group, 1)), rtol=1e-12,
                                    atol=1e-12)
+
+
+def test_deep_cut_layout():
+    """gqa_bf16_fused_deep puts the K_t-th largest alpha more than 32 octaves
+    below the largest (so below the reach of the token top-k's spread first
+    pass, whose buckets cover the 32 octaves under the upper bound), and the
+    default cases put it within them."""
+    for name, deep in (("gqa_bf16_fused_deep", True), ("gqa_bf16_fused", False)):
+        tc = TC.CASES[name]
+        cfg, d, blocks, pa, pb = TC.token_tie_inputs(tc)
+        for (s, g), r in TC.oracle_token_ties(tc, cfg, d, blocks, pa, pb).items():
+            a = np.sort(np.asarray(r["alpha"], dtype=np.float64))[::-1]
+            octaves = np.log2(a[0] / a[cfg.k_t - 1])
+            assert (octaves > 33.0) if deep else (octaves < 31.0), (name, (s, g), octaves)

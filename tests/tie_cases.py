@@ -27,6 +27,8 @@ class TieCase:
     n_dup: int   # identical blocks straddling it (K_b - n_hi of them selected)
     n_a: int     # tokens clearly above the token cut
     n_b: int     # identical tokens straddling it (K_t - n_a of them selected)
+    logit_a: float = 12.0  # approximate logits of the two planted kinds
+    logit_b: float = 9.0   # (sigma * mean query . key)
 
     def cfg(self):
         return synth.config(self.base).replace(**self.over)
@@ -49,12 +51,17 @@ CASES = {
     # bf16 absorbed MLA (G = 32): matrix-core token scoring + token_topk_kernel
     "mla_bf16": TieCase("mla", dict(batch=2, ctx_lo=3000, ctx_hi=4096, k_b=8, k_t=200, clusters=0, seed=7500),
                         5, 10, 120, 150),
+    # the fused kernel with the cut ~45 octaves below the largest alpha (dominant
+    # logits 31 above the tied group): the cut falls in the token top-k's
+    # bottom first-pass bucket, which holds every key more than 32 octaves
+    # below the upper bound and is refined with the keys above it excluded
+    "gqa_bf16_fused_deep": TieCase("qwen3_gqa_48k", dict(batch=2, h_q=8, h_kv=2, ctx_lo=3000, ctx_hi=4096, k_b=8,
+                                                         k_t=128, clusters=0, seed=7150), 5, 10, 100, 60,
+                                   logit_a=40.0),
     "mla_bf16_70k": TieCase("mla", dict(batch=1, ctx_lo=70000, ctx_hi=70000, k_b=128, k_t=2048, clusters=0,
                                         seed=7600), 100, 60, 1500, 1200),
 }
 
-# approximate logits of the planted rows (sigma * mean query . key)
-LOGIT_A, LOGIT_B = 12.0, 9.0
 SEP_REL = 1e-3  # everything but the tied group lies farther than this from the cut score
 
 
@@ -79,7 +86,7 @@ def token_tie_inputs(tc: TieCase, whole_context: bool = False):
     blocks = None if whole_context else synth.draw_block_lists(cfg, d["ctx_lens"], cfg.k_b)
     sig = cfg.sigma
     pa, pb = synth.plant_tie_tokens(cfg, d["q"], d["k"], d["ctx_lens"], d["channels"], blocks, tc.n_a, tc.n_b,
-                                    LOGIT_A / sig, LOGIT_B / sig)
+                                    tc.logit_a / sig, tc.logit_b / sig)
     return cfg, d, blocks, pa, pb
 
 
