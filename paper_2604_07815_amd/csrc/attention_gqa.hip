@@ -76,8 +76,8 @@ __global__ __launch_bounds__(256) void attn_gqa_kernel(
           if (!slot_map) {
             row = tok;
           } else {
-            const int slot = slot_map[size_t(unit) * m_max + tok / B];
-            if (slot >= 0 && slot < n_slots) row = slot * B + tok % B;
+            const int slot = slot_map[size_t(unit) * m_max + tok_block(tok, B)];
+            if (slot >= 0 && slot < n_slots) row = slot * B + tok_offset(tok, B);
             else if (li == 0) set_error(err, 8u);
           }
         }

@@ -112,8 +112,8 @@ __global__ __launch_bounds__(256) void attn_mla_mfma_kernel(
           if (!slot_map) {
             row = tok;
           } else {
-            const int slot = slot_map[size_t(unit) * m_max + tok / B];
-            if (slot >= 0 && slot < n_slots) row = slot * B + tok % B;
+            const int slot = slot_map[size_t(unit) * m_max + tok_block(tok, B)];
+            if (slot >= 0 && slot < n_slots) row = slot * B + tok_offset(tok, B);
             else set_error(err, 8u);
           }
         }

@@ -12,12 +12,12 @@ template <class S>
 __device__ inline const S* kv_row(const S* base, const int32_t* slot_map, int64_t n_slots, size_t unit, int T,
                                   int B, int m_max, int d, int tok, bool* ok) {
   if (!slot_map) return base + (unit * size_t(T) + size_t(tok)) * d;
-  const int slot = slot_map[unit * size_t(m_max) + tok / B];
+  const int slot = slot_map[unit * size_t(m_max) + tok_block(tok, B)];
   if (slot < 0 || slot >= n_slots) {
     *ok = false;
     return base;
   }
-  return base + ((unit * size_t(n_slots) + size_t(slot)) * B + tok % B) * d;
+  return base + ((unit * size_t(n_slots) + size_t(slot)) * B + tok_offset(tok, B)) * d;
 }
 
 // Token of entry p of a unit's work list (-1: empty).  *bad turns true for
@@ -32,8 +32,8 @@ __device__ inline int list_token(const TokenList& L, size_t unit, int p, int n, 
     return t < 0 ? -1 : t;
   }
   if (L.kind == kListBlocks) {
-    const int blk = L.ids[unit * size_t(L.stride) + p / L.B];
-    const int t = blk * L.B + p % L.B;
+    const int blk = L.ids[unit * size_t(L.stride) + tok_block(p, L.B)];
+    const int t = blk * L.B + tok_offset(p, L.B);
     return blk < 0 || t >= n ? -1 : t;
   }
   return p < n ? p : -1;

@@ -158,8 +158,8 @@ __device__ inline void attn_gqa_mfma_body(
             if (!slot_map) {
               row = tok;
             } else {
-              const int slot = slot_map[size_t(unit) * m_max + tok / B];
-              if (slot >= 0 && slot < n_slots) row = slot * B + tok % B;
+              const int slot = slot_map[size_t(unit) * m_max + tok_block(tok, B)];
+              if (slot >= 0 && slot < n_slots) row = slot * B + tok_offset(tok, B);
               else set_error(err, 8u);
             }
           }

@@ -254,6 +254,12 @@ __device__ inline float key_float(uint32_t k) {
   return __uint_as_float(u);
 }
 
+// Block of a token position (or candidate slot) t >= 0 and its offset inside
+// the block, for the power-of-two block size B (the library supports B = 64):
+// a shift and a mask instead of an integer division by a runtime value.
+__device__ inline int tok_block(int t, int B) { return t >> __builtin_ctz(unsigned(B)); }
+__device__ inline int tok_offset(int t, int B) { return t & (B - 1); }
+
 // Device error word (first 4 bytes of the workspace).
 __device__ inline void set_error(uint32_t* err, uint32_t bit) {
   if (err) atomicOr(err, bit);

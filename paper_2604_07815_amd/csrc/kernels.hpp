@@ -27,7 +27,7 @@ constexpr int kTokenSlotsPerWG = 256;
 
 // Workspace carving (byte offsets from the workspace base, 256-aligned).
 struct Workspace {
-  size_t err, xfer, qpn, bscores, bids, logits, stats, keys, tids, po, plse, dkeys, dstats, total;
+  size_t err, xfer, qpn, bscores, bids, logits, stats, keys, kinfo, tids, po, plse, dkeys, dstats, total;
   int n_tchunks;  // token-score work-groups per unit
 };
 // Regions of the workspace, as a mask: a route of a call names the regions
@@ -72,9 +72,9 @@ hipError_t launch_token_score(const Problem& P, const void* q, const uint8_t* co
                               const int32_t* ctx_lens, float* logits, float* stats, int n_tchunks,
                               uint32_t* err, hipStream_t st);
 hipError_t launch_token_alpha(const Problem& P, const float* logits, const float* stats, int n_tchunks,
-                              const int32_t* block_ids, int K_b, const int32_t* ctx_lens, uint32_t* keys,
+                              const int32_t* block_ids, int K_b, const int32_t* ctx_lens, uint32_t* keys, uint32_t* kinfo,
                               hipStream_t st);
-hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32_t* block_ids, int K_b,
+hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const uint32_t* kinfo, const int32_t* block_ids, int K_b,
                              int K_t, int32_t* token_ids, float* token_scores, hipStream_t st);
 
 // One work-group per unit: (optional) block top-k from block_scores, then the

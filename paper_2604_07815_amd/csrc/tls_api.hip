@@ -121,10 +121,11 @@ hipError_t run_token_select(const Problem& P, const tls::Workspace& W, const voi
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[0], stream);
   e = tls::launch_token_alpha(P, at<float>(ws, W.logits), at<float>(ws, W.stats), W.n_tchunks, block_ids, K_b,
-                              ctx_lens, at<uint32_t>(ws, W.keys), stream);
+                              ctx_lens, at<uint32_t>(ws, W.keys), at<uint32_t>(ws, W.kinfo), stream);
   if (e != hipSuccess) return e;
   if (ev) (void)hipEventRecord(ev[1], stream);
-  return tls::launch_token_topk(P, at<uint32_t>(ws, W.keys), block_ids, K_b, K_t, token_ids, token_scores, stream);
+  return tls::launch_token_topk(P, at<uint32_t>(ws, W.keys), at<uint32_t>(ws, W.kinfo), block_ids, K_b, K_t,
+                                token_ids, token_scores, stream);
 }
 
 }  // namespace
@@ -151,6 +152,7 @@ Workspace plan_workspace(const Problem& P, int K_b, int K_t, unsigned regions, i
   take(&w.logits, kWsTokenSel, U * P.G * S * sizeof(float));
   take(&w.stats, kWsTokenSel, U * w.n_tchunks * P.G * 2 * sizeof(float));
   take(&w.keys, kWsTokenSel, U * S * sizeof(uint32_t));
+  take(&w.kinfo, kWsTokenSel, U * 2 * sizeof(uint32_t));  // per unit: valid candidates, key bound
   take(&w.tids, kWsTids, U * size_t(K_t) * sizeof(int32_t));
   take(&w.po, kWsSplit, U * ns * P.G * size_t(P.d_v) * sizeof(float));
   take(&w.plse, kWsSplit, U * ns * P.G * sizeof(float));

@@ -21,7 +21,7 @@ __device__ inline void unpack_nibbles8(uint32_t w, float* f) {
 // TLS_DEVERR_BLOCK_ID and are skipped.
 __device__ inline bool slot_token(const int32_t* bl, int K_b, int B, int m, int n, int slot, int* tok,
                                   uint32_t* err) {
-  const int i = slot / B, o = slot % B;
+  const int i = tok_block(slot, B), o = tok_offset(slot, B);
   if (i >= K_b) return false;
   const int blk = bl[i];
   if (blk < 0) return false;

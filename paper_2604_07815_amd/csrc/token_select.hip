@@ -332,11 +332,39 @@ __global__ __launch_bounds__(256) void token_score_mfma_kernel(
   }
 }
 
+// Work-group 0 of a unit's alpha kernel also writes the unit's number of
+// valid candidate slots and the key of a bound on every alpha key: with each
+// exponential <= 1, the alpha of a slot is at most (1/G) sum_h 1/Z_h summed
+// in the key loop's order (rounding is monotone), so the top-K_t kernel needs
+// no statistics pass of its own.  All 256 threads call it.
+__device__ inline void write_unit_info(const int32_t* bl, int K_b, int B, int m, int n, const float* s_iz, int G,
+                                       float invG, uint32_t* kinfo, int unit, uint32_t* s_cnt) {
+  uint32_t c = 0;
+  for (int i = threadIdx.x; i < K_b; i += 256) {
+    const int b = bl[i];
+    if (b >= 0 && b < m) c += uint32_t(min(B, n - b * B));
+  }
+  c = wave_reduce_bits(c, [](uint32_t a, uint32_t b) { return a + b; });
+  if ((threadIdx.x & 63) == 0) s_cnt[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float bsum = 0.f;
+    for (int h = 0; h < G; ++h) bsum = fmaf(1.0f, s_iz[h], bsum);
+    kinfo[2 * size_t(unit)] = s_cnt[0] + s_cnt[1] + s_cnt[2] + s_cnt[3];
+    kinfo[2 * size_t(unit) + 1] = __float_as_uint(fmaxf(bsum * invG, 0.f)) | 0x80000000u;
+  }
+}
+
+// The alpha key of a candidate: alpha >= +0 has the key bits | 2^31 (as
+// float_key); a NaN alpha (NaN inputs only) ranks as 0.
+__device__ inline uint32_t alpha_key(float a) { return __float_as_uint(fmaxf(a, 0.f)) | 0x80000000u; }
+
 __global__ __launch_bounds__(256) void token_alpha_kernel(
     const float* __restrict__ logits, const float* __restrict__ stats, int n_tchunks,
     const int32_t* __restrict__ block_ids, int K_b, const int32_t* __restrict__ ctx_lens, int H_kv, int G,
-    int B, int T, uint32_t* __restrict__ keys) {
+    int B, int T, uint32_t* __restrict__ keys, uint32_t* __restrict__ kinfo) {
   __shared__ float s_m[kMaxG], s_iz[kMaxG];
+  __shared__ uint32_t s_cnt[4];
   const int unit = blockIdx.y;
   const int s = unit / H_kv;
   int n = ctx_lens[s];
@@ -360,6 +388,7 @@ __global__ __launch_bounds__(256) void token_alpha_kernel(
   __syncthreads();
   const float invG = 1.0f / float(G);
   const int32_t* bl = block_ids + size_t(unit) * K_b;
+  if (blockIdx.x == 0) write_unit_info(bl, K_b, B, m, n, s_iz, G, invG, kinfo, unit, s_cnt);
   const float* lg = logits + size_t(unit) * G * S;
   for (int slot = blockIdx.x * 256 + threadIdx.x; slot < S; slot += gridDim.x * 256) {
     int tok;
@@ -367,7 +396,7 @@ __global__ __launch_bounds__(256) void token_alpha_kernel(
     if (slot_token(bl, K_b, B, m, n, slot, &tok, nullptr)) {
       float a = 0.f;
       for (int h = 0; h < G; ++h) a += __expf(lg[size_t(h) * S + slot] - s_m[h]) * s_iz[h];
-      key = float_key(a * invG);
+      key = alpha_key(a * invG);
     }
     keys[size_t(unit) * S + slot] = key;
   }
@@ -380,9 +409,10 @@ template <int G>
 __global__ __launch_bounds__(256) void token_alpha_kernel_g(
     const float* __restrict__ logits, const float* __restrict__ stats, int n_tchunks,
     const int32_t* __restrict__ block_ids, int K_b, const int32_t* __restrict__ ctx_lens, int H_kv, int B, int T,
-    uint32_t* __restrict__ keys) {
+    uint32_t* __restrict__ keys, uint32_t* __restrict__ kinfo) {
   constexpr int TPH = 256 / G;  // lanes per head (a power of two)
   __shared__ float s_m[G], s_iz[G];
+  __shared__ uint32_t s_cnt[4];
   const int unit = blockIdx.y, tid = threadIdx.x;
   const int s = unit / H_kv;
   int n = ctx_lens[s];
@@ -414,6 +444,7 @@ __global__ __launch_bounds__(256) void token_alpha_kernel_g(
   __syncthreads();
   const float invG = 1.0f / float(G);
   const int32_t* bl = block_ids + size_t(unit) * K_b;
+  if (blockIdx.x == 0) write_unit_info(bl, K_b, B, m, n, s_iz, G, invG, kinfo, unit, s_cnt);
   const float* lg = logits + size_t(unit) * G * S;
   for (int slot = blockIdx.x * 256 + tid; slot < S; slot += gridDim.x * 256) {
     int tok;
@@ -425,7 +456,7 @@ __global__ __launch_bounds__(256) void token_alpha_kernel_g(
       float a = 0.f;
 #pragma unroll
       for (int h = 0; h < G; ++h) a += __expf(v[h] - s_m[h]) * s_iz[h];
-      key = float_key(a * invG);
+      key = alpha_key(a * invG);
     }
     keys[size_t(unit) * S + slot] = key;
   }
@@ -436,6 +467,7 @@ __global__ __launch_bounds__(256) void token_alpha_kernel_g(
 // into registers.
 template <int EPT>
 __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __restrict__ keys,
+                                                           const uint32_t* __restrict__ kinfo,
                                                            const int32_t* __restrict__ block_ids, int K_b,
                                                            int B, int K_t, int32_t* __restrict__ token_ids,
                                                            float* __restrict__ token_scores) {
@@ -450,11 +482,16 @@ __global__ __launch_bounds__(1024) void token_topk_kernel(const uint32_t* __rest
     const int p = threadIdx.x + j * 1024;
     kr[j] = p < S ? keys[size_t(unit) * S + p] : kInvalidKey;
   }
+  // the valid count and the key bound from the alpha kernel; every valid key
+  // is >= the key of +0
+  const TopkKnown known{kinfo[2 * size_t(unit)], kinfo[2 * size_t(unit) + 1], 0x80000000u};
   for (int i = threadIdx.x; i < K_b; i += 1024) s_bl[i] = block_ids[size_t(unit) * K_b + i];
+  topk_prepare<1024>(scratch);
   __syncthreads();
-  wg_topk_regs<1024, EPT>(kr, K_t, token_ids + size_t(unit) * K_t, K_t,
-                          token_scores ? token_scores + size_t(unit) * K_t : nullptr,
-                          [=](int, int slot) { return int32_t(s_bl[slot / B] * B + slot % B); }, scratch);
+  wg_topk_regs<1024, EPT, true>(kr, K_t, token_ids + size_t(unit) * K_t, K_t,
+                                token_scores ? token_scores + size_t(unit) * K_t : nullptr,
+                                [=](int, int slot) { return int32_t(s_bl[tok_block(slot, B)] * B + tok_offset(slot, B)); }, scratch,
+                                &known);
 }
 
 template <int HT, int NGR>
@@ -491,30 +528,30 @@ hipError_t launch_token_score(const Problem& P, const void* q, const uint8_t* co
 
 hipError_t launch_token_alpha(const Problem& P, const float* logits, const float* stats, int n_tchunks,
                               const int32_t* block_ids, int K_b, const int32_t* ctx_lens, uint32_t* keys,
-                              hipStream_t st) {
+                              uint32_t* kinfo, hipStream_t st) {
   const int S = K_b * P.B;
   dim3 grid((S + 255) / 256, P.units);
   switch (P.G) {
-    case 4: token_alpha_kernel_g<4><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys); break;
-    case 8: token_alpha_kernel_g<8><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys); break;
-    case 16: token_alpha_kernel_g<16><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys); break;
-    case 32: token_alpha_kernel_g<32><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys); break;
+    case 4: token_alpha_kernel_g<4><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys, kinfo); break;
+    case 8: token_alpha_kernel_g<8><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys, kinfo); break;
+    case 16: token_alpha_kernel_g<16><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys, kinfo); break;
+    case 32: token_alpha_kernel_g<32><<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.B, P.T, keys, kinfo); break;
     default:
       token_alpha_kernel<<<grid, 256, 0, st>>>(logits, stats, n_tchunks, block_ids, K_b, ctx_lens, P.H_kv, P.G,
-                                               P.B, P.T, keys);
+                                               P.B, P.T, keys, kinfo);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const int32_t* block_ids, int K_b,
-                             int K_t, int32_t* token_ids, float* token_scores, hipStream_t st) {
+hipError_t launch_token_topk(const Problem& P, const uint32_t* keys, const uint32_t* kinfo, const int32_t* block_ids,
+                             int K_b, int K_t, int32_t* token_ids, float* token_scores, hipStream_t st) {
   const int S = K_b * P.B;
   const size_t lds = (topk_scratch_words(1024) + size_t(align4w(K_b))) * sizeof(uint32_t);
   const int ept = (S + 1023) / 1024;
   auto go = [&](auto kern) {
     const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), lds);
     if (e != hipSuccess) return e;
-    kern<<<P.units, 1024, lds, st>>>(keys, block_ids, K_b, P.B, K_t, token_ids, token_scores);
+    kern<<<P.units, 1024, lds, st>>>(keys, kinfo, block_ids, K_b, P.B, K_t, token_ids, token_scores);
     return hipGetLastError();
   };
   if (ept <= 1) return go(token_topk_kernel<1>);

@@ -120,7 +120,8 @@ __device__ __forceinline__ int2 topk_compact_tile(const uint32_t (&kr)[EPT], uin
                                                   uint32_t* cg, uint32_t* ce) {
   constexpr int NW = NT / 64;
   static_assert(NW % ((EPT * NW + 63) / 64) == 0, "keys per thread must keep NW a multiple of PER");
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: the lane reads below take it directly
   const bool ties = r > 0;  // uniform
 #pragma unroll
   for (int j = 0; j < EPT; ++j) {
@@ -178,9 +179,10 @@ __device__ __forceinline__ int2 topk_compact_tile(const uint32_t (&kr)[EPT], uin
       eb = ebase + __builtin_amdgcn_readlane(int(pe), src) + lanes_below(be);
     }
     if (g || (e && eb < r)) {
-      const int pos = gb + min(eb, r);
-      out[pos] = map(j, tid + j * NT);
-      if (out_scores) out_scores[pos] = key_float(key);
+      // (a 32-bit byte offset from the uniform base: pos >= 0)
+      const uint32_t off = uint32_t(gb + min(eb, r)) * 4u;
+      *reinterpret_cast<int32_t*>(reinterpret_cast<char*>(out) + off) = map(j, tid + j * NT);
+      if (out_scores) *reinterpret_cast<float*>(reinterpret_cast<char*>(out_scores) + off) = key_float(key);
     }
   }
   return make_int2(tot_g, tot_e);
