@@ -63,26 +63,23 @@ __device__ inline void token_select_mfma_body(
 
   // block scores (requested first: the longest dependency); every lane loads
   // from a clamped index, so that both requests leave before either is used
-  float bsv[kSelBPT];
+  float bsv[kSelBPT] = {};
   if (block_scores) {
     const float* sc = block_scores + size_t(unit) * m_max;
 #pragma unroll
     for (int j = 0; j < kSelBPT; ++j) bsv[j] = sc[min(tid + j * NT, m_max - 1)];
   }
   // q~ entries in slice order: entry (h, 4k + e) = q[h][C[8(k/2) + slice_chan(4(k%2) + e)]]
-  // (channel id, then the query element: two dependent requests, issued
-  // here and written to LDS only after the block top-k, which hides them)
-  uint16_t qv = 0;
-  if (tid < 4 * 32) {
-    const int h = tid >> 5, x = tid & 31;
-    if (h < G) {
-      const int k = x >> 2, e = x & 3;
-      int ch = channels[g * 32 + 8 * (k >> 1) + slice_chan(4 * (k & 1) + e)];
-      if (ch < 0 || ch >= d) {
-        set_error(err, 32u);
-        ch = 0;
-      }
-      qv = q[(size_t(s) * H_q + size_t(g) * G + h) * d + ch];
+  // (channel id, then the query element: two dependent requests; the
+  // element is written to LDS only after the block top-k, which hides it)
+  const bool qt_lane = tid < 4 * 32 && (tid >> 5) < G;
+  int ch = 0;
+  if (qt_lane) {
+    const int x = tid & 31, k = x >> 2, e = x & 3;
+    ch = channels[g * 32 + 8 * (k >> 1) + slice_chan(4 * (k & 1) + e)];
+    if (ch < 0 || ch >= d) {
+      set_error(err, 32u);
+      ch = 0;
     }
   }
   if (block_ids_in) {
@@ -97,10 +94,21 @@ __device__ inline void token_select_mfma_body(
       s_bl[i] = b < 0 ? -1 : b;
     }
   }
+  // the scores are consumed here on every path (not only inside the branches
+  // below), so that no later wait has to cover their loads
+#pragma unroll
+  for (int j = 0; j < kSelBPT; ++j) asm volatile("" : : "v"(bsv[j]));
+  uint32_t bk[kSelBPT];
   if (block_scores) {
-    uint32_t bk[kSelBPT];
 #pragma unroll
     for (int j = 0; j < kSelBPT; ++j) bk[j] = tid + j * NT < m ? float_key(bsv[j]) : kInvalidKey;
+  }
+  // the query elements are requested only now: every earlier request is
+  // consumed above, so no wait before the block top-k covers these
+  __builtin_amdgcn_sched_barrier(0);
+  uint16_t qv = 0;
+  if (qt_lane) qv = q[(size_t(s) * H_q + size_t(g) * G + (tid >> 5)) * d + ch];
+  if (block_scores) {
     int32_t* dst = block_ids_in ? block_ids_out + size_t(unit) * K_b : s_bl;
     wg_topk_regs<NT, kSelBPT>(bk, K_b, dst, K_b, nullptr, [](int, int i) { return int32_t(i); }, scratch);
   }
