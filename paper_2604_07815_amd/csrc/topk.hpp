@@ -50,7 +50,10 @@ __host__ __device__ constexpr int align4w(int words) { return (words + 3) & ~3; 
 // compaction then emits every key > T and the first r keys == T: per (key
 // slot j, wave) counts in position order (j-major, then wave, then lane) give
 // every key its output index with one barrier, so the output is ordered by
-// position without a sort.
+// position without a sort.  When all keys equal to T are taken (r equals
+// their count, the usual case) the compaction selects the keys > T - 1 and
+// needs one count per key.  SPREAD (with known bounds) replaces the first
+// pass by the spread pass described at kTopkSpreadShift.
 // The digit of one radix pass: the digit holding the remaining-th largest key
 // in play, the number of keys in play in higher digits, and its own count.
 struct TopkDigit {
