@@ -201,7 +201,12 @@ struct TopkKnown {
 
 // Spread first pass (wg_topk_regs<..., true>): bucket b of the first pass
 // holds the keys with key >> kTopkSpreadShift == base + b, base =
-// (hi >> kTopkSpreadShift) - 255, bucket 0 also every key below; for the
+// (hi >> kTopkSpreadShift) - 254, bucket 0 also every key below.  The
+// caller's hi bounds every key up to rounding (a sum of products of
+// exponentials <= 1, in the bound's own operation order); the bucket of
+// headroom above it (an eighth of an octave) keeps a key a few ulps above hi
+// in a bucket whose keys the next passes count, so the counts stay
+// consistent and the compaction never writes past the k-th output; for the
 // keys of non-negative floats (float_key) that is an eighth of an octave
 // per bucket over the 32 octaves below the upper bound, where the top-k of
 // softmax-like scores spreads over many buckets instead of the few that the
@@ -281,9 +286,9 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
     pmask = bits_left >= 32 ? 0u : ~((1u << bits_left) - 1u);
     prefix = kmx & pmask;
   }
-  if (SPREAD && kk > 0 && int(kmx >> kTopkSpreadShift) - int(kmn >> kTopkSpreadShift) > 255) {
+  if (SPREAD && kk > 0 && int(kmx >> kTopkSpreadShift) - int(kmn >> kTopkSpreadShift) > 254) {
     constexpr int fs = kTopkSpreadShift;
-    const int base = int(kmx >> fs) - 255;  // above kmn's bucket: bucket 0 is clamped
+    const int base = int(kmx >> fs) - 254;  // above kmn's bucket: bucket 0 is clamped
     uint32_t* h = hist;
     uint32_t* hc = h + (lane % kTopkHistCopies) * kTopkHistStride;
 #pragma unroll
