@@ -117,15 +117,15 @@ __device__ inline void topk_scan_pass(const uint32_t* h, int remaining, uint32_t
 // thread has returned.
 // r == 0 (no key equal to T is taken, the usual case, see wg_topk_regs)
 // needs one count per (slot, wave) and one prefix sum.
-template <int NT, int EPT, class Map>
-__device__ __forceinline__ int2 topk_compact_tile(const uint32_t (&kr)[EPT], uint32_t T, int r, int gbase,
+template <int NT, int EPT, bool TIES, class Map>
+__device__ __forceinline__ int2 topk_compact_impl(const uint32_t (&kr)[EPT], uint32_t T, int r, int gbase,
                                                   int ebase, int32_t* out, float* out_scores, Map map,
                                                   uint32_t* cg, uint32_t* ce) {
   constexpr int NW = NT / 64;
   static_assert(NW % ((EPT * NW + 63) / 64) == 0, "keys per thread must keep NW a multiple of PER");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: the lane reads below take it directly
-  const bool ties = r > 0;  // uniform
+  constexpr bool ties = TIES;
 #pragma unroll
   for (int j = 0; j < EPT; ++j) {
     const uint32_t key = kr[j];
@@ -189,6 +189,16 @@ __device__ __forceinline__ int2 topk_compact_tile(const uint32_t (&kr)[EPT], uin
     }
   }
   return make_int2(tot_g, tot_e);
+}
+
+// Two instances, so that the usual r == 0 case carries none of the tie
+// bookkeeping (r is uniform).
+template <int NT, int EPT, class Map>
+__device__ __forceinline__ int2 topk_compact_tile(const uint32_t (&kr)[EPT], uint32_t T, int r, int gbase,
+                                                  int ebase, int32_t* out, float* out_scores, Map map,
+                                                  uint32_t* cg, uint32_t* ce) {
+  if (r > 0) return topk_compact_impl<NT, EPT, true>(kr, T, r, gbase, ebase, out, out_scores, map, cg, ce);
+  return topk_compact_impl<NT, EPT, false>(kr, T, r, gbase, ebase, out, out_scores, map, cg, ce);
 }
 
 // Counts the caller already knows about its keys: the number of valid keys
