@@ -343,8 +343,13 @@ __device__ void wg_topk_regs(const uint32_t (&kr)[EPT], int k, int32_t* out, int
 #pragma unroll
     for (int j = 0; j < EPT; ++j) {
       const uint32_t key = kr[j];
+      // the digit as the 8 bits at `shift`: in a last pass narrower than 8
+      // bits (shift 0) the upper bits are prefix bits that every key in play
+      // shares, so the buckets keep their order and OR-ing the found digit
+      // into the prefix below changes nothing else (one v_bfe_u32 with an
+      // inline width)
       if (key != kInvalidKey && (key & pmask) == prefix && (!SPREAD || key <= cap))
-        atomicAdd(&hc[(key >> shift) & dmask], 1u);
+        atomicAdd(&hc[__builtin_amdgcn_ubfe(key, uint32_t(shift), 8u)], 1u);
     }
     __syncthreads();
     const TopkDigit dg = topk_scan_wave(h, remaining);
@@ -460,13 +465,14 @@ __device__ void wg_topk_global(const uint32_t* __restrict__ keys, int n, int k, 
 #pragma unroll
         for (int j = 0; j < EPT; ++j) {
           const uint32_t key = kr[j];
-          if (key != kInvalidKey && (key & pmask) == prefix) atomicAdd(&hc[(key >> shift) & dmask], 1u);
+          if (key != kInvalidKey && (key & pmask) == prefix)
+            atomicAdd(&hc[__builtin_amdgcn_ubfe(key, uint32_t(shift), 8u)], 1u);  // as in wg_topk_regs
         }
       }
     } else {
       for (int i = tid; i < list_n; i += NT) {
         const uint32_t key = list[i];
-        if ((key & pmask) == prefix) atomicAdd(&hc[(key >> shift) & dmask], 1u);
+        if ((key & pmask) == prefix) atomicAdd(&hc[__builtin_amdgcn_ubfe(key, uint32_t(shift), 8u)], 1u);
       }
     }
     __syncthreads();
