@@ -164,71 +164,79 @@ __global__ __launch_bounds__(256) void token_score_mfma_kernel(
   __shared__ __attribute__((aligned(16))) uint16_t s_qt[G * DC];
   __shared__ float s_qs[G * NGR];
   __shared__ float s_red[4][G][2];
-  __shared__ int s_ch[DC];
   const int unit = blockIdx.y, chunk = blockIdx.x;
   const int s = unit / H_kv, g = unit % H_kv;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int t16 = lane & 15, lg = lane >> 4;
-  int n = ctx_lens[s];
-  n = n < 0 ? 0 : (n > T ? T : n);
-  const int m = (n + B - 1) / B;
   const int S = K_b * B;
   const uint16_t* qg = q + (size_t(s) * H_q + size_t(g) * G) * d;
-  // the index rows of the four tiles' slots do not depend on q~: request them
-  // first, so their latency overlaps the q~ gather below
   const int32_t* bl = block_ids + size_t(unit) * K_b;
+  // Two rounds of requests, each with every load in flight at once (loads
+  // are unconditional at clamped addresses, so that none is sunk into a
+  // branch and waited for alone):
+  // 1. the context length, the block-list entries of the four tiles' slots
+  //    and the channel id of this thread's q~ position;
+  // 2. the q~ elements, then the tiles' index rows (so that the wait for q~
+  //    does not cover the rows).
+  // Thread t holds q~ entries t + 256 j: with 256 a multiple of DC they all
+  // lie at operand position x = t % DC, of heads j (256 / DC) + t / DC.
+  static_assert(256 % DC == 0 && G * DC % 256 == 0, "q~ entries per thread");
+  constexpr int PER = G * DC / 256;
+  const int x = tid % DC;
+  int n = ctx_lens[s];
+  int blk[4];
+#pragma unroll
+  for (int tl = 0; tl < 4; ++tl) {
+    const int slot = chunk * kTokenSlotsPerWG + w * 64 + tl * 16 + t16;
+    blk[tl] = bl[min(tok_block(min(slot, S - 1), B), K_b - 1)];
+  }
+  int ch;
+  {
+    const int e = x & 7;
+    ch = channels[g * DC + (x & ~7) + ((e & 3) << 1) + (e >> 2)];  // channel index of position x
+  }
+  n = n < 0 ? 0 : (n > T ? T : n);
+  const int m = (n + B - 1) / B;
+  if (ch < 0 || ch >= d) {
+    set_error(err, 32u);
+    ch = 0;
+  }
+  uint16_t qv[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) qv[j] = qg[size_t(j * (256 / DC) + tid / DC) * d + ch];
+  __builtin_amdgcn_sched_barrier(0);
   bool valid[4];
   uint32_t cx[4][NGR];
   float2 pqv[4][NGR];
 #pragma unroll
   for (int tl = 0; tl < 4; ++tl) {
     const int slot = chunk * kTokenSlotsPerWG + w * 64 + tl * 16 + t16;
-    int tok = 0;
-    valid[tl] = slot < S && slot_token(bl, K_b, B, m, n, slot, &tok, err);
-    const size_t row = size_t(unit) * T + tok;
+    const int b = blk[tl];
+    if (slot < S && b >= m) set_error(err, 2u);
+    const int tok = b * B + tok_offset(slot, B);
+    valid[tl] = slot < S && b >= 0 && b < m && tok < n;
+    const size_t row = size_t(unit) * T + (valid[tl] ? tok : 0);
 #pragma unroll
     for (int grp = 0; grp < NGR; ++grp) {
-      cx[tl][grp] = 0u;
-      pqv[tl][grp] = make_float2(0.f, 0.f);
-      if (valid[tl]) {
-        cx[tl][grp] = *reinterpret_cast<const uint32_t*>(codes + row * (DC / 2) + grp * 16 + lg * 4);
-        pqv[tl][grp] = *reinterpret_cast<const float2*>(qparams + (row * NGR + grp) * 2);
-      }
+      cx[tl][grp] = *reinterpret_cast<const uint32_t*>(codes + row * (DC / 2) + grp * 16 + lg * 4);
+      pqv[tl][grp] = *reinterpret_cast<const float2*>(qparams + (row * NGR + grp) * 2);
     }
   }
-  // the group's channel ids once (every head uses the same), then all of the
-  // work-group's q~ values requested together
-  if (tid < DC) {
-    int ch = channels[g * DC + tid];
-    if (ch < 0 || ch >= d) {
-      set_error(err, 32u);
-      ch = 0;
-    }
-    s_ch[tid] = ch;
+  __builtin_amdgcn_sched_barrier(0);
+  // q~ to LDS in operand order, and each (head, 32-channel group) sum over
+  // the 32 lanes that hold its positions (a 32-lane aligned half-wave): DPP
+  // sums inside each 16-lane row, then the two rows' sums exchanged
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    s_qt[tid + j * 256] = qv[j];
+    const uint32_t r16 = row16_reduce_bits(uint32_t(qv[j]) << 16, [](uint32_t u, uint32_t v) {
+      return __float_as_uint(__uint_as_float(u) + __uint_as_float(v));
+    });
+    const auto sw = __builtin_amdgcn_permlane16_swap(r16, r16, false, false);
+    if ((tid & 31) == 0)
+      s_qs[(j * (256 / DC) + tid / DC) * NGR + x / 32] = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
   }
   __syncthreads();
-  {
-    constexpr int PER = G * DC / 256;
-    static_assert(PER * 256 == G * DC, "q~ entries per thread");
-    uint16_t qv[PER];
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int i = tid + j * 256;
-      const int h = i / DC, x = i % DC;  // x = grp*32 + lg*8 + e (operand position)
-      const int e = x & 7;
-      const int c = (x & ~7) + ((e & 3) << 1) + (e >> 2);  // channel index of that position
-      qv[j] = qg[size_t(h) * d + s_ch[c]];
-    }
-#pragma unroll
-    for (int j = 0; j < PER; ++j) s_qt[tid + j * 256] = qv[j];
-  }
-  __syncthreads();
-  for (int i = tid; i < G * NGR; i += 256) {
-    const int h = i / NGR, grp = i % NGR;
-    float a = 0.f;
-    for (int x = 0; x < 32; ++x) a += __uint_as_float(uint32_t(s_qt[h * DC + grp * 32 + x]) << 16);
-    s_qs[i] = a;
-  }
   // A operands: head ht*16 + t16, channels of group grp at lane group lg
   ts_bf16x8_t qa[HT][NGR];
 #pragma unroll
@@ -236,7 +244,6 @@ __global__ __launch_bounds__(256) void token_score_mfma_kernel(
 #pragma unroll
     for (int grp = 0; grp < NGR; ++grp)
       qa[ht][grp] = *reinterpret_cast<const ts_bf16x8_t*>(&s_qt[(ht * 16 + t16) * DC + grp * 32 + lg * 8]);
-  __syncthreads();
   float qs[HT][4][NGR];  // heads ht*16 + 4lg + r
 #pragma unroll
   for (int ht = 0; ht < HT; ++ht)
