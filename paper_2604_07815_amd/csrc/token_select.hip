@@ -343,12 +343,15 @@ __global__ __launch_bounds__(256) void token_score_mfma_kernel(
 // valid candidate slots and the key of a bound on every alpha key: with each
 // exponential <= 1, the alpha of a slot is at most (1/G) sum_h 1/Z_h summed
 // in the key loop's order (rounding is monotone), so the top-K_t kernel needs
-// no statistics pass of its own.  All 256 threads call it.
-__device__ inline void write_unit_info(const int32_t* bl, int K_b, int B, int m, int n, const float* s_iz, int G,
-                                       float invG, uint32_t* kinfo, int unit, uint32_t* s_cnt) {
+// no statistics pass of its own.  All 256 threads call it; b_first is the
+// list entry bl[threadIdx.x] (any value where threadIdx.x >= K_b), requested
+// by the caller with its other loads.
+__device__ inline void write_unit_info(const int32_t* bl, int b_first, int K_b, int B, int m, int n,
+                                       const float* s_iz, int G, float invG, uint32_t* kinfo, int unit,
+                                       uint32_t* s_cnt) {
   uint32_t c = 0;
   for (int i = threadIdx.x; i < K_b; i += 256) {
-    const int b = bl[i];
+    const int b = i == int(threadIdx.x) ? b_first : bl[i];
     if (b >= 0 && b < m) c += uint32_t(min(B, n - b * B));
   }
   c = wave_reduce_bits(c, [](uint32_t a, uint32_t b) { return a + b; });
@@ -395,7 +398,8 @@ __global__ __launch_bounds__(256) void token_alpha_kernel(
   __syncthreads();
   const float invG = 1.0f / float(G);
   const int32_t* bl = block_ids + size_t(unit) * K_b;
-  if (blockIdx.x == 0) write_unit_info(bl, K_b, B, m, n, s_iz, G, invG, kinfo, unit, s_cnt);
+  if (blockIdx.x == 0)
+    write_unit_info(bl, threadIdx.x < K_b ? bl[threadIdx.x] : -1, K_b, B, m, n, s_iz, G, invG, kinfo, unit, s_cnt);
   const float* lg = logits + size_t(unit) * G * S;
   for (int slot = blockIdx.x * 256 + threadIdx.x; slot < S; slot += gridDim.x * 256) {
     int tok;
@@ -409,38 +413,64 @@ __global__ __launch_bounds__(256) void token_alpha_kernel(
   }
 }
 
-// token_alpha_kernel with the head count fixed at compile time: 256/G lanes
-// combine each head's work-group statistics, and the per-slot sum over heads
-// is unrolled into independent loads.
+// token_alpha_kernel with the head count fixed at compile time, for a grid
+// of one slot per thread: 256/G lanes combine each head's work-group
+// statistics, and every request of a work-group leaves at once before the
+// first is used (its lanes' statistics, the block-list entries of its slots
+// and of the unit information, the slots' G logits; unconditional loads at
+// clamped addresses), so the kernel waits for one memory round trip.
 template <int G>
 __global__ __launch_bounds__(256) void token_alpha_kernel_g(
     const float* __restrict__ logits, const float* __restrict__ stats, int n_tchunks,
     const int32_t* __restrict__ block_ids, int K_b, const int32_t* __restrict__ ctx_lens, int H_kv, int B, int T,
     uint32_t* __restrict__ keys, uint32_t* __restrict__ kinfo) {
   constexpr int TPH = 256 / G;  // lanes per head (a power of two)
+  constexpr int kC = 8;         // statistics chunks per lane requested together
   __shared__ float s_m[G], s_iz[G];
   __shared__ uint32_t s_cnt[4];
   const int unit = blockIdx.y, tid = threadIdx.x;
   const int s = unit / H_kv;
+  const int S = K_b * B;
+  const int h = tid / TPH, j = tid % TPH;
+  const float2* st = reinterpret_cast<const float2*>(stats) + size_t(unit) * n_tchunks * G;
+  const int32_t* bl = block_ids + size_t(unit) * K_b;
+  const float* lg = logits + size_t(unit) * G * S;
+  const int slot = blockIdx.x * 256 + tid, sl = min(slot, S - 1);
+  float2 sv[kC];
+#pragma unroll
+  for (int c = 0; c < kC; ++c) sv[c] = st[size_t(min(j + c * TPH, n_tchunks - 1)) * G + h];
+  __builtin_amdgcn_sched_barrier(0);
+  const int b_slot = bl[tok_block(sl, B)];
+  const int b_first = bl[min(tid, K_b - 1)];
+  float v[G];
+#pragma unroll
+  for (int hh = 0; hh < G; ++hh) v[hh] = lg[size_t(hh) * S + sl];
+  __builtin_amdgcn_sched_barrier(0);
   int n = ctx_lens[s];
   n = n < 0 ? 0 : (n > T ? T : n);
   const int m = (n + B - 1) / B;
-  const int S = K_b * B;
   {
-    const int h = tid / TPH, j = tid % TPH;
-    const float* st = stats + size_t(unit) * n_tchunks * G * 2;
+    // chunks j, j + TPH, ... in ascending order, then the lanes' tree (the
+    // requested entries are used through selects, not branches, so that
+    // no load is sunk into a branch; adding +0 leaves Z >= +0 unchanged)
     float M = -INFINITY;
-#pragma unroll 8
-    for (int c = j; c < n_tchunks; c += TPH) M = fmaxf(M, st[(c * G + h) * 2]);
+#pragma unroll
+    for (int c = 0; c < kC; ++c) M = fmaxf(M, j + c * TPH < n_tchunks ? sv[c].x : -INFINITY);
+    for (int c = j + kC * TPH; c < n_tchunks; c += TPH) M = fmaxf(M, st[size_t(c) * G + h].x);
 #pragma unroll
     for (int o = TPH / 2; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
     float Z = 0.f;
-    if (M != -INFINITY)
-#pragma unroll 8
-      for (int c = j; c < n_tchunks; c += TPH) {
-        const float mc = st[(c * G + h) * 2], zc = st[(c * G + h) * 2 + 1];
-        if (mc != -INFINITY) Z += zc * __expf(mc - M);
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int c = 0; c < kC; ++c) {
+        const bool ok = j + c * TPH < n_tchunks && sv[c].x != -INFINITY;
+        Z += ok ? sv[c].y * __expf(sv[c].x - M) : 0.f;
       }
+      for (int c = j + kC * TPH; c < n_tchunks; c += TPH) {
+        const float2 e = st[size_t(c) * G + h];
+        if (e.x != -INFINITY) Z += e.y * __expf(e.x - M);
+      }
+    }
 #pragma unroll
     for (int o = TPH / 2; o > 0; o >>= 1) Z += __shfl_xor(Z, o, 64);
     if (j == 0) {
@@ -450,19 +480,14 @@ __global__ __launch_bounds__(256) void token_alpha_kernel_g(
   }
   __syncthreads();
   const float invG = 1.0f / float(G);
-  const int32_t* bl = block_ids + size_t(unit) * K_b;
-  if (blockIdx.x == 0) write_unit_info(bl, K_b, B, m, n, s_iz, G, invG, kinfo, unit, s_cnt);
-  const float* lg = logits + size_t(unit) * G * S;
-  for (int slot = blockIdx.x * 256 + tid; slot < S; slot += gridDim.x * 256) {
-    int tok;
+  if (blockIdx.x == 0) write_unit_info(bl, b_first, K_b, B, m, n, s_iz, G, invG, kinfo, unit, s_cnt);
+  if (slot < S) {
+    const int t = b_slot * B + tok_offset(slot, B);
     uint32_t key = kInvalidKey;
-    if (slot_token(bl, K_b, B, m, n, slot, &tok, nullptr)) {
-      float v[G];
-#pragma unroll
-      for (int h = 0; h < G; ++h) v[h] = lg[size_t(h) * S + slot];
+    if (b_slot >= 0 && b_slot < m && t < n) {
       float a = 0.f;
 #pragma unroll
-      for (int h = 0; h < G; ++h) a += __expf(v[h] - s_m[h]) * s_iz[h];
+      for (int hh = 0; hh < G; ++hh) a += __expf(v[hh] - s_m[hh]) * s_iz[hh];
       key = alpha_key(a * invG);
     }
     keys[size_t(unit) * S + slot] = key;
