@@ -125,3 +125,45 @@ def test_capacity_limits(k_b, k_t):
     with pytest.raises(tls.TlsError) as e:
         tls.tls_workspace_size(c.layout, k_b + 1 if k_b == 192 else 193, k_t)
     assert e.value.status == 2
+
+
+@pytest.mark.parametrize("name,over", [
+    # the MLA route: matrix-core scoring over many work-groups, alpha, top-K_t
+    ("mla", dict(batch=2, ctx_lo=3000, ctx_hi=3000, clusters=2, k_b=13, k_t=300, seed=4101)),
+    # the fused bf16 GQA selection (whole blocks per wave)
+    ("qwen3_gqa_48k", dict(ctx_lo=3000, ctx_hi=3000, clusters=2, k_b=13, k_t=300, seed=4102)),
+    # fp32 GQA: the vector-unit scoring kernel
+    ("toy", dict(ctx_lo=3000, ctx_hi=3000, k_b=13, k_t=300, seed=4103)),
+])
+def test_given_blocks_with_empty_and_out_of_range_entries(name, over):
+    """Token selection from a given block list (Sec. 4.1 fine stage) whose
+    entries include -1 (empty), ids at and past the block count (skipped
+    with TLS_DEVERR_BLOCK_ID) and the context's partial last block; with
+    K_b = 13 the candidate count is not a multiple of a work-group's slots.
+    Tokens against the oracle's selection from the valid blocks, then the
+    output against the oracle's attention over the GPU's tokens."""
+    import paper_2604_07815_amd as tls
+    cfg = synth.config(name).replace(**over)
+    c = H.Case(cfg, backend="host").build_index()
+    n = 3000
+    m = -(-n // cfg.block)
+    rng = np.random.default_rng(cfg.seed)
+    ids = np.full((cfg.batch, cfg.h_kv, cfg.k_b), -1, dtype=np.int32)
+    valid = {}
+    for (s, g) in c.units():
+        v = np.append(np.sort(rng.choice(m - 1, 9, replace=False)), m - 1).astype(np.int32)
+        valid[(s, g)] = v
+        ids[s, g] = [v[0], v[1], v[2], -1, v[3], v[4], v[5], m, v[6], v[7], v[8], v[9], m + 5]
+    r = c.decode(block_ids_in=torch.from_numpy(ids).cuda())
+    flags = tls.tls_check_device_error(r["ws"], clear=True)
+    assert flags & tls.DEVERR_BLOCK_ID
+    assert (flags & ~tls.DEVERR_BLOCK_ID) == 0
+    G = cfg.group
+    for (s, g) in c.units():
+        ref = c.oracle_unit(s, g, block_ids=valid[(s, g)])
+        H.check_selection(r["tids"][s, g].cpu().numpy(), ref["token_ids"], H.alpha_lookup(ref),
+                          f"tokens unit {(s, g)}")
+        S = H.valid_ids(r["tids"][s, g].cpu().numpy())
+        ref_s = c.oracle_unit(s, g, token_ids=S)
+        H.check_close(r["out"][s, g * G:(g + 1) * G].float().cpu().numpy(), ref_s["out"], cfg.dtype, "out")
+        H.check_close(r["lse"][s, g * G:(g + 1) * G].cpu().numpy(), ref_s["lse"], cfg.dtype, "lse")
