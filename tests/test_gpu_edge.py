@@ -167,3 +167,31 @@ def test_given_blocks_with_empty_and_out_of_range_entries(name, over):
         ref_s = c.oracle_unit(s, g, token_ids=S)
         H.check_close(r["out"][s, g * G:(g + 1) * G].float().cpu().numpy(), ref_s["out"], cfg.dtype, "out")
         H.check_close(r["lse"][s, g * G:(g + 1) * G].cpu().numpy(), ref_s["lse"], cfg.dtype, "lse")
+
+
+@pytest.mark.parametrize("name,over", [
+    ("mla", dict(batch=2, ctx_lo=2500, ctx_hi=2500, clusters=2, k_b=8, k_t=200, seed=4104)),
+    ("qwen3_gqa_48k", dict(ctx_lo=2500, ctx_hi=2500, clusters=2, k_b=8, k_t=200, seed=4105)),
+    ("toy", dict(ctx_lo=2500, ctx_hi=2500, k_b=8, k_t=200, seed=4106)),
+])
+def test_out_of_range_channel_reads_channel_zero(name, over):
+    """A channel id outside [0, d_qk) in C (Sec. 4.1 channel projection):
+    the index build and the token scoring both read channel 0 at that
+    position and the decode reports TLS_DEVERR_CHANNEL; the whole step then
+    equals the oracle run with channel 0 in that position."""
+    import paper_2604_07815_amd as tls
+    cfg = synth.config(name).replace(**over)
+    c = H.Case(cfg, backend="host")
+    bad = c.ch_host.copy()
+    bad[:, 5] = cfg.d_qk + 3
+    bad[0, 17] = -2
+    c.ch = torch.from_numpy(bad).cuda()
+    fixed = c.ch_host.copy()
+    fixed[:, 5] = 0
+    fixed[0, 17] = 0
+    c.ch_host = fixed
+    c.build_index()
+    r = c.decode()
+    assert tls.tls_check_device_error(r["ws"], clear=True) == tls.DEVERR_CHANNEL
+    for (s, g) in c.units():
+        H.compare_unit(c, r, s, g)
